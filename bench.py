@@ -1,0 +1,344 @@
+"""Benchmark: one step = one full pass of the SAGA-NN hot path of a 2-layer
+GCN on the 2^21-vertex R-MAT graph (50 edges per vertex + self-loops,
+106,954,752 stored edges, features 602 -> 128 -> 41):
+
+    graph layout (plan: degrees, degree order, segments, row blocks)
+    layer 1: ApplyVertex-pre  Z1 = d_out^-1/2 (X W1)          (MFMA GEMM)
+             Scatter+ApplyEdge+Gather+ApplyVertex-post
+                              H1 = ReLU(d_in^-1/2 sum Z1_u + b1)
+    layer 2: Z2 = d_out^-1/2 (H1 W2);  Y = d_in^-1/2 sum Z2_u + b2
+
+Inputs are resident in HBM before the timed region.  ``value`` is layer
+throughput in edges/s: (stored edges x 2 layers) / step time.  Prints one
+JSON line (rank 0, one GPU).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM = 8.0e12          # bytes/s
+PEAK_MFMA = {"f32": 157.3e12, "bf16": 2516.6e12}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def src_sha(name):
+    p = os.path.join(ROOT, "paper_2009_00804_amd", "csrc", name)
+    with open(p, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(kernel, dtype):
+    """Per-launch HBM bytes of `kernel` from the counter summary in
+    profiles/, if it was taken on the current kernel source."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        with open(p) as f:
+            rec = json.load(f)
+        e = rec.get(f"{kernel}:{dtype}")
+        if not e or e.get("src_sha") != src_sha(e["source"]):
+            return None
+        return e["bytes_per_launch"]
+    except Exception:
+        return None
+
+
+class Step:
+    """Preallocated buffers and the op-level call sequence of one step."""
+
+    def __init__(self, g, dtype, dev):
+        import torch
+
+        import paper_2009_00804_amd.saga as S
+
+        self.S = S
+        self.torch = torch
+        self.dtype = dtype
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        self.tdt = tdt
+        f_in, hid, f_out = g["dims"]
+        self.dims = g["dims"]
+        self.V = g["num_vertices"]
+        self.E = g["num_edges"]
+        self.rp = torch.from_numpy(g["row_ptr"]).to(dev)
+        self.col = torch.from_numpy(g["col_idx"]).to(dev)
+        if dtype == "f32":
+            self.X = torch.from_numpy(g["X"]).to(dev)[:, :f_in]
+            W1, W2 = g["W1"], g["W2"]
+        else:
+            self.X = torch.from_numpy(g["X_bf16"].view("int16")).view(torch.bfloat16).to(dev)[:, :f_in]
+            W1, W2 = g["W1_bf"], g["W2_bf"]
+        self.W1 = torch.from_numpy(W1).to(dev).to(tdt)
+        self.W2 = torch.from_numpy(W2).to(dev).to(tdt)
+        self.b1 = torch.from_numpy(g["b1"]).to(dev)
+        self.b2 = torch.from_numpy(g["b2"]).to(dev)
+        es = 4 if dtype == "f32" else 2
+        al = 16 // es
+        ld = lambda c: (c + al - 1) // al * al  # noqa: E731
+        self.Z1 = torch.empty((self.V, ld(hid)), dtype=tdt, device=dev)[:, :hid]
+        self.H1 = torch.empty((self.V, ld(hid)), dtype=tdt, device=dev)[:, :hid]
+        self.Z2 = torch.empty((self.V, ld(f_out)), dtype=tdt, device=dev)[:, :f_out]
+        self.Y = torch.empty((self.V, ld(f_out)), dtype=tdt, device=dev)[:, :f_out]
+        self.graph = S.Graph(self.rp, self.col)     # allocates + builds + checks once
+        self.plan_ws = self.graph.ws
+        p = self.graph.plan
+        op = S.saga_edge_op()
+        self.op1 = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SUM, S.dtype_code(tdt), 1, 0, 1, 0.0,
+                                  S.SAGA_ACT_RELU)
+        self.op2 = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SUM, S.dtype_code(tdt), 1, 0, 1, 0.0,
+                                  S.SAGA_ACT_NONE)
+        del op
+        n1 = S.saga_gather_workspace_size(p, self.op1, hid)
+        n2 = S.saga_gather_workspace_size(p, self.op2, f_out)
+        self.gws = S.workspace(max(n1, n2), dev)
+        self.gop = S.saga_gemm_op(S.dtype_code(tdt), S.SAGA_GEMM_PLAIN, S.SAGA_ACT_NONE, p.d_out)
+        self.none = S.saga_cmat(None, 0, 0, 0)
+        self.in1 = S.saga_edge_inputs()
+        self.in1.src = S.cmat(self.Z1)
+        self.in1.bias = self.b1.data_ptr()
+        self.in2 = S.saga_edge_inputs()
+        self.in2.src = S.cmat(self.Z2)
+        self.in2.bias = self.b2.data_ptr()
+        self.stream = torch.cuda.current_stream()
+        self.sh = S.stream_handle(self.stream)
+        self.names = ["plan", "gemm1", "gather1", "gemm2", "gather2"]
+        self.ev = None
+
+    def run(self, events=None):
+        S = self.S
+        g = self.graph
+        ev = events
+        if ev:
+            ev[0].record(self.stream)
+        S.saga_plan_build(g.num_dst, g.num_src, g.num_edges, C.c_void_p(self.rp.data_ptr()),
+                          C.c_void_p(self.col.data_ptr()), g.opts, C.c_void_p(self.plan_ws.data_ptr()),
+                          self.plan_ws.numel(), self.sh)
+        if ev:
+            ev[1].record(self.stream)
+        p = g.plan
+        S.saga_apply_vertex(self.gop, S.cmat(self.X), S.cmat(self.W1), self.none, self.none, None,
+                            None, S.mat(self.Z1), self.sh)
+        if ev:
+            ev[2].record(self.stream)
+        S.saga_scatter_apply_edge_gather(p, self.op1, self.in1, S.mat(self.H1),
+                                         C.c_void_p(self.gws.data_ptr()), self.gws.numel(), self.sh)
+        if ev:
+            ev[3].record(self.stream)
+        S.saga_apply_vertex(self.gop, S.cmat(self.H1), S.cmat(self.W2), self.none, self.none, None,
+                            None, S.mat(self.Z2), self.sh)
+        if ev:
+            ev[4].record(self.stream)
+        S.saga_scatter_apply_edge_gather(p, self.op2, self.in2, S.mat(self.Y),
+                                         C.c_void_p(self.gws.data_ptr()), self.gws.numel(), self.sh)
+        if ev:
+            ev[5].record(self.stream)
+
+
+def algorithmic(step, stage):
+    """Algorithmic work of one launch of a stage: (bytes, flops).
+
+    Gather: compulsory bytes -- every CSR index once (4 B/edge), row_ptr,
+    the source matrix once and the output once (each unique byte once).
+    GEMM: flops 2 M K N; bytes = A + W + output once."""
+    V, E = step.V, step.E
+    f_in, hid, f_out = step.dims
+    es = 4 if step.dtype == "f32" else 2
+    if stage == "gather1":
+        return E * 4 + (V + 1) * 4 + 2 * V * hid * es, 2 * E * hid
+    if stage == "gather2":
+        return E * 4 + (V + 1) * 4 + 2 * V * f_out * es, 2 * E * f_out
+    if stage == "gemm1":
+        return V * f_in * es + f_in * hid * es + V * hid * es, 2 * V * f_in * hid
+    if stage == "gemm2":
+        return V * hid * es + hid * f_out * es + V * f_out * es, 2 * V * hid * f_out
+    return (V + 1) * 4 + E * 4 + 3 * V * 4, 0
+
+
+def noreuse_bytes(step, stage):
+    """Bytes the gather moves through the memory hierarchy if no source row
+    were reused from cache: per edge the index and the full source row."""
+    V, E = step.V, step.E
+    f_in, hid, f_out = step.dims
+    es = 4 if step.dtype == "f32" else 2
+    F = hid if stage == "gather1" else f_out
+    row = (F * es + 15) // 16 * 16
+    return E * (4 + row) + (V + 1) * 4 + V * F * es
+
+
+def time_step(step, steps, warmup):
+    torch = step.torch
+    for _ in range(warmup):
+        step.run()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        step.run(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = {n: [] for n in step.names}
+    tot = []
+    for e in evs:
+        for i, n in enumerate(step.names):
+            per[n].append(e[i].elapsed_time(e[i + 1]))
+        tot.append(e[0].elapsed_time(e[5]))
+    return wall, per, tot
+
+
+def cpu_baseline(g, budget_s=12.0):
+    """The oracle's layer-1 GCN (aggregate-first, float64) on a bounded random
+    sample of destination rows of the same workload, one thread."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import saga_oracle as O
+
+    f_in = g["dims"][0]
+    X = g["X"][:, :f_in]
+    rp = g["row_ptr"].astype(np.int64)
+    rng = np.random.default_rng(7)
+    V = g["num_vertices"]
+    # degrees once, outside the timed region (the oracle recomputes them per
+    # call otherwise); the per-row Gather and the transform are timed
+    d_out = O.out_degrees(g["col_idx"], V)
+    s_out = O.degree_scale(d_out)
+    s_in = O.degree_scale(np.diff(rp))
+    edges = 0
+    rows_done = 0
+    t = 0.0
+    with threadpool_limits(1):
+        while t < budget_s and rows_done < 400000:
+            rows = rng.integers(0, V, 2000)
+            t0 = time.perf_counter()
+            agg = O.gather(rp, g["col_idx"], X, "sum", rows=rows, src_scale=s_out)
+            agg = agg * s_in[rows][:, None]
+            O.dense(agg, g["W1"], bias=g["b1"], act="relu")
+            t += time.perf_counter() - t0
+            edges += int((rp[rows + 1] - rp[rows]).sum())
+            rows_done += len(rows)
+    return dict(value=edges / t, unit="edges/s", cores=1, kind="oracle",
+                sample=f"layer-1 GCN (602->128, aggregate-first, float64) on {rows_done} random "
+                       f"destination rows ({edges} in-edges) of the same graph; {t:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--dtype", choices=["f32", "bf16"], default="f32")
+    ap.add_argument("--variants", default="bf16", help="extra dtypes to time (comma list or '')")
+    ap.add_argument("--scale", type=int, default=21)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(sharding is a design note); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from synth import configs as Cfg
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    g = Cfg.build("gcn_rmat", scale=args.scale)
+    dtypes = [args.dtype] + [d for d in args.variants.split(",") if d and d != args.dtype]
+    if "bf16" in dtypes:
+        Cfg.add_bf16_variant(g)
+    log(f"inputs: V={g['num_vertices']} E={g['num_edges']} in {time.time() - t0:.1f}s")
+
+    results = {}
+    for dt in dtypes:
+        step = Step(g, dt, dev)
+        counts = step.graph.counts
+        wall, per, tot = time_step(step, args.steps, args.warmup)
+        ms = wall * 1e3 / args.steps
+        med = {n: statistics.median(v) for n, v in per.items()}
+        mean = {n: statistics.fmean(v) for n, v in per.items()}
+        results[dt] = dict(step=step, ms=ms, med=med, mean=mean, counts=counts,
+                           ev_ms=statistics.median(tot))
+        log(f"{dt}: {ms:.3f} ms/step (events {statistics.median(tot):.3f}); "
+            + ", ".join(f"{n} {med[n]:.3f}" for n in step.names))
+        if dt != args.dtype:
+            del step
+            results[dt]["step"] = None
+            torch.cuda.empty_cache()
+
+    r = results[args.dtype]
+    step = r["step"]
+    E, V = step.E, step.V
+    value = 2 * E / (r["ms"] * 1e-3)
+    # dominant kernel of the step
+    stages = ["gemm1", "gather1", "gemm2", "gather2"]
+    dom = max(stages, key=lambda n: r["mean"][n])
+    byts, flops = algorithmic(step, dom)
+    dur = r["mean"][dom] * 1e-3
+    kernel_name = {"gather1": "k_gather_simple", "gather2": "k_gather_simple",
+                   "gemm1": "k_gemm", "gemm2": "k_gemm"}[dom]
+    if dom.startswith("gemm") and args.dtype == "f32":
+        roof = dict(bound="mfma", achieved=flops / dur / 1e12, peak=PEAK_MFMA["f32"] / 1e12,
+                    unit="TFLOP/s")
+    else:
+        roof = dict(bound="hbm", achieved=byts / dur / 1e9, peak=PEAK_HBM / 1e9, unit="GB/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = load_traffic(f"{dom}", args.dtype)
+    roof["kernel"] = f"{dom} ({kernel_name})"
+    roof["algorithmic"] = ("compulsory bytes: 4 B per CSR index + row_ptr + source matrix "
+                           "and output once" if roof["bound"] == "hbm" else "2 M K N flops")
+    stage_ms = {n: round(r["mean"][n], 4) for n in step.names}
+    out = {
+        "metric": "GNN layer throughput: edges/s (GTEPS) + achieved HBM GB/s fraction, 1 MI355X",
+        "value": value,
+        "unit": "edges/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": r["ms"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic (seeded R-MAT + N(0,1) features, random-init Glorot weights)",
+        "config": {"workload": "2-layer GCN, R-MAT scale 21 (a,b,c=0.57,0.19,0.19), 50 edges/vertex "
+                               "+ self-loops, features 602->128->41",
+                   "vertices": V, "edges": E, "layers": 2, "parallelism": "single GPU"},
+        "gteps": value / 1e9,
+        "vertices_per_s": 2 * V / (r["ms"] * 1e-3),
+        "stage_ms": stage_ms,
+        "gather1_noreuse_GBps": noreuse_bytes(step, "gather1") / (r["mean"]["gather1"] * 1e-3) / 1e9,
+        "gemm1_TFLOPs": algorithmic(step, "gemm1")[1] / (r["mean"]["gemm1"] * 1e-3) / 1e12,
+        "plan": {"segments": r["counts"].num_segments, "blocks": r["counts"].num_blocks,
+                 "split_rows": r["counts"].n_split, "max_in_degree": r["counts"].max_in_degree},
+        "roofline": roof,
+    }
+    for dt in dtypes[1:]:
+        rr = results[dt]
+        out.setdefault("variants", {})[dt] = {
+            "value": 2 * E / (rr["ms"] * 1e-3), "ms_per_step": rr["ms"],
+            "stage_ms": {n: round(rr["mean"][n], 4) for n in rr["mean"]}}
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(g, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,334 @@
+/*
+ * saga.h -- SAGA-NN message-passing layer for AMD Instinct MI355X (gfx950).
+ *
+ * A GNN layer takes the graph (an adjacency matrix), the vertex embedding
+ * matrix and optionally an edge embedding matrix, and produces the next
+ * layer's embeddings (Zhang et al., "Architectural Implications of Graph
+ * Neural Networks", IEEE CAL 2020, Sec. 2 "Model Survey").  It is
+ * decomposed into four stages -- Scatter, ApplyEdge, Gather, ApplyVertex
+ * (Sec. 2 "Model Decomposition"; the GGNN walk-through of Fig. 2).  This
+ * library runs that layer on one GPU:
+ *
+ *   saga_plan_build                 graph layout: degrees, degree-sorted row
+ *                                   order, row segments and row blocks
+ *   saga_scatter_apply_edge_gather  fused Scatter + ApplyEdge + Gather: a
+ *                                   per-destination segment reduction over
+ *                                   the in-CSR (the fused Gather is the
+ *                                   sparse adjacency x embedding product,
+ *                                   Sec. 3.2 "Gather", Fig. 7b)
+ *   saga_apply_vertex               dense per-vertex transform on the matrix
+ *                                   cores, with fused epilogues (Sec. 3.2
+ *                                   "ApplyVertex", Table III)
+ *   saga_layer                      one whole layer of a Table I model
+ *
+ * Conventions (all entry points):
+ *   - Every pointer argument except the host-side structs (saga_plan_opts,
+ *     saga_plan, saga_edge_op, saga_edge_inputs, saga_gemm_op,
+ *     saga_layer_desc) is a DEVICE pointer.  The caller allocates, owns and
+ *     frees all device memory; the library allocates nothing, ever.  Scratch
+ *     space comes from a caller-provided workspace whose size the matching
+ *     *_workspace_size call reports.
+ *   - Matrices are row-major.  `ld` is the leading dimension in ELEMENTS.
+ *     Feature matrices must have a 16-byte-aligned base and ld*elem_size a
+ *     multiple of 16 bytes; columns [cols, ld) are never read as data and
+ *     never written.
+ *   - float32 ("f32") or bfloat16 ("bf16") storage; accumulation is always
+ *     float32.  Biases, attention vectors, gate weights and degree scalings
+ *     are float32.
+ *   - All work is enqueued on `stream` (a hipStream_t; NULL = the null
+ *     stream) and is asynchronous.  The returned status covers argument
+ *     validation and kernel launch only; no call blocks except
+ *     saga_plan_check.
+ *   - Outputs must not overlap any input (checked on address ranges;
+ *     SAGA_EINVAL).  Every output row is written, including rows with no
+ *     in-edges.
+ *   - Results are deterministic: the same inputs give byte-identical outputs
+ *     from run to run (no floating-point atomics).
+ *   - Functions never throw, abort or print.  On error they return a status
+ *     and saga_last_error() gives a detail string (thread-local).
+ */
+#ifndef SAGA_H
+#define SAGA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum saga_status {
+  SAGA_OK = 0,
+  SAGA_EINVAL = 1,        /* bad argument: null, size, alignment, ld, overlap */
+  SAGA_EGRAPH = 2,        /* CSR arrays violate the CSR rules */
+  SAGA_EUNSUPPORTED = 3,  /* valid but not supported combination */
+  SAGA_EDEVICE = 4,       /* HIP runtime error */
+  SAGA_EWORKSPACE = 5,    /* workspace missing or too small */
+  SAGA_EINTERNAL = 6
+} saga_status;
+
+typedef enum saga_dtype { SAGA_F32 = 0, SAGA_BF16 = 1 } saga_dtype;
+
+/* Gather reductions (Table I "Gather" column; the simple sum/mean/max
+ * reductions and the attention reduction of Sec. 2 "Survey Result"). */
+typedef enum saga_reduce {
+  SAGA_RED_SUM = 0,
+  SAGA_RED_MEAN = 1,     /* sum / d_in(v) */
+  SAGA_RED_MAX = 2,      /* elementwise maximum */
+  SAGA_RED_SOFTMAX = 3   /* attention: per-destination softmax-weighted sum */
+} saga_reduce;
+
+/* Scatter + ApplyEdge message kinds (Table I "Scatter"/"ApplyEdge"). */
+typedef enum saga_msg {
+  SAGA_MSG_COPY = 0,      /* message of edge u->v = src row u              */
+  SAGA_MSG_SRC_NORM = 1,  /* src row u * d_out(u)^-1/2  (GCN normalisation) */
+  SAGA_MSG_GAT = 2,       /* score LeakyReLU(el[u,k] + er[v,k]); SOFTMAX only */
+  SAGA_MSG_GATED = 3      /* sigmoid(gs[u] + gd[v] + b_e + e_uv W_ee) * src[u] */
+} saga_msg;
+
+typedef enum saga_act {
+  SAGA_ACT_NONE = 0,
+  SAGA_ACT_RELU = 1,     /* x > 0 ? x : +0 */
+  SAGA_ACT_ELU = 2,      /* x > 0 ? x : exp(x) - 1 */
+  SAGA_ACT_SIGMOID = 3,
+  SAGA_ACT_TANH = 4
+} saga_act;
+
+/* A device matrix view.  ptr == NULL means "absent" where an input is
+ * optional. */
+typedef struct saga_cmat { const void* ptr; int64_t rows, cols, ld; } saga_cmat;
+typedef struct saga_mat { void* ptr; int64_t rows, cols, ld; } saga_mat;
+
+/* ======================================================================
+ * Graph layout (plan)
+ * ======================================================================
+ *
+ * The graph is a destination-major CSR ("in-CSR"): row v of the adjacency
+ * lists the sources of v's in-edges (the edge-to-vertex adjacency of
+ * Sec. 3.2 "Gather", where a nonzero is an in-edge of the row's vertex).
+ * row_ptr is int32[num_dst + 1], col_idx is int32[num_edges]; multi-edges
+ * and self-loops are allowed and count once per copy.
+ *
+ * The plan holds, on the device:
+ *   d_in[v]  = row_ptr[v+1] - row_ptr[v]                    (int32[num_dst])
+ *   d_out[u] = number of entries of col_idx equal to u      (int32[num_src])
+ *   perm     = rows sorted by d_in descending, then id ascending (power-law
+ *              degree skew, Sec. 3.2 / Fig. 8a)              (int32[num_dst])
+ *   segments: each row, taken in perm order, is cut into pieces of at most
+ *              seg_len edges (a row with d_in <= seg_len, or an empty row,
+ *              is one piece).  Segment s covers CSR entries
+ *              [seg_beg[s], seg_end[s]) of row seg_row[s]; the segments of
+ *              perm position i are row_seg_first[i] .. row_seg_first[i+1]-1.
+ *              Rows with d_in > seg_len ("split rows") are perm positions
+ *              0 .. n_split-1 and own segments 0 .. s_split-1.
+ *   blocks:   segment s costs (seg_end - seg_beg) + row_cost; with P(s) the
+ *              total cost of the segments before s, block b holds the
+ *              segments with floor(P(s) / block_cost) == b;
+ *              block_ptr[b] = its first segment, block_ptr[num_blocks] = S.
+ * All of it is integer and reproducible bit for bit.
+ */
+typedef struct saga_plan_opts {
+  int32_t seg_len;     /* > 0; default 512 */
+  int32_t block_cost;  /* >= seg_len + row_cost; default 4096 */
+  int32_t row_cost;    /* >= 1; default 4 */
+} saga_plan_opts;
+
+/* Filled by saga_plan_build.  Plain data: copy it freely; it stays valid as
+ * long as the workspace and the caller's CSR arrays live. */
+typedef struct saga_plan {
+  int32_t num_dst, num_src;
+  int64_t num_edges;
+  const int32_t* row_ptr;   /* the caller's arrays, referenced not copied */
+  const int32_t* col_idx;
+  int32_t seg_len, block_cost, row_cost;
+  int64_t max_segments;     /* capacity of the segment arrays */
+  int64_t max_blocks;       /* capacity of block_ptr (minus one) */
+  int64_t max_split;        /* upper bound on split rows */
+  int64_t max_split_segments;
+  /* device arrays inside the workspace */
+  int32_t* d_in;
+  int32_t* d_out;
+  int32_t* perm;
+  int32_t* row_seg_first;   /* [num_dst + 1] */
+  int32_t* seg_row;         /* [max_segments] */
+  int32_t* seg_beg;
+  int32_t* seg_end;
+  int32_t* block_ptr;       /* [max_blocks + 1] */
+  int32_t* counts;          /* [8]: see saga_plan_counts */
+  void* scratch;            /* sort / scan temporaries */
+  size_t scratch_bytes;
+} saga_plan;
+
+typedef struct saga_plan_counts {
+  int64_t num_segments;
+  int64_t num_blocks;
+  int64_t n_split;          /* rows with d_in > seg_len */
+  int64_t s_split;          /* segments owned by split rows */
+  int32_t error_flags;      /* bit 0: row_ptr[0] != 0, bit 1: row_ptr not
+                               non-decreasing, bit 2: row_ptr[num_dst] !=
+                               num_edges, bit 3: col_idx out of range */
+  int32_t max_in_degree;
+} saga_plan_counts;
+
+/* Bytes of workspace saga_plan_build needs for this graph size.
+ * Errors: SAGA_EINVAL on null `bytes`, negative sizes, num_edges >= 2^31,
+ * or invalid options (opts may be NULL for the defaults). */
+saga_status saga_plan_workspace_size(int32_t num_dst, int32_t num_src, int64_t num_edges,
+                                     const saga_plan_opts* opts, size_t* bytes);
+
+/* Build the plan of a device-resident in-CSR on `stream`.  The CSR arrays
+ * are read, validated on the device and referenced by the plan (they must
+ * stay alive and unchanged while the plan is used).  `workspace` (device,
+ * 256-byte aligned, caller-owned) receives every plan array.  Returns after
+ * enqueuing; an invalid CSR is reported by saga_plan_check, and every later
+ * kernel that uses a plan whose validation failed leaves its outputs
+ * unwritten instead of reading out of bounds.
+ * Errors: SAGA_EINVAL (null pointers, sizes, options, alignment),
+ * SAGA_EWORKSPACE (too small), SAGA_EDEVICE (launch failure). */
+saga_status saga_plan_build(int32_t num_dst, int32_t num_src, int64_t num_edges,
+                            const int32_t* row_ptr, const int32_t* col_idx,
+                            const saga_plan_opts* opts, void* workspace,
+                            size_t workspace_bytes, void* stream, saga_plan* plan);
+
+/* Synchronise `stream` and read the plan's counters.  Returns SAGA_EGRAPH
+ * if the device validation found a CSR error (details in counts->error_flags
+ * and saga_last_error), SAGA_EDEVICE if the stream reported a fault. */
+saga_status saga_plan_check(const saga_plan* plan, void* stream, saga_plan_counts* counts);
+
+/* ======================================================================
+ * Scatter + ApplyEdge + Gather (fused)
+ * ======================================================================
+ * For every destination v, reduce the messages of its in-edges (Sec. 3.2
+ * "Scatter", "ApplyEdge", "Gather"; Table I), then apply the epilogue
+ *     out[v] = act(post(agg_v) + bias)
+ * where post() is:  SUM/MAX: agg (times d_in(v)^-1/2 if dst_norm);
+ * MEAN: agg / d_in(v); SOFTMAX: the per-head weighted sum, heads
+ * concatenated (head_mean = 0) or averaged (head_mean = 1).  A row with no
+ * in-edges has agg = 0.  No E x F edge tensor is ever materialised.
+ *
+ * Inputs by message kind (feature width F = src.cols):
+ *   COPY, SRC_NORM: src  (num_src x F, f32 or bf16)
+ *   GAT:   src = z (num_src x F, f32), el (num_src x heads), er (num_dst x
+ *          heads), F % heads == 0, F/heads a multiple of 4; score of edge
+ *          u->v for head k is LeakyReLU(el[u,k] + er[v,k], neg_slope).
+ *   GATED: src = h (num_src x F, f32), gate_src (num_src x F), gate_dst
+ *          (num_dst x F), edge_feat (num_edges x Fe, row e = CSR entry e),
+ *          w_edge (Fe x F, dense), gate_bias (F); message of edge e = u->v
+ *          is sigmoid(gate_src[u] + gate_dst[v] + gate_bias +
+ *          edge_feat[e] w_edge) * h[u] elementwise.  F == 64, Fe <= 16.
+ * Output: num_dst x F (x F/heads if head_mean), same dtype as src.
+ * Supported: COPY/SRC_NORM with SUM/MEAN/MAX in f32 and bf16, GAT with
+ * SOFTMAX in f32, GATED with SUM in f32; others give SAGA_EUNSUPPORTED.
+ */
+typedef struct saga_edge_op {
+  saga_msg msg;
+  saga_reduce reduce;
+  saga_dtype dtype;
+  int32_t heads;       /* GAT: number of heads; else ignored */
+  int32_t head_mean;   /* GAT: 1 = average over heads */
+  int32_t dst_norm;    /* 1 = multiply SUM/MAX aggregate by d_in(v)^-1/2 */
+  float neg_slope;     /* GAT LeakyReLU slope (0.2 in GAT) */
+  saga_act act;
+} saga_edge_op;
+
+typedef struct saga_edge_inputs {
+  saga_cmat src;
+  saga_cmat el, er;                /* GAT (4-byte aligned) */
+  saga_cmat gate_src, gate_dst;    /* GATED */
+  saga_cmat edge_feat;             /* GATED */
+  const float* w_edge;             /* GATED */
+  const float* gate_bias;          /* GATED, nullable */
+  const float* bias;               /* nullable, length = output cols */
+} saga_edge_inputs;
+
+saga_status saga_gather_workspace_size(const saga_plan* plan, const saga_edge_op* op,
+                                       int64_t feat, size_t* bytes);
+
+saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edge_op* op,
+                                           const saga_edge_inputs* in, saga_mat out,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* stream);
+
+/* ======================================================================
+ * ApplyVertex: dense transform on the matrix cores
+ * ======================================================================
+ * Sec. 3.2 "ApplyVertex" (all vertices batched into one GEMM), Table III.
+ * mode PLAIN:  out = act(rs * (a w) + bias)
+ * mode CONCAT: out = act(rs * (a w + a2 w2) + bias)   ([a | a2] [w ; w2])
+ * mode GRU:    GRU cell with input a and hidden state a2 (Fig. 2, GGNN):
+ *              gi = a w + bias, gh = a2 w2 + bias2 (column blocks r, z, n of
+ *              width F = a2.cols), r = s(gi_r + gh_r), z = s(gi_z + gh_z),
+ *              n = tanh(gi_n + r * gh_n), out = (1 - z) n + z a2.
+ * rs = row_scale_deg ? (deg[i] > 0 ? deg[i]^-1/2 : 0) : 1  (row i).
+ * a: M x K, w: K x N (dense weights, ld may exceed N), out: M x N; bf16 or
+ * f32 storage per op->dtype, float32 accumulation; N <= 256 per call.
+ */
+typedef enum saga_gemm_mode { SAGA_GEMM_PLAIN = 0, SAGA_GEMM_CONCAT = 1, SAGA_GEMM_GRU = 2 } saga_gemm_mode;
+
+typedef struct saga_gemm_op {
+  saga_dtype dtype;
+  saga_gemm_mode mode;
+  saga_act act;                   /* PLAIN / CONCAT */
+  const int32_t* row_scale_deg;   /* nullable, int32[M] */
+} saga_gemm_op;
+
+saga_status saga_apply_vertex(const saga_gemm_op* op, saga_cmat a, saga_cmat w,
+                              saga_cmat a2, saga_cmat w2, const float* bias,
+                              const float* bias2, saga_mat out, void* stream);
+
+/* ======================================================================
+ * One whole layer (Table I models)
+ * ======================================================================
+ * GCN       out = act(d_in^-1/2 A d_out^-1/2 X W + b), evaluated
+ *           transform-first: Z = d_out^-1/2 (X W) on the matrix cores, then
+ *           the fused sum-Gather with d_in^-1/2, bias and act.
+ * GAT       [z | el | er] = X [W | W a_l | W a_r], softmax Gather, then
+ *           act(concat + b) or mean over heads + b.
+ * SAGE_POOL P = ReLU(X W_pool + b_pool); A = max-Gather of P;
+ *           out = [X | A] W + b   (W is 2 F_in x F_out).
+ * GATED_GRU [S_src, S_dst] = X [W_e,src, W_e,dst]; gated sum-Gather with
+ *           W_e,edge and b_e; out = GRU(a, X) with W_ih, W_hh, b_ih, b_hh.
+ *           (W_e rows: [0,F) src part, [F,2F) dst part, [2F,2F+Fe) edge.)
+ * Weights are dense device matrices (ld = cols) in the layer dtype; biases
+ * and attention vectors f32.  x: num_src x F_in (num_src == num_dst).
+ */
+typedef enum saga_layer_kind {
+  SAGA_LAYER_GCN = 0,
+  SAGA_LAYER_GAT = 1,
+  SAGA_LAYER_SAGE_POOL = 2,
+  SAGA_LAYER_GATED_GRU = 3
+} saga_layer_kind;
+
+typedef struct saga_layer_desc {
+  saga_layer_kind kind;
+  saga_dtype dtype;
+  int32_t in_feat, out_feat;
+  int32_t heads, head_mean;       /* GAT */
+  float neg_slope;                /* GAT */
+  saga_act act;                   /* GCN, GAT */
+  int32_t edge_feat;              /* GATED_GRU: Fe */
+  const void* w;  const float* b;             /* GCN, GAT, SAGE_POOL */
+  const void* w_pool; const float* b_pool;    /* SAGE_POOL */
+  const float* attn_l; const float* attn_r;   /* GAT: heads x (F/heads) */
+  const float* w_e; const float* b_e;         /* GATED_GRU: (2F + Fe) x F, F */
+  const float* w_ih; const float* b_ih;       /* GATED_GRU: F x 3F, 3F */
+  const float* w_hh; const float* b_hh;
+} saga_layer_desc;
+
+saga_status saga_layer_workspace_size(const saga_plan* plan, const saga_layer_desc* desc,
+                                      size_t* bytes);
+
+saga_status saga_layer(const saga_plan* plan, const saga_layer_desc* desc, saga_cmat x,
+                       saga_cmat edge_feat, saga_mat out, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* ====================================================================== */
+const char* saga_status_str(saga_status s);
+const char* saga_last_error(void);
+/* Library version string. */
+const char* saga_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SAGA_H */

@@ -1,0 +1,736 @@
+// C-ABI entry points: argument validation, workspace carving and dispatch
+// to the kernel launchers; whole-layer composition of the Table I models.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <exception>
+
+#include "saga.h"
+#include "saga_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+saga_status fail(saga_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+saga_status ok() {
+  g_err[0] = 0;
+  return SAGA_OK;
+}
+
+saga_status dev_fail(hipError_t e, const char* where) {
+  return fail(SAGA_EDEVICE, "%s: %s", where, hipGetErrorString(e));
+}
+
+inline size_t esize(saga_dtype t) { return t == SAGA_BF16 ? 2 : 4; }
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+bool range_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+size_t mat_bytes(int64_t rows, int64_t cols, int64_t ld, size_t es) {
+  if (rows <= 0 || cols <= 0) return 0;
+  return ((size_t)(rows - 1) * (size_t)ld + (size_t)cols) * es;
+}
+
+// a feature matrix: rows x cols, ld >= cols, 16-byte base and row pitch
+saga_status check_mat(const void* ptr, int64_t rows, int64_t cols, int64_t ld, int64_t want_rows,
+                      int64_t want_cols, size_t es, bool vec, const char* name) {
+  if (rows != want_rows || cols != want_cols)
+    return fail(SAGA_EINVAL, "%s: shape %lld x %lld, expected %lld x %lld", name, (long long)rows,
+                (long long)cols, (long long)want_rows, (long long)want_cols);
+  if (ld < cols) return fail(SAGA_EINVAL, "%s: ld %lld < cols %lld", name, (long long)ld, (long long)cols);
+  if (rows > 0 && cols > 0 && !ptr) return fail(SAGA_EINVAL, "%s: null pointer", name);
+  if (vec) {
+    if ((uintptr_t)ptr % 16 != 0) return fail(SAGA_EINVAL, "%s: base not 16-byte aligned", name);
+    if (((size_t)ld * es) % 16 != 0)
+      return fail(SAGA_EINVAL, "%s: row pitch ld*elem = %zu not a multiple of 16", name, (size_t)ld * es);
+  } else if ((uintptr_t)ptr % es != 0) {
+    return fail(SAGA_EINVAL, "%s: misaligned base", name);
+  }
+  return SAGA_OK;
+}
+
+saga_status resolve_opts(const saga_plan_opts* o, int32_t* T, int32_t* B, int32_t* c) {
+  *T = o && o->seg_len ? o->seg_len : 512;
+  *c = o && o->row_cost ? o->row_cost : 4;
+  *B = o && o->block_cost ? o->block_cost : 4096;
+  if (*T <= 0 || *c <= 0) return fail(SAGA_EINVAL, "plan options: seg_len and row_cost must be > 0");
+  if (*B < *T + *c) return fail(SAGA_EINVAL, "plan options: block_cost must be >= seg_len + row_cost");
+  return SAGA_OK;
+}
+
+saga_status check_plan(const saga_plan* p) {
+  if (!p) return fail(SAGA_EINVAL, "plan is null");
+  if (!p->counts || !p->d_in || !p->perm || !p->seg_row || !p->block_ptr)
+    return fail(SAGA_EINVAL, "plan is not built");
+  return SAGA_OK;
+}
+
+// bump allocator over a caller workspace
+struct Carve {
+  char* base;
+  size_t cap, used = 0;
+  Carve(void* b, size_t c) : base(static_cast<char*>(b)), cap(c) {}
+  void* take(size_t n) {
+    void* p = base ? base + used : nullptr;
+    used = align256(used + n);
+    return p;
+  }
+  bool fits() const { return used <= cap; }
+};
+
+saga::GatherArgs gather_args_from_plan(const saga_plan& p) {
+  saga::GatherArgs a;
+  memset(&a, 0, sizeof(a));
+  a.row_ptr = p.row_ptr;
+  a.col_idx = p.col_idx;
+  a.d_in = p.d_in;
+  a.d_out = p.d_out;
+  a.perm = p.perm;
+  a.row_seg_first = p.row_seg_first;
+  a.seg_row = p.seg_row;
+  a.seg_beg = p.seg_beg;
+  a.seg_end = p.seg_end;
+  a.block_ptr = p.block_ptr;
+  a.counts = p.counts;
+  a.max_blocks = p.max_blocks;
+  a.max_split = p.max_split;
+  return a;
+}
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+saga_status gather_ws_bytes(const saga_plan& p, const saga_edge_op& op, int64_t feat,
+                            size_t* bytes) {
+  const size_t ps = saga::gather_partial_stride(op, feat);
+  *bytes = align256((size_t)p.max_split_segments * ps * sizeof(float));
+  return SAGA_OK;
+}
+
+saga_status validate_edge_op(const saga_plan& p, const saga_edge_op& op,
+                             const saga_edge_inputs& in, const saga_mat& out) {
+  const size_t es = esize(op.dtype);
+  const int64_t F = in.src.cols;
+  if (op.dtype != SAGA_F32 && op.dtype != SAGA_BF16) return fail(SAGA_EINVAL, "bad dtype");
+  if (op.act < SAGA_ACT_NONE || op.act > SAGA_ACT_TANH) return fail(SAGA_EINVAL, "bad activation");
+  if (F <= 0) return fail(SAGA_EINVAL, "src: no feature columns");
+  if (F > (op.dtype == SAGA_BF16 ? 1024 : 512))
+    return fail(SAGA_EUNSUPPORTED, "feature width %lld too large", (long long)F);
+  saga_status s = check_mat(in.src.ptr, in.src.rows, in.src.cols, in.src.ld, p.num_src, F, es, true, "src");
+  if (s) return s;
+  int64_t out_cols = F;
+  switch (op.msg) {
+    case SAGA_MSG_COPY:
+    case SAGA_MSG_SRC_NORM:
+      if (op.reduce != SAGA_RED_SUM && op.reduce != SAGA_RED_MEAN && op.reduce != SAGA_RED_MAX)
+        return fail(SAGA_EUNSUPPORTED, "COPY/SRC_NORM messages take SUM, MEAN or MAX");
+      break;
+    case SAGA_MSG_GAT: {
+      if (op.reduce != SAGA_RED_SOFTMAX) return fail(SAGA_EUNSUPPORTED, "GAT messages need SOFTMAX");
+      if (op.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "GAT gather is float32 only");
+      const int64_t H = op.heads;
+      if (H <= 0 || F % H != 0 || (F / H) % 4 != 0 || F / 4 > 64)
+        return fail(SAGA_EUNSUPPORTED, "GAT: heads must divide F into multiples of 4 (F <= 256)");
+      if (op.head_mean && (!is_pow2(H) || !is_pow2(F / 4)))
+        return fail(SAGA_EUNSUPPORTED, "GAT head mean needs power-of-two heads and F/4");
+      s = check_mat(in.el.ptr, in.el.rows, in.el.cols, in.el.ld, p.num_src, H, 4, false, "el");
+      if (s) return s;
+      s = check_mat(in.er.ptr, in.er.rows, in.er.cols, in.er.ld, p.num_dst, H, 4, false, "er");
+      if (s) return s;
+      if (op.head_mean) out_cols = F / H;
+      break;
+    }
+    case SAGA_MSG_GATED: {
+      if (op.reduce != SAGA_RED_SUM) return fail(SAGA_EUNSUPPORTED, "GATED messages need SUM");
+      if (op.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "GATED gather is float32 only");
+      if (F != 64) return fail(SAGA_EUNSUPPORTED, "GATED gather needs F == 64");
+      const int64_t Fe = in.edge_feat.cols;
+      if (Fe <= 0 || Fe > 16 || Fe % 4 != 0)
+        return fail(SAGA_EUNSUPPORTED, "GATED: edge feature width must be 4, 8, 12 or 16");
+      s = check_mat(in.gate_src.ptr, in.gate_src.rows, in.gate_src.cols, in.gate_src.ld, p.num_src, F, 4, true, "gate_src");
+      if (s) return s;
+      s = check_mat(in.gate_dst.ptr, in.gate_dst.rows, in.gate_dst.cols, in.gate_dst.ld, p.num_dst, F, 4, true, "gate_dst");
+      if (s) return s;
+      s = check_mat(in.edge_feat.ptr, in.edge_feat.rows, in.edge_feat.cols, in.edge_feat.ld, p.num_edges, Fe, 4, true, "edge_feat");
+      if (s) return s;
+      if (!in.w_edge) return fail(SAGA_EINVAL, "w_edge is null");
+      break;
+    }
+    default:
+      return fail(SAGA_EINVAL, "bad message kind");
+  }
+  s = check_mat(out.ptr, out.rows, out.cols, out.ld, p.num_dst, out_cols, es, true, "out");
+  if (s) return s;
+  const size_t ob = mat_bytes(out.rows, out.cols, out.ld, es);
+  const void* ins[] = {in.src.ptr, in.el.ptr, in.er.ptr, in.gate_src.ptr, in.gate_dst.ptr,
+                       in.edge_feat.ptr, p.row_ptr, p.col_idx};
+  const size_t inb[] = {mat_bytes(in.src.rows, in.src.cols, in.src.ld, es),
+                        mat_bytes(in.el.rows, in.el.cols, in.el.ld, 4),
+                        mat_bytes(in.er.rows, in.er.cols, in.er.ld, 4),
+                        mat_bytes(in.gate_src.rows, in.gate_src.cols, in.gate_src.ld, 4),
+                        mat_bytes(in.gate_dst.rows, in.gate_dst.cols, in.gate_dst.ld, 4),
+                        mat_bytes(in.edge_feat.rows, in.edge_feat.cols, in.edge_feat.ld, 4),
+                        (size_t)(p.num_dst + 1) * 4, (size_t)p.num_edges * 4};
+  for (int i = 0; i < 8; ++i)
+    if (range_overlap(out.ptr, ob, ins[i], inb[i])) return fail(SAGA_EINVAL, "output overlaps an input");
+  return SAGA_OK;
+}
+
+saga_status run_gather(const saga_plan& p, const saga_edge_op& op, const saga_edge_inputs& in,
+                       const saga_mat& out, void* ws, size_t ws_bytes, hipStream_t st) {
+  saga_status s = validate_edge_op(p, op, in, out);
+  if (s) return s;
+  size_t need;
+  gather_ws_bytes(p, op, in.src.cols, &need);
+  if (p.max_split_segments > 0 && (!ws || ws_bytes < need))
+    return fail(SAGA_EWORKSPACE, "gather workspace: need %zu bytes, got %zu", need, ws_bytes);
+  if (p.num_dst == 0) return ok();
+  saga::GatherArgs a = gather_args_from_plan(p);
+  a.msg = op.msg;
+  a.reduce = op.reduce;
+  a.dtype = op.dtype;
+  a.heads = op.msg == SAGA_MSG_GAT ? op.heads : 1;
+  a.head_mean = op.msg == SAGA_MSG_GAT ? op.head_mean : 0;
+  a.dst_norm = op.dst_norm;
+  a.act = op.act;
+  a.neg_slope = op.neg_slope;
+  a.feat = (int)in.src.cols;
+  a.out_cols = (int)out.cols;
+  a.src = in.src.ptr;
+  a.ld_src = in.src.ld;
+  a.el = static_cast<const float*>(in.el.ptr);
+  a.ld_el = in.el.ld;
+  a.er = static_cast<const float*>(in.er.ptr);
+  a.ld_er = in.er.ld;
+  a.gsrc = static_cast<const float*>(in.gate_src.ptr);
+  a.ld_gsrc = in.gate_src.ld;
+  a.gdst = static_cast<const float*>(in.gate_dst.ptr);
+  a.ld_gdst = in.gate_dst.ld;
+  a.efeat = static_cast<const float*>(in.edge_feat.ptr);
+  a.ld_efeat = in.edge_feat.ld;
+  a.fe = (int)in.edge_feat.cols;
+  a.w_edge = in.w_edge;
+  a.gate_bias = in.gate_bias;
+  a.bias = in.bias;
+  a.out = out.ptr;
+  a.ld_out = out.ld;
+  a.partial = static_cast<float*>(ws);
+  a.pstride = (int64_t)saga::gather_partial_stride(op, in.src.cols);
+  a.pcols = saga::gather_partial_cols(in.src.cols);
+  hipError_t e = saga::launch_gather(a, st);
+  if (e != hipSuccess) return dev_fail(e, "gather launch");
+  return ok();
+}
+
+saga_status validate_gemm(const saga_gemm_op& op, const saga_cmat& a, const saga_cmat& w,
+                          const saga_cmat& a2, const saga_cmat& w2, const saga_mat& out) {
+  if (op.dtype != SAGA_F32 && op.dtype != SAGA_BF16) return fail(SAGA_EINVAL, "bad dtype");
+  if (op.mode < SAGA_GEMM_PLAIN || op.mode > SAGA_GEMM_GRU) return fail(SAGA_EINVAL, "bad mode");
+  if (op.act < SAGA_ACT_NONE || op.act > SAGA_ACT_TANH) return fail(SAGA_EINVAL, "bad activation");
+  const size_t es = esize(op.dtype);
+  const int64_t M = a.rows, K = a.cols, N = w.cols;
+  if (M < 0 || K <= 0 || N <= 0) return fail(SAGA_EINVAL, "gemm: empty operand");
+  saga_status s = check_mat(a.ptr, a.rows, a.cols, a.ld, M, K, es, true, "a");
+  if (s) return s;
+  s = check_mat(w.ptr, w.rows, w.cols, w.ld, K, N, es, false, "w");
+  if (s) return s;
+  if (op.mode != SAGA_GEMM_PLAIN) {
+    s = check_mat(a2.ptr, a2.rows, a2.cols, a2.ld, M, a2.cols, es, true, "a2");
+    if (s) return s;
+    if (a2.cols <= 0) return fail(SAGA_EINVAL, "a2: no columns");
+    s = check_mat(w2.ptr, w2.rows, w2.cols, w2.ld, a2.cols, N, es, false, "w2");
+    if (s) return s;
+  }
+  int64_t out_cols = N;
+  if (op.mode == SAGA_GEMM_GRU) {
+    if (N % 3 != 0) return fail(SAGA_EINVAL, "GRU: w must have 3F columns");
+    out_cols = N / 3;
+    if (out_cols != 16 && out_cols != 32 && out_cols != 48 && out_cols != 64)
+      return fail(SAGA_EUNSUPPORTED, "GRU: F must be 16, 32, 48 or 64");
+    if (a2.cols != out_cols) return fail(SAGA_EINVAL, "GRU: hidden state a2 must have F columns");
+  } else if (N > 4096) {
+    return fail(SAGA_EUNSUPPORTED, "gemm: N too large");
+  }
+  s = check_mat(out.ptr, out.rows, out.cols, out.ld, M, out_cols, es, false, "out");
+  if (s) return s;
+  const size_t ob = mat_bytes(out.rows, out.cols, out.ld, es);
+  if (range_overlap(out.ptr, ob, a.ptr, mat_bytes(a.rows, a.cols, a.ld, es)) ||
+      range_overlap(out.ptr, ob, w.ptr, mat_bytes(w.rows, w.cols, w.ld, es)) ||
+      range_overlap(out.ptr, ob, a2.ptr, mat_bytes(a2.rows, a2.cols, a2.ld, es)) ||
+      range_overlap(out.ptr, ob, w2.ptr, mat_bytes(w2.rows, w2.cols, w2.ld, es)))
+    return fail(SAGA_EINVAL, "output overlaps an input");
+  return SAGA_OK;
+}
+
+saga_status run_gemm(const saga_gemm_op& op, const saga_cmat& a, const saga_cmat& w,
+                     const saga_cmat& a2, const saga_cmat& w2, const float* bias,
+                     const float* bias2, const saga_mat& out, hipStream_t st) {
+  saga_status s = validate_gemm(op, a, w, a2, w2, out);
+  if (s) return s;
+  saga::GemmArgs g;
+  memset(&g, 0, sizeof(g));
+  g.dtype = op.dtype;
+  g.mode = op.mode;
+  g.act = op.act;
+  g.M = a.rows;
+  g.N = w.cols;
+  g.K = a.cols;
+  g.K2 = a2.cols;
+  g.a = a.ptr;
+  g.lda = a.ld;
+  g.w = w.ptr;
+  g.ldw = w.ld;
+  g.a2 = a2.ptr;
+  g.lda2 = a2.ld;
+  g.w2 = w2.ptr;
+  g.ldw2 = w2.ld;
+  g.bias = bias;
+  g.bias2 = bias2;
+  g.row_scale_deg = op.row_scale_deg;
+  g.out = out.ptr;
+  g.ldo = out.ld;
+  hipError_t e = saga::launch_gemm(g, st);
+  if (e != hipSuccess) return dev_fail(e, "gemm launch");
+  return ok();
+}
+
+// -------------------------------------------------------------------------
+// layers
+// -------------------------------------------------------------------------
+struct LayerPlanWs {
+  size_t bytes;
+};
+
+int64_t ld_for(int64_t cols, saga_dtype t) { return round_up(cols, t == SAGA_BF16 ? 8 : 4); }
+
+saga_status layer_check_desc(const saga_plan& p, const saga_layer_desc& d) {
+  if (p.num_dst != p.num_src) return fail(SAGA_EINVAL, "layers need num_src == num_dst");
+  if (d.in_feat <= 0 || d.out_feat <= 0) return fail(SAGA_EINVAL, "layer feature sizes must be > 0");
+  if (d.dtype != SAGA_F32 && d.dtype != SAGA_BF16) return fail(SAGA_EINVAL, "bad dtype");
+  switch (d.kind) {
+    case SAGA_LAYER_GCN:
+      if (!d.w) return fail(SAGA_EINVAL, "GCN: w is null");
+      break;
+    case SAGA_LAYER_GAT:
+      if (d.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "GAT layer is float32 only");
+      if (!d.w || !d.attn_l || !d.attn_r) return fail(SAGA_EINVAL, "GAT: null weights");
+      if (d.heads <= 0) return fail(SAGA_EINVAL, "GAT: heads must be > 0");
+      break;
+    case SAGA_LAYER_SAGE_POOL:
+      if (d.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "SAGE layer is float32 only");
+      if (!d.w || !d.w_pool) return fail(SAGA_EINVAL, "SAGE: null weights");
+      break;
+    case SAGA_LAYER_GATED_GRU:
+      if (d.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "gated layer is float32 only");
+      if (!d.w_e || !d.w_ih || !d.w_hh) return fail(SAGA_EINVAL, "gated: null weights");
+      if (d.in_feat != d.out_feat) return fail(SAGA_EINVAL, "gated: in_feat must equal out_feat");
+      break;
+    default:
+      return fail(SAGA_EINVAL, "bad layer kind");
+  }
+  return SAGA_OK;
+}
+
+// returns workspace bytes; with a non-null base, also carves the buffers
+struct LayerBufs {
+  void* z = nullptr; int64_t ldz = 0;      // GCN Z / GAT [z|el|er] / SAGE P / gated S_src
+  void* z2 = nullptr; int64_t ldz2 = 0;    // SAGE A / gated S_dst / GCN agg (aggregate-first)
+  void* z3 = nullptr; int64_t ldz3 = 0;    // gated a
+  float* wext = nullptr; int64_t ldw = 0;  // GAT folded weights
+  void* part = nullptr;
+  size_t part_bytes = 0;
+};
+
+bool gcn_transform_first(const saga_layer_desc& d) { return d.out_feat <= d.in_feat; }
+
+size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, LayerBufs* b) {
+  Carve c(base, (size_t)-1);
+  const int64_t V = p.num_dst;
+  const saga_dtype t = d.dtype;
+  const size_t es = esize(t);
+  saga_edge_op op;
+  memset(&op, 0, sizeof(op));
+  int64_t gfeat = d.out_feat;
+  switch (d.kind) {
+    case SAGA_LAYER_GCN:
+      if (gcn_transform_first(d)) {
+        b->ldz = ld_for(d.out_feat, t);
+        b->z = c.take((size_t)V * b->ldz * es);
+        gfeat = d.out_feat;
+      } else {
+        b->ldz2 = ld_for(d.in_feat, t);
+        b->z2 = c.take((size_t)V * b->ldz2 * es);
+        gfeat = d.in_feat;
+      }
+      op.reduce = SAGA_RED_SUM;
+      break;
+    case SAGA_LAYER_GAT: {
+      const int64_t F = d.head_mean ? (int64_t)d.out_feat * d.heads : d.out_feat;
+      const int64_t cols = F + 2 * d.heads;
+      b->ldw = ld_for(cols, SAGA_F32);
+      b->wext = static_cast<float*>(c.take((size_t)d.in_feat * b->ldw * 4));
+      b->ldz = ld_for(cols, SAGA_F32);
+      b->z = c.take((size_t)V * b->ldz * 4);
+      op.reduce = SAGA_RED_SOFTMAX;
+      op.heads = d.heads;
+      gfeat = F;
+      break;
+    }
+    case SAGA_LAYER_SAGE_POOL:
+      b->ldz = ld_for(d.in_feat, t);
+      b->z = c.take((size_t)V * b->ldz * es);
+      b->ldz2 = ld_for(d.in_feat, t);
+      b->z2 = c.take((size_t)V * b->ldz2 * es);
+      op.reduce = SAGA_RED_MAX;
+      gfeat = d.in_feat;
+      break;
+    case SAGA_LAYER_GATED_GRU:
+      b->ldz = ld_for(d.in_feat, t);
+      b->z = c.take((size_t)V * b->ldz * es);
+      b->ldz2 = b->ldz;
+      b->z2 = c.take((size_t)V * b->ldz2 * es);
+      b->ldz3 = b->ldz;
+      b->z3 = c.take((size_t)V * b->ldz3 * es);
+      op.reduce = SAGA_RED_SUM;
+      gfeat = d.in_feat;
+      break;
+  }
+  size_t pb;
+  gather_ws_bytes(p, op, gfeat, &pb);
+  b->part_bytes = pb;
+  b->part = c.take(pb);
+  return c.used;
+}
+
+saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_cmat& x,
+                      const saga_cmat& ef, const saga_mat& out, void* ws, size_t ws_bytes,
+                      hipStream_t st) {
+  saga_status s = layer_check_desc(p, d);
+  if (s) return s;
+  LayerBufs b;
+  const size_t need = layer_carve(p, d, nullptr, &b);
+  if (!ws || ws_bytes < need)
+    return fail(SAGA_EWORKSPACE, "layer workspace: need %zu bytes, got %zu", need, ws_bytes);
+  if ((uintptr_t)ws % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
+  b = LayerBufs();
+  layer_carve(p, d, ws, &b);
+  const size_t es = esize(d.dtype);
+  const int64_t V = p.num_dst, Fi = d.in_feat, Fo = d.out_feat;
+  s = check_mat(x.ptr, x.rows, x.cols, x.ld, V, Fi, es, true, "x");
+  if (s) return s;
+  const void* wsend = static_cast<char*>(ws) + need;
+  if (range_overlap(out.ptr, mat_bytes(out.rows, out.cols, out.ld, es), ws,
+                    (size_t)((char*)wsend - (char*)ws)))
+    return fail(SAGA_EINVAL, "output overlaps the workspace");
+
+  saga_gemm_op g;
+  memset(&g, 0, sizeof(g));
+  g.dtype = d.dtype;
+  saga_edge_op op;
+  memset(&op, 0, sizeof(op));
+  op.dtype = d.dtype;
+  saga_edge_inputs in;
+  memset(&in, 0, sizeof(in));
+  const saga_cmat none = {nullptr, 0, 0, 0};
+
+  switch (d.kind) {
+    case SAGA_LAYER_GCN: {
+      if (gcn_transform_first(d)) {
+        // Z = d_out^-1/2 (X W); out = act(d_in^-1/2 sum_u Z_u + b)
+        g.mode = SAGA_GEMM_PLAIN;
+        g.row_scale_deg = p.d_out;
+        s = run_gemm(g, x, saga_cmat{d.w, Fi, Fo, Fo}, none, none, nullptr, nullptr,
+                     saga_mat{b.z, V, Fo, b.ldz}, st);
+        if (s) return s;
+        op.msg = SAGA_MSG_COPY;
+        op.reduce = SAGA_RED_SUM;
+        op.dst_norm = 1;
+        op.act = d.act;
+        in.src = saga_cmat{b.z, V, Fo, b.ldz};
+        in.bias = d.b;
+        return run_gather(p, op, in, out, b.part, b.part_bytes, st);
+      }
+      // aggregate first: agg = d_in^-1/2 sum_u d_out(u)^-1/2 X_u; out = act(agg W + b)
+      op.msg = SAGA_MSG_SRC_NORM;
+      op.reduce = SAGA_RED_SUM;
+      op.dst_norm = 1;
+      in.src = x;
+      s = run_gather(p, op, in, saga_mat{b.z2, V, Fi, b.ldz2}, b.part, b.part_bytes, st);
+      if (s) return s;
+      g.mode = SAGA_GEMM_PLAIN;
+      g.act = d.act;
+      return run_gemm(g, saga_cmat{b.z2, V, Fi, b.ldz2}, saga_cmat{d.w, Fi, Fo, Fo}, none, none,
+                      d.b, nullptr, out, st);
+    }
+    case SAGA_LAYER_GAT: {
+      const int64_t H = d.heads;
+      const int64_t F = d.head_mean ? Fo * H : Fo;
+      const int64_t cols = F + 2 * H;
+      hipError_t e = saga::launch_fold_attention(static_cast<const float*>(d.w), Fi, F, (int)H,
+                                                 d.attn_l, d.attn_r, b.wext, b.ldw, st);
+      if (e != hipSuccess) return dev_fail(e, "fold launch");
+      g.mode = SAGA_GEMM_PLAIN;
+      s = run_gemm(g, x, saga_cmat{b.wext, Fi, cols, b.ldw}, none, none, nullptr, nullptr,
+                   saga_mat{b.z, V, cols, b.ldz}, st);
+      if (s) return s;
+      const float* z = static_cast<const float*>(b.z);
+      op.msg = SAGA_MSG_GAT;
+      op.reduce = SAGA_RED_SOFTMAX;
+      op.heads = (int32_t)H;
+      op.head_mean = d.head_mean;
+      op.neg_slope = d.neg_slope;
+      op.act = d.act;
+      in.src = saga_cmat{z, V, F, b.ldz};
+      in.el = saga_cmat{z + F, V, H, b.ldz};
+      in.er = saga_cmat{z + F + H, V, H, b.ldz};
+      in.bias = d.b;
+      return run_gather(p, op, in, out, b.part, b.part_bytes, st);
+    }
+    case SAGA_LAYER_SAGE_POOL: {
+      g.mode = SAGA_GEMM_PLAIN;
+      g.act = SAGA_ACT_RELU;
+      s = run_gemm(g, x, saga_cmat{d.w_pool, Fi, Fi, Fi}, none, none, d.b_pool, nullptr,
+                   saga_mat{b.z, V, Fi, b.ldz}, st);
+      if (s) return s;
+      op.msg = SAGA_MSG_COPY;
+      op.reduce = SAGA_RED_MAX;
+      in.src = saga_cmat{b.z, V, Fi, b.ldz};
+      s = run_gather(p, op, in, saga_mat{b.z2, V, Fi, b.ldz2}, b.part, b.part_bytes, st);
+      if (s) return s;
+      const char* w = static_cast<const char*>(d.w);
+      g.mode = SAGA_GEMM_CONCAT;
+      g.act = SAGA_ACT_NONE;
+      return run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, Fi, b.ldz2},
+                      saga_cmat{w + (size_t)Fi * Fo * es, Fi, Fo, Fo}, d.b, nullptr, out, st);
+    }
+    case SAGA_LAYER_GATED_GRU: {
+      const int64_t F = Fi, Fe = d.edge_feat;
+      g.mode = SAGA_GEMM_PLAIN;
+      s = run_gemm(g, x, saga_cmat{d.w_e, F, F, F}, none, none, nullptr, nullptr,
+                   saga_mat{b.z, V, F, b.ldz}, st);
+      if (s) return s;
+      s = run_gemm(g, x, saga_cmat{d.w_e + F * F, F, F, F}, none, none, nullptr, nullptr,
+                   saga_mat{b.z2, V, F, b.ldz2}, st);
+      if (s) return s;
+      op.msg = SAGA_MSG_GATED;
+      op.reduce = SAGA_RED_SUM;
+      in.src = x;
+      in.gate_src = saga_cmat{b.z, V, F, b.ldz};
+      in.gate_dst = saga_cmat{b.z2, V, F, b.ldz2};
+      in.edge_feat = ef;
+      if (ef.cols != Fe) return fail(SAGA_EINVAL, "edge_feat: %lld columns, desc says %d", (long long)ef.cols, d.edge_feat);
+      in.w_edge = d.w_e + 2 * F * F;
+      in.gate_bias = d.b_e;
+      s = run_gather(p, op, in, saga_mat{b.z3, V, F, b.ldz3}, b.part, b.part_bytes, st);
+      if (s) return s;
+      g.mode = SAGA_GEMM_GRU;
+      return run_gemm(g, saga_cmat{b.z3, V, F, b.ldz3}, saga_cmat{d.w_ih, F, 3 * F, 3 * F}, x,
+                      saga_cmat{d.w_hh, F, 3 * F, 3 * F}, d.b_ih, d.b_hh, out, st);
+    }
+  }
+  return fail(SAGA_EINVAL, "bad layer kind");
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* saga_status_str(saga_status s) {
+  switch (s) {
+    case SAGA_OK: return "ok";
+    case SAGA_EINVAL: return "invalid argument";
+    case SAGA_EGRAPH: return "invalid graph";
+    case SAGA_EUNSUPPORTED: return "unsupported";
+    case SAGA_EDEVICE: return "device error";
+    case SAGA_EWORKSPACE: return "workspace too small";
+    case SAGA_EINTERNAL: return "internal error";
+  }
+  return "unknown status";
+}
+
+const char* saga_last_error(void) { return g_err; }
+
+const char* saga_version(void) { return "saga-mi355x 0.1 (gfx950)"; }
+
+saga_status saga_plan_workspace_size(int32_t num_dst, int32_t num_src, int64_t num_edges,
+                                     const saga_plan_opts* opts, size_t* bytes) {
+  try {
+    if (!bytes) return fail(SAGA_EINVAL, "bytes is null");
+    int32_t T, B, c;
+    saga_status s = resolve_opts(opts, &T, &B, &c);
+    if (s) return s;
+    saga::PlanLayout L;
+    if (!saga::plan_layout(num_dst, num_src, num_edges, T, B, c, &L))
+      return fail(SAGA_EINVAL, "graph sizes out of range (need 0 <= E < 2^31 and E + row_cost * segments < 2^31)");
+    *bytes = L.total;
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_plan_build(int32_t num_dst, int32_t num_src, int64_t num_edges,
+                            const int32_t* row_ptr, const int32_t* col_idx,
+                            const saga_plan_opts* opts, void* workspace, size_t workspace_bytes,
+                            void* stream, saga_plan* plan) {
+  try {
+    if (!plan) return fail(SAGA_EINVAL, "plan is null");
+    int32_t T, B, c;
+    saga_status s = resolve_opts(opts, &T, &B, &c);
+    if (s) return s;
+    saga::PlanLayout L;
+    if (!saga::plan_layout(num_dst, num_src, num_edges, T, B, c, &L))
+      return fail(SAGA_EINVAL, "graph sizes out of range");
+    if (!row_ptr) return fail(SAGA_EINVAL, "row_ptr is null");
+    if (num_edges > 0 && !col_idx) return fail(SAGA_EINVAL, "col_idx is null");
+    if (!workspace || workspace_bytes < L.total)
+      return fail(SAGA_EWORKSPACE, "plan workspace: need %zu bytes, got %zu", L.total, workspace_bytes);
+    if ((uintptr_t)workspace % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
+    char* w = static_cast<char*>(workspace);
+    saga_plan p;
+    memset(&p, 0, sizeof(p));
+    p.num_dst = num_dst;
+    p.num_src = num_src;
+    p.num_edges = num_edges;
+    p.row_ptr = row_ptr;
+    p.col_idx = col_idx;
+    p.seg_len = T;
+    p.block_cost = B;
+    p.row_cost = c;
+    p.max_segments = L.max_segments;
+    p.max_blocks = L.max_blocks;
+    p.max_split = L.max_split;
+    p.max_split_segments = L.max_split_segments;
+    p.d_in = reinterpret_cast<int32_t*>(w + L.off_d_in);
+    p.d_out = reinterpret_cast<int32_t*>(w + L.off_d_out);
+    p.perm = reinterpret_cast<int32_t*>(w + L.off_perm);
+    p.row_seg_first = reinterpret_cast<int32_t*>(w + L.off_first);
+    p.seg_row = reinterpret_cast<int32_t*>(w + L.off_seg_row);
+    p.seg_beg = reinterpret_cast<int32_t*>(w + L.off_seg_beg);
+    p.seg_end = reinterpret_cast<int32_t*>(w + L.off_seg_end);
+    p.block_ptr = reinterpret_cast<int32_t*>(w + L.off_block_ptr);
+    p.counts = reinterpret_cast<int32_t*>(w + L.off_counts);
+    p.scratch = w + L.off_scratch;
+    p.scratch_bytes = L.scratch_bytes;
+    hipError_t e = saga::launch_plan_build(p, L, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return dev_fail(e, "plan launch");
+    *plan = p;
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_plan_check(const saga_plan* plan, void* stream, saga_plan_counts* counts) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    int32_t h[saga::kCountSlots];
+    hipError_t e = hipMemcpyAsync(h, plan->counts, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return dev_fail(e, "plan check");
+    if (counts) {
+      counts->num_segments = h[saga::kNumSegments];
+      counts->num_blocks = h[saga::kNumBlocks];
+      counts->n_split = h[saga::kNSplit];
+      counts->s_split = h[saga::kSSplit];
+      counts->error_flags = h[saga::kErrFlags];
+      counts->max_in_degree = h[saga::kMaxDegree];
+    }
+    const int f = h[saga::kErrFlags];
+    if (f & saga::kErrInternal) return fail(SAGA_EINTERNAL, "plan builder invariant violated");
+    if (f)
+      return fail(SAGA_EGRAPH, "CSR invalid:%s%s%s%s", (f & 1) ? " row_ptr[0]!=0" : "",
+                  (f & 2) ? " row_ptr decreasing" : "", (f & 4) ? " row_ptr[num_dst]!=num_edges" : "",
+                  (f & 8) ? " col_idx out of range" : "");
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_gather_workspace_size(const saga_plan* plan, const saga_edge_op* op,
+                                       int64_t feat, size_t* bytes) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!op || !bytes) return fail(SAGA_EINVAL, "null argument");
+    if (feat <= 0) return fail(SAGA_EINVAL, "feat must be > 0");
+    return gather_ws_bytes(*plan, *op, feat, bytes) ? SAGA_EINTERNAL : ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edge_op* op,
+                                           const saga_edge_inputs* in, saga_mat out,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* stream) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!op || !in) return fail(SAGA_EINVAL, "null argument");
+    return run_gather(*plan, *op, *in, out, workspace, workspace_bytes,
+                      static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_apply_vertex(const saga_gemm_op* op, saga_cmat a, saga_cmat w, saga_cmat a2,
+                              saga_cmat w2, const float* bias, const float* bias2, saga_mat out,
+                              void* stream) {
+  try {
+    if (!op) return fail(SAGA_EINVAL, "op is null");
+    return run_gemm(*op, a, w, a2, w2, bias, bias2, out, static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_layer_workspace_size(const saga_plan* plan, const saga_layer_desc* desc,
+                                      size_t* bytes) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!desc || !bytes) return fail(SAGA_EINVAL, "null argument");
+    s = layer_check_desc(*plan, *desc);
+    if (s) return s;
+    LayerBufs b;
+    *bytes = layer_carve(*plan, *desc, nullptr, &b);
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_layer(const saga_plan* plan, const saga_layer_desc* desc, saga_cmat x,
+                       saga_cmat edge_feat, saga_mat out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!desc) return fail(SAGA_EINVAL, "desc is null");
+    return run_layer(*plan, *desc, x, edge_feat, out, workspace, workspace_bytes,
+                     static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,566 @@
+// Fused Scatter + ApplyEdge + Gather on the in-CSR (Sec. 3.2 of the paper:
+// Scatter moves the source embeddings along the edges, ApplyEdge turns them
+// into messages or attention scores, Gather reduces them per destination;
+// fused, the sum-Gather is the sparse adjacency x embedding product of
+// Fig. 7b).  No edge tensor is materialised: every message lives only in
+// registers.
+//
+// Work decomposition (one plan, all reductions):
+//   * a "group" of LPR lanes owns one segment (<= seg_len in-edges of one
+//     destination row) at a time; each lane holds a 16-byte slice of the
+//     feature row (LPR = next power of two of the row's 16-byte vectors);
+//   * a workgroup (256 threads) walks one row block (consecutive segments of
+//     the degree-sorted order, bounded total cost), groups striding over it;
+//   * the neighbour indices of a segment are read 1 per lane, coalesced, and
+//     broadcast inside the group with a cross-lane permute; the source rows
+//     are fetched as 128-bit loads, U rows in flight per lane;
+//   * a segment that is a whole row applies the epilogue and writes the
+//     output row; segments of split rows (d_in > seg_len) write float32
+//     partials, merged in segment order by k_combine (deterministic: no
+//     floating-point atomics anywhere).
+#include "saga_device.h"
+#include "saga_internal.h"
+
+namespace saga {
+namespace {
+
+constexpr int kThreads = 256;
+enum { kSum = 0, kMean = 1, kMax = 2, kSoftmax = 3 };
+
+template <typename T>
+__device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int col0,
+                                          float (&x)[Vec16<T>::N]) {
+  constexpr int EPV = Vec16<T>::N;
+#pragma unroll
+  for (int k = 0; k < EPV; ++k) {
+    const int c = col0 + k;
+    float v = x[k];
+    if (a.bias && c < a.out_cols) v += a.bias[c];
+    x[k] = apply_act(a.act, v);
+  }
+  T* o = static_cast<T*>(a.out) + row * a.ld_out + col0;
+  if (col0 + EPV <= a.out_cols)
+    Vec16<T>::store(o, x);
+  else if (col0 < a.out_cols)
+    Vec16<T>::store_n(o, x, a.out_cols - col0);
+}
+
+// ------------------------------------------------------------------------
+// COPY / SRC_NORM messages with SUM, MEAN or MAX
+// ------------------------------------------------------------------------
+template <typename T, int LPR, int VPL, int U, bool MAXRED>
+__global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a) {
+  constexpr int EPV = Vec16<T>::N;
+  constexpr int NG = kThreads / LPR;
+  const int32_t* __restrict__ counts = a.counts;
+  if (counts[kErrFlags]) return;
+  const int nb = counts[kNumBlocks];
+  const int s_split = counts[kSSplit];
+  const int gl = threadIdx.x % LPR;
+  const int grp = threadIdx.x / LPR;
+  const int gbase = (threadIdx.x & 63) - gl;
+  const int nv = (int)((a.feat * (int64_t)sizeof(T) + 15) / 16);
+  const bool srcnorm = a.msg == SAGA_MSG_SRC_NORM;
+  const T* __restrict__ src = static_cast<const T*>(a.src);
+  const int32_t* __restrict__ col = a.col_idx;
+  const float init = MAXRED ? -INFINITY : 0.0f;
+
+  for (int b = blockIdx.x; b < nb; b += gridDim.x) {
+    const int s0 = a.block_ptr[b], s1 = a.block_ptr[b + 1];
+    for (int s = s0 + grp; s < s1; s += NG) {
+      const int row = a.seg_row[s];
+      const int beg = a.seg_beg[s], end = a.seg_end[s];
+      float acc[VPL][EPV];
+#pragma unroll
+      for (int q = 0; q < VPL; ++q)
+#pragma unroll
+        for (int i = 0; i < EPV; ++i) acc[q][i] = init;
+
+      for (int e = beg; e < end; e += LPR) {
+        const int my = e + gl;
+        const int c = my < end ? col[my] : 0;
+        float w = 1.0f;
+        if (srcnorm) w = my < end ? rsqrt_deg(a.d_out[c]) : 0.0f;
+        const int n = (end - e) < LPR ? (end - e) : LPR;
+        int t = 0;
+        for (; t + U <= n; t += U) {
+          int u[U];
+          float wu[U];
+#pragma unroll
+          for (int k = 0; k < U; ++k) {
+            u[k] = __shfl(c, gbase + t + k, 64);
+            wu[k] = srcnorm ? __shfl(w, gbase + t + k, 64) : 1.0f;
+          }
+          float x[U][VPL][EPV];
+#pragma unroll
+          for (int k = 0; k < U; ++k)
+#pragma unroll
+            for (int q = 0; q < VPL; ++q) {
+              const int vi = gl + q * LPR;
+              if (vi < nv) Vec16<T>::load(src + (int64_t)u[k] * a.ld_src + vi * EPV, x[k][q]);
+            }
+#pragma unroll
+          for (int k = 0; k < U; ++k)
+#pragma unroll
+            for (int q = 0; q < VPL; ++q)
+#pragma unroll
+              for (int i = 0; i < EPV; ++i) {
+                if (MAXRED)
+                  acc[q][i] = fmaxf(acc[q][i], x[k][q][i] * wu[k]);
+                else
+                  acc[q][i] += x[k][q][i] * wu[k];
+              }
+        }
+        for (; t < n; ++t) {
+          const int uu = __shfl(c, gbase + t, 64);
+          const float ww = srcnorm ? __shfl(w, gbase + t, 64) : 1.0f;
+#pragma unroll
+          for (int q = 0; q < VPL; ++q) {
+            const int vi = gl + q * LPR;
+            float x[EPV];
+            if (vi < nv) {
+              Vec16<T>::load(src + (int64_t)uu * a.ld_src + vi * EPV, x);
+#pragma unroll
+              for (int i = 0; i < EPV; ++i) {
+                if (MAXRED)
+                  acc[q][i] = fmaxf(acc[q][i], x[i] * ww);
+                else
+                  acc[q][i] += x[i] * ww;
+              }
+            }
+          }
+        }
+      }
+
+      if (s < s_split) {
+        float* p = a.partial + (int64_t)s * a.pstride;
+#pragma unroll
+        for (int q = 0; q < VPL; ++q) {
+          const int vi = gl + q * LPR;
+          if (vi < nv)
+#pragma unroll
+            for (int i = 0; i < EPV; ++i) p[vi * EPV + i] = acc[q][i];
+        }
+      } else {
+        const int d = end - beg;  // a whole row
+        float scale = 1.0f;
+        if (a.reduce == kMean) scale = d > 0 ? 1.0f / (float)d : 0.0f;
+        if (a.dst_norm) scale *= rsqrt_deg(d);
+#pragma unroll
+        for (int q = 0; q < VPL; ++q) {
+          const int vi = gl + q * LPR;
+          if (vi < nv) {
+            float x[EPV];
+#pragma unroll
+            for (int i = 0; i < EPV; ++i) {
+              float v = acc[q][i];
+              if (MAXRED && d == 0) v = 0.0f;
+              x[i] = v * scale;
+            }
+            store_out<T>(a, row, vi * EPV, x);
+          }
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------
+// GAT: LeakyReLU(el[u] + er[v]) scores, online softmax per head (float32)
+// ------------------------------------------------------------------------
+template <int LPR, int U>
+__global__ __launch_bounds__(kThreads) void k_gather_gat(GatherArgs a) {
+  constexpr int NG = kThreads / LPR;
+  const int32_t* __restrict__ counts = a.counts;
+  if (counts[kErrFlags]) return;
+  const int nb = counts[kNumBlocks];
+  const int s_split = counts[kSSplit];
+  const int gl = threadIdx.x % LPR;
+  const int grp = threadIdx.x / LPR;
+  const int gbase = (threadIdx.x & 63) - gl;
+  const int F = a.feat, H = a.heads, D = F / H;
+  const int nv = F / 4;
+  const bool active = gl < nv;
+  const int head = active ? (gl * 4) / D : 0;
+  const float* __restrict__ z = static_cast<const float*>(a.src);
+  const int32_t* __restrict__ col = a.col_idx;
+  const float slope = a.neg_slope;
+
+  for (int b = blockIdx.x; b < nb; b += gridDim.x) {
+    const int s0 = a.block_ptr[b], s1 = a.block_ptr[b + 1];
+    for (int s = s0 + grp; s < s1; s += NG) {
+      const int row = a.seg_row[s];
+      const int beg = a.seg_beg[s], end = a.seg_end[s];
+      const float erv = active ? a.er[(int64_t)row * a.ld_er + head] : 0.0f;
+      float m = -INFINITY, l = 0.0f;
+      float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int e = beg; e < end; e += LPR) {
+        const int my = e + gl;
+        const int c = my < end ? col[my] : 0;
+        const int n = (end - e) < LPR ? (end - e) : LPR;
+        for (int t = 0; t < n; t += U) {
+          int u[U];
+          float sc[U], x[U][4];
+#pragma unroll
+          for (int k = 0; k < U; ++k) {
+            u[k] = __shfl(c, gbase + ((t + k) < n ? t + k : t), 64);
+            if (active) {
+              sc[k] = a.el[(int64_t)u[k] * a.ld_el + head];
+              Vec16<float>::load(z + (int64_t)u[k] * a.ld_src + gl * 4, x[k]);
+            }
+          }
+#pragma unroll
+          for (int k = 0; k < U; ++k) {
+            if (t + k < n) {
+              float sv = sc[k] + erv;
+              sv = sv > 0.0f ? sv : slope * sv;
+              const float mn = fmaxf(m, sv);
+              const float f = __expf(m - mn);
+              const float p = __expf(sv - mn);
+              l = l * f + p;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) acc[i] = acc[i] * f + p * x[k][i];
+              m = mn;
+            }
+          }
+        }
+      }
+      if (s < s_split) {
+        if (active) {
+          float* p = a.partial + (int64_t)s * a.pstride;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) p[gl * 4 + i] = acc[i];
+          if ((gl * 4) % D == 0) {
+            p[a.pcols + head] = m;
+            p[a.pcols + H + head] = l;
+          }
+        }
+      } else {
+        float o[4];
+        const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = active ? acc[i] * inv : 0.0f;
+        if (a.head_mean) {
+          // sum over heads: lanes gl = head * (D/4) + off
+          for (int k = D / 4; k < nv; k <<= 1)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o[i] += __shfl_xor(o[i], k, 64);
+          if (active && head == 0) {
+            const float r = 1.0f / (float)H;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o[i] *= r;
+            store_out<float>(a, row, gl * 4, o);
+          }
+        } else if (active) {
+          store_out<float>(a, row, gl * 4, o);
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------
+// Gated messages: sigmoid(gs[u] + gd[v] + b_e + e_uv W_ee) * h[u], SUM
+// (float32, F = 64, one 16-byte slice of 4 features per lane)
+// ------------------------------------------------------------------------
+template <int LPR>
+__global__ __launch_bounds__(kThreads) void k_gather_gated(GatherArgs a) {
+  constexpr int NG = kThreads / LPR;
+  constexpr int FE_MAX = 16;
+  const int32_t* __restrict__ counts = a.counts;
+  if (counts[kErrFlags]) return;
+  const int nb = counts[kNumBlocks];
+  const int s_split = counts[kSSplit];
+  const int gl = threadIdx.x % LPR;
+  const int grp = threadIdx.x / LPR;
+  const int gbase = (threadIdx.x & 63) - gl;
+  const int F = a.feat, Fe = a.fe;
+  const int nv = F / 4;
+  const bool active = gl < nv;
+  const float* __restrict__ h = static_cast<const float*>(a.src);
+  const int32_t* __restrict__ col = a.col_idx;
+  float wr[FE_MAX][4];
+#pragma unroll
+  for (int i = 0; i < FE_MAX; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      wr[i][q] = (active && i < Fe) ? a.w_edge[(int64_t)i * F + gl * 4 + q] : 0.0f;
+  float gb[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) gb[q] = (active && a.gate_bias) ? a.gate_bias[gl * 4 + q] : 0.0f;
+
+  for (int b = blockIdx.x; b < nb; b += gridDim.x) {
+    const int s0 = a.block_ptr[b], s1 = a.block_ptr[b + 1];
+    for (int s = s0 + grp; s < s1; s += NG) {
+      const int row = a.seg_row[s];
+      const int beg = a.seg_beg[s], end = a.seg_end[s];
+      float gd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (active) {
+        Vec16<float>::load(a.gdst + (int64_t)row * a.ld_gdst + gl * 4, gd);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gd[q] += gb[q];
+      }
+      float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int e = beg; e < end; e += LPR) {
+        const int my = e + gl;
+        const int c = my < end ? col[my] : 0;
+        const int n = (end - e) < LPR ? (end - e) : LPR;
+        for (int t = 0; t < n; ++t) {
+          const int u = __shfl(c, gbase + t, 64);
+          if (!active) continue;
+          const int64_t eid = (int64_t)(e + t);
+          float hs[4], gs[4];
+          Vec16<float>::load(h + (int64_t)u * a.ld_src + gl * 4, hs);
+          Vec16<float>::load(a.gsrc + (int64_t)u * a.ld_gsrc + gl * 4, gs);
+          float pre[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) pre[q] = gs[q] + gd[q];
+          const float* ef = a.efeat + eid * a.ld_efeat;
+#pragma unroll
+          for (int i4 = 0; i4 < FE_MAX / 4; ++i4) {
+            if (i4 * 4 < Fe) {
+              float ev[4];
+              Vec16<float>::load(ef + i4 * 4, ev);
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) pre[q] += ev[j] * wr[i4 * 4 + j][q];
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[q] += sigmoidf_(pre[q]) * hs[q];
+        }
+      }
+      if (!active) continue;
+      if (s < s_split) {
+        float* p = a.partial + (int64_t)s * a.pstride;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) p[gl * 4 + q] = acc[q];
+      } else {
+        store_out<float>(a, row, gl * 4, acc);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------
+// Split rows: merge the segment partials of each row in segment order.
+// Thread t handles column t % pc of every SPL-th segment; the SPL partial
+// results are then merged in order through LDS.
+// ------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_combine(GatherArgs a) {
+  __shared__ float sm_acc[kThreads];
+  __shared__ float sm_m[kThreads];
+  __shared__ float sm_l[kThreads];
+  __shared__ float fin[1024];
+  const int32_t* __restrict__ counts = a.counts;
+  if (counts[kErrFlags]) return;
+  const int n_split = counts[kNSplit];
+  const int red = a.reduce;
+  const int F = a.feat;
+  const int pc = a.pcols;  // partial columns (F rounded up to 8), <= 1024
+  const int H = a.heads > 0 ? a.heads : 1;
+  const int D = F / H;
+  const int spl = pc >= kThreads ? 1 : kThreads / pc;
+  const int t = threadIdx.x;
+
+  for (int i = blockIdx.x; i < n_split; i += gridDim.x) {
+    const int row = a.perm[i];
+    const int f0 = a.row_seg_first[i], f1 = a.row_seg_first[i + 1];
+    const int d = a.d_in[row];
+    for (int c0 = 0; c0 < pc; c0 += kThreads) {
+      int colc, sp;
+      bool on;
+      if (spl > 1) {
+        sp = t / pc;
+        colc = t % pc;
+        on = sp < spl;
+      } else {
+        sp = 0;
+        colc = c0 + t;
+        on = colc < pc;
+      }
+      float A = red == kMax ? -INFINITY : 0.0f, M = -INFINITY, L = 0.0f;
+      if (on) {
+        const int hd = (red == kSoftmax && colc < F) ? colc / D : 0;
+        for (int j = f0 + sp; j < f1; j += spl) {
+          const float* p = a.partial + (int64_t)j * a.pstride;
+          const float v = p[colc];
+          if (red == kMax) {
+            A = fmaxf(A, v);
+          } else if (red == kSoftmax) {
+            const float mj = p[pc + hd], lj = p[pc + H + hd];
+            const float mn = fmaxf(M, mj);
+            const float fa = __expf(M - mn), fb = __expf(mj - mn);
+            A = A * fa + v * fb;
+            L = L * fa + lj * fb;
+            M = mn;
+          } else {
+            A += v;
+          }
+        }
+      }
+      sm_acc[t] = A;
+      sm_m[t] = M;
+      sm_l[t] = L;
+      __syncthreads();
+      if (on && sp == 0) {
+        for (int q = 1; q < spl; ++q) {
+          const int o = q * pc + colc;
+          if (red == kMax) {
+            A = fmaxf(A, sm_acc[o]);
+          } else if (red == kSoftmax) {
+            const float mn = fmaxf(M, sm_m[o]);
+            const float fa = __expf(M - mn), fb = __expf(sm_m[o] - mn);
+            A = A * fa + sm_acc[o] * fb;
+            L = L * fa + sm_l[o] * fb;
+            M = mn;
+          } else {
+            A += sm_acc[o];
+          }
+        }
+        float v;
+        if (red == kSoftmax) {
+          v = L > 0.0f ? A / L : 0.0f;
+        } else {
+          v = A;
+          if (red == kMax && d == 0) v = 0.0f;
+          if (red == kMean) v = d > 0 ? v / (float)d : 0.0f;
+          if (a.dst_norm) v *= rsqrt_deg(d);
+        }
+        fin[colc] = v;
+      }
+      __syncthreads();
+    }
+    // epilogue over output columns
+    for (int c = t; c < a.out_cols; c += kThreads) {
+      float v;
+      if (red == kSoftmax && a.head_mean) {
+        v = 0.0f;
+        for (int k = 0; k < H; ++k) v += fin[k * D + c];
+        v *= 1.0f / (float)H;
+      } else {
+        v = fin[c];
+      }
+      if (a.bias) v += a.bias[c];
+      v = apply_act(a.act, v);
+      T* o = static_cast<T*>(a.out) + (int64_t)row * a.ld_out + c;
+      if constexpr (sizeof(T) == 4)
+        *o = v;
+      else
+        *o = f32_to_bf16(v);
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void k_fold_attention(const float* __restrict__ w, int64_t K, int64_t F, int H,
+                                 const float* __restrict__ al, const float* __restrict__ ar,
+                                 float* __restrict__ wx, int64_t ldx) {
+  const int64_t ncol = F + 2 * H;
+  const int64_t n = K * ncol;
+  const int64_t D = F / H;
+  for (int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; idx < n;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t k = idx / ncol, c = idx % ncol;
+    float v;
+    if (c < F) {
+      v = w[k * F + c];
+    } else {
+      const int64_t hh = (c - F) % H;
+      const float* att = (c - F) < H ? al : ar;
+      v = 0.0f;
+      for (int64_t dd = 0; dd < D; ++dd) v += w[k * F + hh * D + dd] * att[hh * D + dd];
+    }
+    wx[k * ldx + c] = v;
+  }
+}
+
+inline int next_pow2(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+template <typename T, int LPR, int VPL>
+hipError_t launch_simple_lpr(const GatherArgs& a, unsigned grid, hipStream_t st) {
+  constexpr int U = LPR >= 8 ? (VPL == 1 ? 8 : 4) : 4;
+  if (a.reduce == kMax)
+    hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, true>), dim3(grid), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, false>), dim3(grid), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_simple(const GatherArgs& a, int nv, unsigned grid, hipStream_t st) {
+  if (nv > 64) return launch_simple_lpr<T, 64, 2>(a, grid, st);
+  switch (next_pow2(nv)) {
+    case 1: return launch_simple_lpr<T, 1, 1>(a, grid, st);
+    case 2: return launch_simple_lpr<T, 2, 1>(a, grid, st);
+    case 4: return launch_simple_lpr<T, 4, 1>(a, grid, st);
+    case 8: return launch_simple_lpr<T, 8, 1>(a, grid, st);
+    case 16: return launch_simple_lpr<T, 16, 1>(a, grid, st);
+    case 32: return launch_simple_lpr<T, 32, 1>(a, grid, st);
+    default: return launch_simple_lpr<T, 64, 1>(a, grid, st);
+  }
+}
+
+}  // namespace
+
+int gather_partial_cols(int64_t feat) { return (int)((feat + 7) / 8 * 8); }
+
+size_t gather_partial_stride(const saga_edge_op& op, int64_t feat) {
+  int64_t pc = gather_partial_cols(feat);
+  if (op.reduce == SAGA_RED_SOFTMAX) pc += 2 * op.heads;
+  return (size_t)((pc + 3) / 4 * 4);
+}
+
+hipError_t launch_gather(const GatherArgs& a, hipStream_t st) {
+  const unsigned grid = (unsigned)(a.max_blocks > 0 ? a.max_blocks : 1);
+  const int esz = a.dtype == SAGA_BF16 ? 2 : 4;
+  const int nv = (int)((a.feat * (int64_t)esz + 15) / 16);
+  hipError_t err = hipSuccess;
+  if (a.msg == SAGA_MSG_GAT) {
+    const int lpr = next_pow2(nv);
+    switch (lpr) {
+      case 1: hipLaunchKernelGGL((k_gather_gat<1, 4>), dim3(grid), dim3(kThreads), 0, st, a); break;
+      case 2: hipLaunchKernelGGL((k_gather_gat<2, 4>), dim3(grid), dim3(kThreads), 0, st, a); break;
+      case 4: hipLaunchKernelGGL((k_gather_gat<4, 4>), dim3(grid), dim3(kThreads), 0, st, a); break;
+      case 8: hipLaunchKernelGGL((k_gather_gat<8, 4>), dim3(grid), dim3(kThreads), 0, st, a); break;
+      case 16: hipLaunchKernelGGL((k_gather_gat<16, 4>), dim3(grid), dim3(kThreads), 0, st, a); break;
+      case 32: hipLaunchKernelGGL((k_gather_gat<32, 4>), dim3(grid), dim3(kThreads), 0, st, a); break;
+      default: hipLaunchKernelGGL((k_gather_gat<64, 4>), dim3(grid), dim3(kThreads), 0, st, a); break;
+    }
+    err = hipGetLastError();
+  } else if (a.msg == SAGA_MSG_GATED) {
+    hipLaunchKernelGGL((k_gather_gated<16>), dim3(grid), dim3(kThreads), 0, st, a);
+    err = hipGetLastError();
+  } else if (a.dtype == SAGA_BF16) {
+    err = launch_simple<uint16_t>(a, nv, grid, st);
+  } else {
+    err = launch_simple<float>(a, nv, grid, st);
+  }
+  if (err != hipSuccess) return err;
+  if (a.max_split > 0) {
+    const unsigned cg = (unsigned)(a.max_split < 4096 ? a.max_split : 4096);
+    if (a.dtype == SAGA_BF16)
+      hipLaunchKernelGGL(k_combine<uint16_t>, dim3(cg), dim3(kThreads), 0, st, a);
+    else
+      hipLaunchKernelGGL(k_combine<float>, dim3(cg), dim3(kThreads), 0, st, a);
+    err = hipGetLastError();
+  }
+  return err;
+}
+
+hipError_t launch_fold_attention(const float* w, int64_t K, int64_t F, int heads, const float* al,
+                                 const float* ar, float* w_ext, int64_t ld_ext, hipStream_t st) {
+  const int64_t n = K * (F + 2 * heads);
+  const unsigned grid = (unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+  hipLaunchKernelGGL(k_fold_attention, dim3(grid), dim3(256), 0, st, w, K, F, heads, al, ar, w_ext,
+                     ld_ext);
+  return hipGetLastError();
+}
+
+}  // namespace saga

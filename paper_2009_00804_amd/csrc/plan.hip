@@ -1,0 +1,481 @@
+// Graph layout on the GPU: CSR validation, in/out degrees, degree-sorted row
+// order (stable LSD radix sort, largest degree first), row segments of at
+// most seg_len edges and row blocks of bounded cost.
+//
+// The degree skew of real graphs follows a power law (Sec. 3.2, Fig. 8a of
+// the paper); batching vertices by degree as the profiled library did left
+// the GPU idle (Fig. 8b/c).  Here the sorted order only schedules work: rows
+// of similar degree share a workgroup, the heaviest rows start first, and a
+// row longer than seg_len is split across several lanes groups so that no
+// single wave walks a hub row alone.
+#include "saga_device.h"
+#include "saga_internal.h"
+
+namespace saga {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kItems = 8;
+constexpr int kTile = kThreads * kItems;  // 2048 items per workgroup tile
+constexpr int kBins = 256;                // 8-bit radix digits
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// ------------------------------------------------------------------------
+// block-wide scans (blockDim.x == NT)
+// ------------------------------------------------------------------------
+__device__ __forceinline__ int32_t wave_incl_scan(int32_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int32_t y = __shfl_up(v, off, 64);
+    if (lane >= off) v += y;
+  }
+  return v;
+}
+
+template <int NT>
+__device__ __forceinline__ int32_t block_excl_scan(int32_t v, int32_t* total) {
+  __shared__ int32_t ws[NT / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int32_t incl = wave_incl_scan(v);
+  if (lane == 63) ws[wave] = incl;
+  __syncthreads();
+  int32_t off = 0, tot = 0;
+#pragma unroll
+  for (int k = 0; k < NT / 64; ++k) {
+    if (k < wave) off += ws[k];
+    tot += ws[k];
+  }
+  __syncthreads();
+  *total = tot;
+  return off + incl - v;
+}
+
+// ------------------------------------------------------------------------
+// functors feeding the generic scan
+// ------------------------------------------------------------------------
+struct ArrF {
+  const int32_t* p;
+  __device__ int32_t operator()(int64_t i) const { return p[i]; }
+};
+// number of segments of perm position i
+struct NsegF {
+  const int32_t* d_in;
+  const int32_t* perm;
+  int32_t T;
+  __device__ int32_t operator()(int64_t i) const {
+    int32_t d = d_in[perm[i]];
+    return d > T ? (d + T - 1) / T : 1;
+  }
+};
+// cost of segment s
+struct CostF {
+  const int32_t* beg;
+  const int32_t* end;
+  int32_t c;
+  __device__ int32_t operator()(int64_t i) const { return end[i] - beg[i] + c; }
+};
+
+// ------------------------------------------------------------------------
+// kernels
+// ------------------------------------------------------------------------
+__global__ void k_zero(int32_t* p, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+// d_in, d_out and CSR validation; error bits go to counts[kErrFlags]
+__global__ __launch_bounds__(kThreads) void k_degrees(const int32_t* __restrict__ rp,
+                                                      const int32_t* __restrict__ col, int32_t V,
+                                                      int32_t Vs, int64_t E, int32_t* d_in,
+                                                      int32_t* d_out, int32_t* counts) {
+  int err = 0;
+  int maxd = 0;
+  const int64_t n = V > E ? (int64_t)V : E;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    if (i < V) {
+      int32_t a = rp[i], b = rp[i + 1];
+      if (b < a) err |= 2;
+      int32_t d = b - a;
+      d = d < 0 ? 0 : d;
+      d_in[i] = d;
+      maxd = d > maxd ? d : maxd;
+      if (i == 0) {
+        if (a != 0) err |= 1;
+        if ((int64_t)rp[V] != E) err |= 4;
+      }
+    }
+    if (i < E) {
+      int32_t c = col[i];
+      if (c < 0 || c >= Vs)
+        err |= 8;
+      else
+        atomicAdd(&d_out[c], 1);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    err |= __shfl_xor(err, off, 64);
+    int m = __shfl_xor(maxd, off, 64);
+    maxd = m > maxd ? m : maxd;
+  }
+  if ((threadIdx.x & 63) == 0) {
+    if (err) atomicOr(&counts[kErrFlags], err);
+    atomicMax(&counts[kMaxDegree], maxd);
+  }
+}
+
+// per-tile digit histogram, stored digit-major: hist[digit * ntiles + tile]
+template <bool FIRST>
+__global__ __launch_bounds__(kThreads) void k_radix_hist(const int32_t* __restrict__ d_in,
+                                                         const uint32_t* __restrict__ keys,
+                                                         int32_t n, int shift,
+                                                         int32_t* __restrict__ hist, int64_t ntiles,
+                                                         const int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  __shared__ int32_t h[kBins];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t tile = blockIdx.x;
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    int64_t i = tile * kTile + j * kThreads + threadIdx.x;
+    if (i < n) {
+      uint32_t k = FIRST ? (0x7fffffffu - (uint32_t)d_in[i]) : keys[i];
+      atomicAdd(&h[(k >> shift) & (kBins - 1)], 1);
+    }
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * ntiles + tile] = h[threadIdx.x];
+}
+
+// Stable scatter.  Items are visited in index order (round j, thread t ->
+// item j*256 + t); an item's rank among equal digits inside the tile comes
+// from a wave-level match (8 ballots) plus the counts of lower waves and of
+// earlier rounds, so equal keys keep their input order.
+template <bool FIRST, bool LAST>
+__global__ __launch_bounds__(kThreads) void k_radix_scatter(
+    const int32_t* __restrict__ d_in, const uint32_t* __restrict__ keys_in,
+    const int32_t* __restrict__ vals_in, int32_t n, int shift,
+    const int32_t* __restrict__ offsets, int64_t ntiles, uint32_t* __restrict__ keys_out,
+    int32_t* __restrict__ vals_out, const int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  __shared__ int32_t running[kBins];
+  __shared__ int32_t wcnt[kThreads / 64][kBins];
+  const int t = threadIdx.x, w = t >> 6;
+  const int64_t tile = blockIdx.x;
+  running[t] = offsets[(int64_t)t * ntiles + tile];
+#pragma unroll
+  for (int k = 0; k < kThreads / 64; ++k) wcnt[k][t] = 0;
+  __syncthreads();
+  const uint64_t lt = lanemask_lt();
+  for (int j = 0; j < kItems; ++j) {
+    const int64_t i = tile * kTile + j * kThreads + t;
+    const bool valid = i < n;
+    uint32_t key = 0;
+    int32_t val = 0;
+    int dg = 0;
+    if (valid) {
+      key = FIRST ? (0x7fffffffu - (uint32_t)d_in[i]) : keys_in[i];
+      val = FIRST ? (int32_t)i : vals_in[i];
+      dg = (key >> shift) & (kBins - 1);
+    }
+    uint64_t m = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (dg >> b) & 1;
+      uint64_t bal = __ballot(valid && bit);
+      m &= bit ? bal : ~bal;
+    }
+    const int rank = __popcll(m & lt);
+    if (valid && rank == 0) wcnt[w][dg] = __popcll(m);
+    __syncthreads();
+    if (valid) {
+      int32_t pos = running[dg] + rank;
+      for (int k = 0; k < w; ++k) pos += wcnt[k][dg];
+      if (pos >= 0 && pos < n) {
+        if (!LAST) keys_out[pos] = key;
+        vals_out[pos] = val;
+      } else {
+        atomicOr(const_cast<int32_t*>(counts) + kErrFlags, kErrInternal);
+      }
+    }
+    __syncthreads();
+    int32_t tot = 0;
+#pragma unroll
+    for (int k = 0; k < kThreads / 64; ++k) {
+      tot += wcnt[k][t];
+      wcnt[k][t] = 0;
+    }
+    running[t] += tot;
+    __syncthreads();
+  }
+}
+
+template <class F>
+__global__ __launch_bounds__(kThreads) void k_scan_reduce(F f, int64_t n_host,
+                                                          const int32_t* n_dev,
+                                                          int32_t* tile_sums,
+                                                          const int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  const int64_t n = n_dev ? ((int64_t)*n_dev < n_host ? (int64_t)*n_dev : n_host) : n_host;
+  const int64_t base = blockIdx.x * (int64_t)kTile + threadIdx.x * kItems;
+  int32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kItems; ++k)
+    if (base + k < n) s += f(base + k);
+  int32_t tot;
+  block_excl_scan<kThreads>(s, &tot);
+  if (threadIdx.x == 0) tile_sums[blockIdx.x] = tot;
+}
+
+// exclusive scan of the tile sums by one workgroup of 1024 threads
+__global__ __launch_bounds__(1024) void k_scan_tilesums(int32_t* ts, int64_t nt, int32_t* total,
+                                                        const int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  __shared__ int32_t carry_s;
+  if (threadIdx.x == 0) carry_s = 0;
+  __syncthreads();
+  for (int64_t base = 0; base < nt; base += 1024) {
+    const int64_t i = base + threadIdx.x;
+    const int32_t v = i < nt ? ts[i] : 0;
+    int32_t tot;
+    const int32_t ex = block_excl_scan<1024>(v, &tot);
+    const int32_t carry = carry_s;
+    if (i < nt) ts[i] = carry + ex;
+    __syncthreads();
+    if (threadIdx.x == 0) carry_s = carry + tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && total) *total = carry_s;
+}
+
+template <class F>
+__global__ __launch_bounds__(kThreads) void k_scan_apply(F f, int64_t n_host,
+                                                         const int32_t* n_dev,
+                                                         const int32_t* tile_sums,
+                                                         int32_t* out, const int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  const int64_t n = n_dev ? ((int64_t)*n_dev < n_host ? (int64_t)*n_dev : n_host) : n_host;
+  const int64_t base = blockIdx.x * (int64_t)kTile + threadIdx.x * kItems;
+  int32_t v[kItems];
+  int32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kItems; ++k) {
+    v[k] = base + k < n ? f(base + k) : 0;
+    s += v[k];
+  }
+  int32_t tot;
+  int32_t run = block_excl_scan<kThreads>(s, &tot) + tile_sums[blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < kItems; ++k) {
+    if (base + k < n) out[base + k] = run;
+    run += v[k];
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_segments(const int32_t* __restrict__ rp,
+                                                       const int32_t* __restrict__ d_in,
+                                                       const int32_t* __restrict__ perm,
+                                                       const int32_t* __restrict__ first,
+                                                       int32_t V, int32_t T, int64_t max_seg,
+                                                       int32_t* seg_row, int32_t* seg_beg,
+                                                       int32_t* seg_end, int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < V;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t v = perm[i];
+    if (v < 0 || v >= V) {
+      atomicOr(&counts[kErrFlags], kErrInternal);
+      return;
+    }
+    const int32_t d = d_in[v];
+    const int32_t f = first[i];
+    const int32_t ns = d > T ? (d + T - 1) / T : 1;
+    if (f < 0 || (int64_t)f + ns > max_seg) {
+      atomicOr(&counts[kErrFlags], kErrInternal);
+      return;
+    }
+    const int32_t b0 = rp[v], e0 = rp[v + 1];
+    for (int32_t j = 0; j < ns; ++j) {
+      const int32_t b = b0 + j * T;
+      seg_row[f + j] = v;
+      seg_beg[f + j] = b;
+      seg_end[f + j] = (e0 - b) > T ? b + T : e0;
+    }
+    const bool split = d > T;
+    const bool next_split = (i + 1 < V) && d_in[perm[i + 1]] > T;
+    if (split && !next_split) {
+      counts[kNSplit] = (int32_t)(i + 1);
+      counts[kSSplit] = f + ns;
+    }
+    if (i == V - 1) counts[kNumSegments] = f + ns;
+  }
+}
+
+// block b holds the segments s with floor(P(s) / B) == b; consecutive
+// segments differ in P by at most seg_len + row_cost <= B, so no block id
+// is skipped.
+__global__ __launch_bounds__(kThreads) void k_blocks(const int32_t* __restrict__ P, int32_t B,
+                                                     int64_t max_seg, int64_t max_blocks,
+                                                     int32_t* block_ptr, int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  const int32_t S = counts[kNumSegments];
+  if (S > max_seg) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&counts[kErrFlags], kErrInternal);
+    return;
+  }
+  for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < S;
+       s += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t b = P[s] / B;
+    if (b < 0 || b >= max_blocks) {
+      atomicOr(&counts[kErrFlags], kErrInternal);
+      return;
+    }
+    if (s == 0 || P[s - 1] / B != b) block_ptr[b] = (int32_t)s;
+    if (s == S - 1) {
+      block_ptr[b + 1] = S;
+      counts[kNumBlocks] = b + 1;
+    }
+  }
+}
+
+template <class F>
+void scan(F f, int64_t n_host, const int32_t* n_dev, int32_t* out, int32_t* total,
+          int32_t* tile_sums, const int32_t* counts, hipStream_t st) {
+  const int64_t nt = cdiv(n_host, kTile);
+  if (nt == 0) return;
+  hipLaunchKernelGGL(k_scan_reduce<F>, dim3(nt), dim3(kThreads), 0, st, f, n_host, n_dev,
+                     tile_sums, counts);
+  hipLaunchKernelGGL(k_scan_tilesums, dim3(1), dim3(1024), 0, st, tile_sums, nt, total, counts);
+  hipLaunchKernelGGL(k_scan_apply<F>, dim3(nt), dim3(kThreads), 0, st, f, n_host, n_dev,
+                     tile_sums, out, counts);
+}
+
+inline unsigned grid_for(int64_t n, int64_t cap = 16384) {
+  int64_t g = cdiv(n, kThreads);
+  if (g < 1) g = 1;
+  return (unsigned)(g < cap ? g : cap);
+}
+
+}  // namespace
+
+bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t c,
+                 PlanLayout* L) {
+  if (V < 0 || Vs < 0 || E < 0 || E >= (int64_t(1) << 31) || T <= 0 || c <= 0 || B < T + c)
+    return false;
+  L->max_segments = (int64_t)V + cdiv(E, T);
+  const int64_t ptot = E + (int64_t)c * L->max_segments;
+  if (ptot >= (int64_t(1) << 31) - 1) return false;
+  L->max_blocks = ptot / B + 1;
+  L->max_split = E / (int64_t(T) + 1) < V ? E / (int64_t(T) + 1) : V;
+  L->max_split_segments = cdiv(E, T) + L->max_split;
+  L->radix_tiles = cdiv(V, kTile);
+  L->scan_tiles_rows = cdiv(V, kTile);
+  L->scan_tiles_segs = cdiv(L->max_segments, kTile);
+  const int64_t hist_n = (int64_t)kBins * L->radix_tiles;
+  int64_t scan_tiles = cdiv(hist_n, kTile);
+  if (L->scan_tiles_rows > scan_tiles) scan_tiles = L->scan_tiles_rows;
+  if (L->scan_tiles_segs > scan_tiles) scan_tiles = L->scan_tiles_segs;
+
+  size_t o = 0;
+  auto take = [&](int64_t n_int) {
+    size_t at = o;
+    o = align256(o + (size_t)n_int * 4);
+    return at;
+  };
+  L->off_d_in = take(V);
+  L->off_d_out = take(Vs);
+  L->off_perm = take(V);
+  L->off_first = take((int64_t)V + 1);
+  L->off_seg_row = take(L->max_segments);
+  L->off_seg_beg = take(L->max_segments);
+  L->off_seg_end = take(L->max_segments);
+  L->off_block_ptr = take(L->max_blocks + 1);
+  L->off_counts = take(kCountSlots);
+  L->off_scratch = o;
+  // scratch: keysA, valsA, keysB, valsB, hist, tile sums, cost prefix
+  take(V); take(V); take(V); take(V);
+  take(hist_n);
+  take(scan_tiles + 1);
+  take(L->max_segments);
+  L->scratch_bytes = o - L->off_scratch;
+  L->total = o;
+  return true;
+}
+
+hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_t st) {
+  const int32_t V = p.num_dst, Vs = p.num_src, T = p.seg_len;
+  const int64_t E = p.num_edges;
+  char* sc = static_cast<char*>(p.scratch);
+  size_t o = 0;
+  auto take = [&](int64_t n_int) {
+    char* at = sc + o;
+    o = align256(o + (size_t)n_int * 4);
+    return at;
+  };
+  uint32_t* keysA = reinterpret_cast<uint32_t*>(take(V));
+  int32_t* valsA = reinterpret_cast<int32_t*>(take(V));
+  uint32_t* keysB = reinterpret_cast<uint32_t*>(take(V));
+  int32_t* valsB = reinterpret_cast<int32_t*>(take(V));
+  const int64_t ntiles = L.radix_tiles;
+  int32_t* hist = reinterpret_cast<int32_t*>(take((int64_t)kBins * ntiles));
+  int64_t scan_tiles = cdiv((int64_t)kBins * ntiles, kTile);
+  if (L.scan_tiles_rows > scan_tiles) scan_tiles = L.scan_tiles_rows;
+  if (L.scan_tiles_segs > scan_tiles) scan_tiles = L.scan_tiles_segs;
+  int32_t* tile_sums = reinterpret_cast<int32_t*>(take(scan_tiles + 1));
+  int32_t* P = reinterpret_cast<int32_t*>(take(L.max_segments));
+
+  hipLaunchKernelGGL(k_zero, dim3(1), dim3(64), 0, st, p.counts, (int64_t)kCountSlots);
+  if (Vs > 0) hipLaunchKernelGGL(k_zero, dim3(grid_for(Vs)), dim3(kThreads), 0, st, p.d_out, (int64_t)Vs);
+  if (V == 0) return hipGetLastError();
+  hipLaunchKernelGGL(k_degrees, dim3(grid_for(V > E ? V : E)), dim3(kThreads), 0, st, p.row_ptr,
+                     p.col_idx, V, Vs, E, p.d_in, p.d_out, p.counts);
+
+  // degree order: 4 stable passes of 8 bits over key = 0x7fffffff - d_in
+  const uint32_t* kin[4] = {nullptr, keysA, keysB, keysA};
+  const int32_t* vin[4] = {nullptr, valsA, valsB, valsA};
+  uint32_t* kout[4] = {keysA, keysB, keysA, nullptr};
+  int32_t* vout[4] = {valsA, valsB, valsA, p.perm};
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 8 * pass;
+    if (pass == 0)
+      hipLaunchKernelGGL(k_radix_hist<true>, dim3(ntiles), dim3(kThreads), 0, st, p.d_in,
+                         kin[pass], V, shift, hist, ntiles, p.counts);
+    else
+      hipLaunchKernelGGL(k_radix_hist<false>, dim3(ntiles), dim3(kThreads), 0, st, p.d_in,
+                         kin[pass], V, shift, hist, ntiles, p.counts);
+    scan(ArrF{hist}, (int64_t)kBins * ntiles, nullptr, hist, nullptr, tile_sums, p.counts, st);
+    if (pass == 0)
+      hipLaunchKernelGGL((k_radix_scatter<true, false>), dim3(ntiles), dim3(kThreads), 0, st,
+                         p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
+                         vout[pass], p.counts);
+    else if (pass < 3)
+      hipLaunchKernelGGL((k_radix_scatter<false, false>), dim3(ntiles), dim3(kThreads), 0, st,
+                         p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
+                         vout[pass], p.counts);
+    else
+      hipLaunchKernelGGL((k_radix_scatter<false, true>), dim3(ntiles), dim3(kThreads), 0, st,
+                         p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
+                         vout[pass], p.counts);
+  }
+
+  // segments per row in perm order -> row_seg_first (total at [V])
+  scan(NsegF{p.d_in, p.perm, T}, V, nullptr, p.row_seg_first, p.row_seg_first + V, tile_sums,
+       p.counts, st);
+  hipLaunchKernelGGL(k_segments, dim3(grid_for(V)), dim3(kThreads), 0, st, p.row_ptr, p.d_in,
+                     p.perm, p.row_seg_first, V, T, L.max_segments, p.seg_row, p.seg_beg,
+                     p.seg_end, p.counts);
+  // cost prefix over segments -> row blocks
+  scan(CostF{p.seg_beg, p.seg_end, p.row_cost}, L.max_segments, p.counts + kNumSegments, P,
+       nullptr, tile_sums, p.counts, st);
+  hipLaunchKernelGGL(k_blocks, dim3(grid_for(L.max_segments)), dim3(kThreads), 0, st, P,
+                     p.block_cost, L.max_segments, L.max_blocks, p.block_ptr, p.counts);
+  return hipGetLastError();
+}
+
+}  // namespace saga

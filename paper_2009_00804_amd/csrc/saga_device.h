@@ -1,0 +1,97 @@
+// Device-side helpers shared by the HIP kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace saga {
+
+constexpr int kWave = 64;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// --------------------------------------------------------------------------
+// bfloat16 storage: 16-bit patterns in uint16_t
+// --------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// round to nearest, ties to even; NaN stays a quiet NaN
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// A 16-byte slice of a feature row, widened to float.
+template <typename T> struct Vec16;
+
+template <> struct Vec16<float> {
+  static constexpr int N = 4;
+  __device__ __forceinline__ static void load(const float* p, float (&x)[4]) {
+    float4 v = *reinterpret_cast<const float4*>(p);
+    x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+  }
+  __device__ __forceinline__ static void store(float* p, const float (&x)[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+  }
+  __device__ __forceinline__ static void store_n(float* p, const float (&x)[4], int n) {
+    for (int i = 0; i < 4; ++i)
+      if (i < n) p[i] = x[i];
+  }
+};
+
+template <> struct Vec16<uint16_t> {
+  static constexpr int N = 8;
+  __device__ __forceinline__ static void load(const uint16_t* p, float (&x)[8]) {
+    uint4 v = *reinterpret_cast<const uint4*>(p);
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+  __device__ __forceinline__ static void store(uint16_t* p, const float (&x)[8]) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = static_cast<uint32_t>(f32_to_bf16(x[2 * i])) |
+             (static_cast<uint32_t>(f32_to_bf16(x[2 * i + 1])) << 16);
+    *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  __device__ __forceinline__ static void store_n(uint16_t* p, const float (&x)[8], int n) {
+    for (int i = 0; i < 8; ++i)
+      if (i < n) p[i] = f32_to_bf16(x[i]);
+  }
+};
+
+// --------------------------------------------------------------------------
+// activations (codes match saga_act)
+// --------------------------------------------------------------------------
+__device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + __expf(-x)); }
+
+__device__ __forceinline__ float apply_act(int act, float x) {
+  switch (act) {
+    case 1: return x > 0.0f ? x : 0.0f;                 // ReLU, +0 for x <= 0
+    case 2: return x > 0.0f ? x : expm1f(x);            // ELU(alpha = 1)
+    case 3: return 1.0f / (1.0f + expf(-x));            // sigmoid
+    case 4: return tanhf(x);
+    default: return x;
+  }
+}
+
+__device__ __forceinline__ float rsqrt_deg(int d) {
+  return d > 0 ? 1.0f / sqrtf(static_cast<float>(d)) : 0.0f;
+}
+
+// lanes of the wave with index below the caller's
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const int lane = threadIdx.x & 63;
+  return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+}  // namespace saga

@@ -1,0 +1,100 @@
+// Internal interfaces between the C-ABI layer and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "saga.h"
+
+namespace saga {
+
+// counters kept at plan->counts
+enum Count : int {
+  kNumSegments = 0,
+  kNumBlocks = 1,
+  kNSplit = 2,
+  kSSplit = 3,
+  kErrFlags = 4,
+  kMaxDegree = 5,
+  kCountSlots = 8
+};
+// error bits in counts[kErrFlags]: 1, 2, 4, 8 are CSR errors (see saga.h);
+// this one marks a broken internal invariant of the plan builder
+constexpr int kErrInternal = 1 << 16;
+
+// ---- plan.hip ----
+struct PlanLayout {
+  size_t off_d_in, off_d_out, off_perm, off_first, off_seg_row, off_seg_beg, off_seg_end,
+      off_block_ptr, off_counts, off_scratch, scratch_bytes, total;
+  int64_t max_segments, max_blocks, max_split, max_split_segments;
+  int64_t radix_tiles, scan_tiles_rows, scan_tiles_segs;
+};
+
+bool plan_layout(int32_t num_dst, int32_t num_src, int64_t num_edges, int32_t seg_len,
+                 int32_t block_cost, int32_t row_cost, PlanLayout* L);
+
+hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_t st);
+
+// ---- gather.hip ----
+struct GatherArgs {
+  // plan
+  const int32_t* row_ptr;
+  const int32_t* col_idx;
+  const int32_t* d_in;
+  const int32_t* d_out;
+  const int32_t* perm;
+  const int32_t* row_seg_first;
+  const int32_t* seg_row;
+  const int32_t* seg_beg;
+  const int32_t* seg_end;
+  const int32_t* block_ptr;
+  const int32_t* counts;
+  int64_t max_blocks;
+  int64_t max_split;
+  // op
+  int msg, reduce, dtype, heads, head_mean, dst_norm, act;
+  float neg_slope;
+  int feat;        // F (input feature columns)
+  int out_cols;    // F or F/heads
+  // inputs
+  const void* src; int64_t ld_src;
+  const float* el; int64_t ld_el;
+  const float* er; int64_t ld_er;
+  const float* gsrc; int64_t ld_gsrc;
+  const float* gdst; int64_t ld_gdst;
+  const float* efeat; int64_t ld_efeat; int fe;
+  const float* w_edge;
+  const float* gate_bias;
+  const float* bias;
+  // output
+  void* out; int64_t ld_out;
+  // split-row partials (float32), stride pstride floats per segment
+  float* partial; int64_t pstride;
+  int pcols;       // partial accumulator columns; softmax m/l follow at pcols
+};
+
+int gather_partial_cols(int64_t feat);
+size_t gather_partial_stride(const saga_edge_op& op, int64_t feat);
+hipError_t launch_gather(const GatherArgs& a, hipStream_t st);
+
+// ---- gemm.hip ----
+struct GemmArgs {
+  int dtype, mode, act;
+  int64_t M, N, K, K2;
+  const void* a; int64_t lda;
+  const void* w; int64_t ldw;
+  const void* a2; int64_t lda2;
+  const void* w2; int64_t ldw2;
+  const float* bias;
+  const float* bias2;
+  const int32_t* row_scale_deg;
+  void* out; int64_t ldo;
+};
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t st);
+
+// ---- layer helpers (gather.hip) ----
+hipError_t launch_fold_attention(const float* w, int64_t K, int64_t F, int heads, const float* al,
+                                 const float* ar, float* w_ext, int64_t ld_ext, hipStream_t st);
+
+}  // namespace saga

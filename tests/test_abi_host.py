@@ -1,0 +1,164 @@
+"""The C-ABI library on the host (no GPU needed): it loads, exports every
+entry point include/saga.h declares, and rejects bad arguments before any
+kernel is launched."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def S():
+    import paper_2009_00804_amd.saga as S
+
+    if not os.path.exists(S.LIB_PATH):
+        from paper_2009_00804_amd import build
+
+        build.build()
+    S.lib()
+    return S
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "saga.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(saga_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for want in ("saga_plan_build", "saga_scatter_apply_edge_gather", "saga_apply_vertex",
+                 "saga_layer"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol(S):
+    L = S.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+    assert sorted(S.EXPORTS) == _declared()
+
+
+def test_version_and_status_strings(S):
+    assert "gfx950" in S.saga_version()
+    L = S.lib()
+    assert L.saga_status_str(S.SAGA_OK) == b"ok"
+    assert L.saga_status_str(S.SAGA_EGRAPH) == b"invalid graph"
+
+
+def test_plan_workspace_size_rules(S):
+    n = S.saga_plan_workspace_size(1000, 1000, 5000)
+    assert n > 0 and n % 256 == 0
+    assert S.saga_plan_workspace_size(0, 0, 0) >= 0
+    for args, opts in [((10, 10, -1), None), ((10, 10, 1 << 31), None),
+                       ((10, 10, 5), S.saga_plan_opts(64, 32, 4))]:
+        with pytest.raises(S.SagaError) as e:
+            S.saga_plan_workspace_size(*args, opts)
+        assert e.value.status == S.SAGA_EINVAL
+
+
+def test_plan_build_rejects_bad_arguments_without_launching(S):
+    ws = C.create_string_buffer(1 << 16)
+    with pytest.raises(S.SagaError) as e:
+        S.saga_plan_build(10, 10, 5, None, None, None, C.addressof(ws), 1 << 16, None)
+    assert e.value.status == S.SAGA_EINVAL
+    with pytest.raises(S.SagaError) as e:   # workspace too small
+        S.saga_plan_build(10, 10, 5, 1024, 2048, None, 4096, 16, None)
+    assert e.value.status == S.SAGA_EWORKSPACE
+
+
+def _fake_plan(S, V=16, E=40):
+    p = S.saga_plan()
+    p.num_dst = p.num_src = V
+    p.num_edges = E
+    p.row_ptr, p.col_idx = 0x10000, 0x20000
+    for f in ("d_in", "d_out", "perm", "row_seg_first", "seg_row", "seg_beg", "seg_end",
+              "block_ptr", "counts"):
+        setattr(p, f, 0x30000)
+    p.max_split_segments = 0
+    return p
+
+
+def test_gather_rejects_bad_arguments(S):
+    p = _fake_plan(S)
+    op = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 0, 0.2, 0)
+    inp = S.saga_edge_inputs()
+    out = S.saga_mat(0x40000, 16, 8, 8)
+    L = S.lib()
+
+    def call(o=op, i=inp, ou=out):
+        return L.saga_scatter_apply_edge_gather(C.byref(p), C.byref(o), C.byref(i), ou, None, 0, None)
+
+    inp.src = S.saga_cmat(0x50000, 16, 8, 8)
+    # wrong source shape
+    inp.src = S.saga_cmat(0x50000, 15, 8, 8)
+    assert call() == S.SAGA_EINVAL
+    # ld < cols
+    inp.src = S.saga_cmat(0x50000, 16, 8, 4)
+    assert call() == S.SAGA_EINVAL
+    # misaligned base
+    inp.src = S.saga_cmat(0x50004, 16, 8, 8)
+    assert call() == S.SAGA_EINVAL
+    # row pitch not a multiple of 16 bytes
+    inp.src = S.saga_cmat(0x50000, 16, 3, 3)
+    assert call(ou=S.saga_mat(0x40000, 16, 3, 4)) == S.SAGA_EINVAL
+    inp.src = S.saga_cmat(0x50000, 16, 8, 8)
+    # output overlapping the source
+    assert call(ou=S.saga_mat(0x50000 + 64, 16, 8, 8)) == S.SAGA_EINVAL
+    # unsupported combinations
+    bad = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SOFTMAX, S.SAGA_F32, 1, 0, 0, 0.2, 0)
+    assert call(o=bad) == S.SAGA_EUNSUPPORTED
+    bad = S.saga_edge_op(S.SAGA_MSG_GAT, S.SAGA_RED_SOFTMAX, S.SAGA_BF16, 2, 0, 0, 0.2, 0)
+    inp.src = S.saga_cmat(0x50000, 16, 8, 8)
+    assert call(o=bad) == S.SAGA_EUNSUPPORTED
+    bad = S.saga_edge_op(S.SAGA_MSG_GAT, S.SAGA_RED_SOFTMAX, S.SAGA_F32, 3, 0, 0, 0.2, 0)
+    assert call(o=bad) == S.SAGA_EUNSUPPORTED   # 3 heads do not divide 8 columns
+    bad = S.saga_edge_op(S.SAGA_MSG_GATED, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 0, 0.2, 0)
+    assert call(o=bad) == S.SAGA_EUNSUPPORTED   # gated needs F == 64
+    assert b"F == 64" in L.saga_last_error()
+
+
+def test_gemm_rejects_bad_arguments(S):
+    L = S.lib()
+    op = S.saga_gemm_op(S.SAGA_F32, S.SAGA_GEMM_PLAIN, 0, None)
+    a = S.saga_cmat(0x10000, 100, 32, 32)
+    w = S.saga_cmat(0x20000, 32, 16, 16)
+    none = S.saga_cmat(None, 0, 0, 0)
+    out = S.saga_mat(0x30000, 100, 16, 16)
+    f = lambda *args: L.saga_apply_vertex(C.byref(args[0]), *args[1:])  # noqa: E731
+    assert f(op, a, S.saga_cmat(0x20000, 31, 16, 16), none, none, None, None, out, None) == S.SAGA_EINVAL
+    assert f(op, a, w, none, none, None, None, S.saga_mat(0x30000, 99, 16, 16), None) == S.SAGA_EINVAL
+    assert f(op, a, w, none, none, None, None, S.saga_mat(0x10000 + 128, 100, 16, 16), None) == S.SAGA_EINVAL
+    gru = S.saga_gemm_op(S.SAGA_F32, S.SAGA_GEMM_GRU, 0, None)
+    w3 = S.saga_cmat(0x20000, 32, 60, 60)
+    a2 = S.saga_cmat(0x60000, 100, 20, 20)
+    w23 = S.saga_cmat(0x70000, 20, 60, 60)
+    assert f(gru, a, w3, a2, w23, None, None, S.saga_mat(0x30000, 100, 20, 20), None) == S.SAGA_EUNSUPPORTED
+    bad_mode = S.saga_gemm_op(S.SAGA_F32, 7, 0, None)
+    assert f(bad_mode, a, w, none, none, None, None, out, None) == S.SAGA_EINVAL
+
+
+def test_layer_rejects_bad_descriptors(S):
+    p = _fake_plan(S)
+    L = S.lib()
+    d = S.saga_layer_desc()
+    d.kind = S.SAGA_LAYER_GAT
+    d.dtype = S.SAGA_BF16
+    d.in_feat, d.out_feat, d.heads = 8, 8, 2
+    d.w = d.attn_l = d.attn_r = 0x1000
+    n = C.c_size_t()
+    assert L.saga_layer_workspace_size(C.byref(p), C.byref(d), C.byref(n)) == S.SAGA_EUNSUPPORTED
+    d.kind = 9
+    assert L.saga_layer_workspace_size(C.byref(p), C.byref(d), C.byref(n)) == S.SAGA_EINVAL
+    d.kind = S.SAGA_LAYER_GCN
+    d.dtype = S.SAGA_F32
+    assert L.saga_layer_workspace_size(C.byref(p), C.byref(d), C.byref(n)) == S.SAGA_OK
+    assert n.value > 0
+    # workspace missing
+    x = S.saga_cmat(0x50000, 16, 8, 8)
+    out = S.saga_mat(0x60000, 16, 8, 8)
+    none = S.saga_cmat(None, 0, 0, 0)
+    assert L.saga_layer(C.byref(p), C.byref(d), x, none, out, None, 0, None) == S.SAGA_EWORKSPACE

@@ -1,0 +1,119 @@
+"""The 2^21-vertex R-MAT GCN (50 edges per vertex + self-loops, 602 -> 128
+-> 41) at full size, in the launch configuration the benchmark times.
+
+The oracle cannot evaluate 2M rows, so it checks: the whole plan bit for bit
+(integer layout), sampled output rows of layer 1 (including the largest hub
+and split rows), sampled rows of the two-layer model whose two-hop
+neighbourhoods are small, and properties that hold at any size (finite
+outputs, run-to-run identical bytes)."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import dev_int, lib, to_np
+from helpers import BF16_TOL, FP32_TOL, rel_err
+from oracle import saga_oracle as O
+from synth import configs as C
+from synth import tensors as T
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+@pytest.fixture(scope="module")
+def big():
+    print("generating the 2^21-vertex R-MAT workload ...", flush=True)
+    g = C.build("gcn_rmat")
+    print(f"V={g['num_vertices']} E={g['num_edges']}", flush=True)
+    return g
+
+
+@pytest.fixture(scope="module")
+def dev_graph(big):
+    S = lib()
+    rp = dev_int(big["row_ptr"])
+    col = dev_int(big["col_idx"])
+    return S.Graph(rp, col)
+
+
+def _samples(g, k=48, seed=0):
+    rp = g["row_ptr"].astype(np.int64)
+    d = np.diff(rp)
+    rng = np.random.default_rng(seed)
+    rows = set(rng.integers(0, len(d), k).tolist())
+    rows.add(int(np.argmax(d)))                    # the largest hub
+    split = np.flatnonzero(d > 512)
+    rows.update(rng.choice(split, 8, replace=False).tolist())
+    rows.update(np.flatnonzero(d == d.min())[:4].tolist())
+    return np.array(sorted(rows))
+
+
+def _small_two_hop(g, k=24, limit=40000, seed=1):
+    rp = g["row_ptr"].astype(np.int64)
+    col = g["col_idx"]
+    d = np.diff(rp)
+    rng = np.random.default_rng(seed)
+    out = []
+    for v in rng.permutation(len(d)):
+        nb = col[rp[v]:rp[v + 1]]
+        if d[nb].sum() <= limit:
+            out.append(int(v))
+        if len(out) == k:
+            break
+    return np.array(sorted(out))
+
+
+def test_full_plan_bit_exact(big, dev_graph):
+    got = {k: v.cpu().numpy().astype(np.int64) for k, v in dev_graph.arrays().items()}
+    p = dev_graph.plan
+    print("oracle plan ...", flush=True)
+    want = O.plan(big["row_ptr"], big["col_idx"], big["num_vertices"], p.seg_len, p.block_cost,
+                  p.row_cost)
+    for k in ("d_in", "d_out", "perm", "row_seg_first", "seg_row", "seg_beg", "seg_end",
+              "block_ptr"):
+        assert np.array_equal(got[k], want[k]), k
+    assert dev_graph.counts.n_split == want["n_split"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_full_gcn_sampled(big, dev_graph, dtype):
+    from paper_2009_00804_amd import layers as LY
+
+    g = big
+    f_in, hid, f_out = g["dims"]
+    if dtype == "f32":
+        X = torch.from_numpy(g["X"]).cuda()[:, :f_in]   # ld 604: 16-byte rows
+        Xo = g["X"][:, :f_in]
+        W1, W2 = g["W1"], g["W2"]
+        tdt, tol = torch.float32, FP32_TOL
+    else:
+        C.add_bf16_variant(g)
+        bits = torch.from_numpy(g["X_bf16"].view(np.int16)).view(torch.bfloat16)
+        X = bits.cuda()[:, :f_in]                        # ld 608
+        Xo = T.bf16_to_f32(g["X_bf16"][:, :f_in])
+        W1, W2 = g["W1_bf"], g["W2_bf"]
+        tdt, tol = torch.bfloat16, BF16_TOL
+    model = LY.gcn2(dev_graph, torch.from_numpy(W1), torch.from_numpy(g["b1"]),
+                    torch.from_numpy(W2), torch.from_numpy(g["b2"]), dtype=tdt, out_ld=44 if dtype == "f32" else 48)
+    print(f"running the {dtype} forward on the GPU", flush=True)
+    y = LY.run(model, X).clone()
+    h1 = model[0].out
+    torch.cuda.synchronize()
+    assert torch.isfinite(y.float()).all()
+    y_again = LY.run(model, X)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y_again)                 # deterministic bytes
+
+    rp, col = g["row_ptr"], g["col_idx"]
+    rows = _samples(g)
+    print(f"oracle layer 1 on {len(rows)} sampled rows", flush=True)
+    ref1 = O.gcn_layer(rp, col, Xo, W1, g["b1"], "relu", rows=rows)
+    got1 = to_np(h1[torch.from_numpy(rows).cuda()])
+    e1 = rel_err(got1, ref1)
+    rows2 = _small_two_hop(g)
+    print(f"oracle two layers on {len(rows2)} sampled rows", flush=True)
+    ref2 = O.gcn_2layer(dict(g, X=Xo), X=Xo, W1=W1, W2=W2, rows=rows2)
+    got2 = to_np(y[torch.from_numpy(rows2).cuda()])
+    e2 = rel_err(got2, ref2)
+    print(f"{dtype}: layer-1 sampled err {e1:.3e}, two-layer sampled err {e2:.3e}", flush=True)
+    assert e1 <= tol
+    assert e2 <= (tol if dtype == "f32" else 2 * tol)

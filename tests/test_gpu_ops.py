@@ -1,0 +1,294 @@
+"""Op-level parity of the HIP kernels against the CPU oracle: the fused
+Scatter+ApplyEdge+Gather for every reduction and message kind, and the
+ApplyVertex GEMM with its epilogues, on seeded inputs that span several
+tiles, a ragged tail, empty rows and split (long) rows."""
+import ctypes as C
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import dev_padded, device, graph, lib, to_np
+from helpers import BF16_TOL, FP32_TOL, edges_to_csr, rel_err, tiny_graphs
+from oracle import saga_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+ACTS = {"none": 0, "relu": 1, "elu": 2, "sigmoid": 3, "tanh": 4}
+
+
+def _power_law(seed=0):
+    """R-MAT graph with many empty rows and hub rows longer than seg_len."""
+    from synth import configs as C_
+
+    g = C_.build("sage_rmat", small=True)
+    return g["row_ptr"], g["col_idx"], g["num_vertices"]
+
+
+def _bf16_round(a):
+    from synth import tensors as T
+
+    return T.bf16_to_f32(T.bf16_bits(np.asarray(a, np.float32)))
+
+
+def run_gather(g, src_t, op_kw, out_cols, out_dtype, el=None, er=None, bias=None, extra=None):
+    S = lib()
+    op = S.saga_edge_op()
+    op.msg = op_kw.get("msg", S.SAGA_MSG_COPY)
+    op.reduce = op_kw["reduce"]
+    op.dtype = S.dtype_code(src_t.dtype)
+    op.heads = op_kw.get("heads", 1)
+    op.head_mean = op_kw.get("head_mean", 0)
+    op.dst_norm = op_kw.get("dst_norm", 0)
+    op.neg_slope = op_kw.get("neg_slope", 0.2)
+    op.act = ACTS[op_kw.get("act", "none")]
+    inp = S.saga_edge_inputs()
+    inp.src = S.cmat(src_t)
+    inp.el = S.cmat(el)
+    inp.er = S.cmat(er)
+    if extra:
+        for k, v in extra.items():
+            setattr(inp, k, v)
+    bias_t = None
+    if bias is not None:
+        bias_t = torch.from_numpy(np.asarray(bias, np.float32)).to(device())
+        inp.bias = bias_t.data_ptr()
+    out = dev_padded(np.zeros((g.num_dst, out_cols)), dtype=out_dtype, fill=7.0)
+    n = S.saga_gather_workspace_size(g.plan, op, src_t.shape[1])
+    ws = S.workspace(n, device())
+    S.saga_scatter_apply_edge_gather(g.plan, op, inp, S.mat(out), C.c_void_p(ws.data_ptr()),
+                                     ws.numel(), S.stream_handle())
+    torch.cuda.synchronize()
+    return out
+
+
+def _ref_simple(rp, col, X, reduce, msg, dst_norm, bias, act, nsrc):
+    d_out = O.out_degrees(col, nsrc)
+    scale = O.degree_scale(d_out) if msg == "src_norm" else None
+    r = O.gather(rp, col, X, reduce, src_scale=scale)
+    if dst_norm:
+        r = r * O.degree_scale(O.in_degrees(rp))[:, None]
+    if bias is not None:
+        r = r + np.asarray(bias, np.float64)[None, :]
+    return O.ACTS[act](r)
+
+
+GRAPHS = {"tiny_" + c[0]: c for c in tiny_graphs()}
+
+
+def _get_graph(name, seg_len=16, block_cost=128):
+    if name == "rmat":
+        rp, col, n = _power_law()
+    else:
+        _, n, src, dst = GRAPHS[name]
+        rp, col, _ = edges_to_csr(n, src, dst)
+    return rp, col, n, graph(rp, col, num_src=n, seg_len=seg_len, block_cost=block_cost, row_cost=4)
+
+
+@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_star", "tiny_random"])
+@pytest.mark.parametrize("F", [1, 8, 16, 41, 64, 128, 256, 300])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gather_sum_mean(gname, F, dtype):
+    S = lib()
+    rp, col, n, g = _get_graph(gname)
+    rng = np.random.default_rng(F)
+    X = rng.standard_normal((n, F)).astype(np.float32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    if dtype == "bf16":
+        X = _bf16_round(X)
+    Xt = dev_padded(X, tdt)
+    tol = FP32_TOL if dtype == "f32" else BF16_TOL
+    bias = rng.standard_normal(F)
+    cases = [
+        ("sum", "copy", 0, None, "none"),
+        ("sum", "src_norm", 1, bias, "relu"),
+        ("mean", "copy", 0, bias, "tanh"),
+    ]
+    for red, msg, dn, b, act in cases:
+        print(f"gather {gname} F={F} {dtype} {red} {msg} dst_norm={dn} act={act}", flush=True)
+        out = run_gather(g, Xt, dict(reduce={"sum": S.SAGA_RED_SUM, "mean": S.SAGA_RED_MEAN}[red],
+                                     msg={"copy": S.SAGA_MSG_COPY, "src_norm": S.SAGA_MSG_SRC_NORM}[msg],
+                                     dst_norm=dn, act=act), F, tdt, bias=b)
+        ref = _ref_simple(rp, col, X, red, msg, dn, b, act, n)
+        err = rel_err(to_np(out), ref)
+        assert err <= tol, (red, msg, err)
+
+
+@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_star"])
+@pytest.mark.parametrize("F", [4, 41, 128, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gather_max_bit_exact(gname, F, dtype):
+    S = lib()
+    rp, col, n, g = _get_graph(gname)
+    rng = np.random.default_rng(100 + F)
+    X = rng.standard_normal((n, F)).astype(np.float32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    if dtype == "bf16":
+        X = _bf16_round(X)
+    print(f"gather max {gname} F={F} {dtype}", flush=True)
+    out = run_gather(g, dev_padded(X, tdt), dict(reduce=S.SAGA_RED_MAX), F, tdt)
+    ref = O.gather(rp, col, X, "max")
+    got = to_np(out)
+    assert np.array_equal(got, ref)   # exact: the max is one of the inputs (0 for empty rows)
+
+
+@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_random"])
+@pytest.mark.parametrize("heads,D,head_mean", [(8, 8, 0), (8, 8, 1), (2, 4, 0), (4, 16, 1), (1, 4, 0)])
+def test_gather_attention(gname, heads, D, head_mean):
+    S = lib()
+    rp, col, n, g = _get_graph(gname)
+    rng = np.random.default_rng(7 * heads + D)
+    F = heads * D
+    Zx = rng.standard_normal((n, F + 2 * heads)).astype(np.float32)
+    Z = Zx[:, :F]
+    el = Zx[:, F:F + heads]
+    er = Zx[:, F + heads:]
+    zt = dev_padded(Zx, torch.float32)
+    bias = rng.standard_normal(D if head_mean else F)
+    print(f"gather attention {gname} H={heads} D={D} mean={head_mean}", flush=True)
+    out = run_gather(g, zt[:, :F], dict(msg=S.SAGA_MSG_GAT, reduce=S.SAGA_RED_SOFTMAX, heads=heads,
+                                        head_mean=head_mean, act="elu", neg_slope=0.2),
+                     D if head_mean else F, torch.float32, el=zt[:, F:F + heads],
+                     er=zt[:, F + heads:], bias=bias)
+    o = O.attention_gather(rp, col, Z, el, er, heads, 0.2)
+    if head_mean:
+        o = o.reshape(n, heads, D).mean(axis=1)
+    ref = O.elu(o + bias[None, :])
+    assert rel_err(to_np(out), ref) <= FP32_TOL
+
+
+@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_chain"])
+def test_gather_gated(gname):
+    """Gated messages: the kernel gets the split form (gate_src = H W_src,
+    gate_dst = H W_dst, W_edge); the oracle evaluates the concatenated
+    definition [h_u | h_v | e_uv] W_e + b_e directly."""
+    S = lib()
+    rp, col, n, g = _get_graph(gname)
+    E = len(col)
+    F, Fe = 64, 16
+    rng = np.random.default_rng(11)
+    H = rng.standard_normal((n, F)).astype(np.float32)
+    Ef = rng.standard_normal((E, Fe)).astype(np.float32)
+    W_e = (rng.standard_normal((2 * F + Fe, F)) * 0.1).astype(np.float32)
+    b_e = rng.standard_normal(F).astype(np.float32)
+    Gs = (H.astype(np.float64) @ W_e[:F]).astype(np.float32)
+    Gd = (H.astype(np.float64) @ W_e[F:2 * F]).astype(np.float32)
+    t = lambda a: dev_padded(a, torch.float32)  # noqa: E731
+    Ht, Gst, Gdt, Eft = t(H), t(Gs), t(Gd), t(Ef)
+    wt = torch.from_numpy(W_e[2 * F:].copy()).to(device())
+    bt = torch.from_numpy(b_e).to(device())
+    extra = dict(gate_src=S.cmat(Gst), gate_dst=S.cmat(Gdt), edge_feat=S.cmat(Eft),
+                 w_edge=wt.data_ptr(), gate_bias=bt.data_ptr())
+    print(f"gather gated {gname}", flush=True)
+    out = run_gather(g, Ht, dict(msg=S.SAGA_MSG_GATED, reduce=S.SAGA_RED_SUM), F, torch.float32,
+                     extra=extra)
+    ref = O.gated_gather(rp, col, H, Ef, W_e, b_e)
+    assert rel_err(to_np(out), ref) <= FP32_TOL
+
+
+def test_gather_deterministic():
+    S = lib()
+    rp, col, n, g = _get_graph("rmat")
+    X = np.random.default_rng(5).standard_normal((n, 128)).astype(np.float32)
+    Xt = dev_padded(X)
+    a = run_gather(g, Xt, dict(reduce=S.SAGA_RED_SUM, dst_norm=1), 128, torch.float32)
+    b = run_gather(g, Xt, dict(reduce=S.SAGA_RED_SUM, dst_norm=1), 128, torch.float32)
+    assert torch.equal(a.cpu(), b.cpu())
+
+
+# --------------------------------------------------------------------------
+# ApplyVertex GEMM
+# --------------------------------------------------------------------------
+def run_gemm(A, W, dtype, bias=None, act="none", deg=None, A2=None, W2=None, bias2=None,
+             mode="plain", out_cols=None):
+    S = lib()
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    op = S.saga_gemm_op()
+    op.dtype = S.dtype_code(tdt)
+    op.mode = {"plain": 0, "concat": 1, "gru": 2}[mode]
+    op.act = ACTS[act]
+    dev = device()
+    keep = []
+    if deg is not None:
+        dt = torch.from_numpy(np.asarray(deg, np.int32)).to(dev)
+        keep.append(dt)
+        op.row_scale_deg = dt.data_ptr()
+    At = dev_padded(A, tdt)
+    Wt = torch.from_numpy(np.asarray(W, np.float32)).to(tdt).to(dev)
+    A2t = dev_padded(A2, tdt) if A2 is not None else None
+    W2t = torch.from_numpy(np.asarray(W2, np.float32)).to(tdt).to(dev) if W2 is not None else None
+    bt = torch.from_numpy(np.asarray(bias, np.float32)).to(dev) if bias is not None else None
+    b2t = torch.from_numpy(np.asarray(bias2, np.float32)).to(dev) if bias2 is not None else None
+    M = A.shape[0]
+    N = out_cols or W.shape[1]
+    out = dev_padded(np.zeros((M, N)), tdt, fill=3.0)
+    S.saga_apply_vertex(op, S.cmat(At), S.cmat(Wt), S.cmat(A2t), S.cmat(W2t),
+                        None if bt is None else bt.data_ptr(),
+                        None if b2t is None else b2t.data_ptr(), S.mat(out), S.stream_handle())
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("M,K,N", [(1000, 602, 128), (777, 128, 41), (2000, 128, 16),
+                                   (130, 16, 8), (513, 512, 80), (300, 256, 256),
+                                   (64, 64, 192), (5, 37, 3)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gemm_plain(M, K, N, dtype):
+    rng = np.random.default_rng(M + K + N)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((K, N)) / np.sqrt(K)).astype(np.float32)
+    if dtype == "bf16":
+        A, W = _bf16_round(A), _bf16_round(W)
+    bias = rng.standard_normal(N)
+    deg = rng.integers(0, 9, M)
+    print(f"gemm plain M={M} K={K} N={N} {dtype}", flush=True)
+    out = run_gemm(A, W, dtype, bias=bias, act="relu", deg=deg)
+    ref = O.dense(A, W, bias=bias, act="relu", row_scale=O.degree_scale(deg))
+    assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
+    out = run_gemm(A, W, dtype)
+    ref = O.dense(A, W)
+    assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
+
+
+def test_gemm_small_integers_exact():
+    rng = np.random.default_rng(1)
+    A = rng.integers(-8, 9, (333, 64)).astype(np.float32)
+    W = rng.integers(-8, 9, (64, 48)).astype(np.float32)
+    exact = A.astype(np.float64) @ W
+    out = run_gemm(A, W, "f32")
+    assert np.array_equal(to_np(out), exact)
+    # bf16 storage: products and sums are exact in the fp32 accumulator, the
+    # stored result is the round-to-nearest-even bf16 of the exact integer
+    out = run_gemm(A, W, "bf16")
+    assert np.array_equal(to_np(out), _bf16_round(exact))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gemm_concat(dtype):
+    rng = np.random.default_rng(2)
+    M, K1, K2, N = 700, 256, 200, 256
+    A = rng.standard_normal((M, K1)).astype(np.float32)
+    A2 = rng.standard_normal((M, K2)).astype(np.float32)
+    W = (rng.standard_normal((K1, N)) / 16).astype(np.float32)
+    W2 = (rng.standard_normal((K2, N)) / 16).astype(np.float32)
+    if dtype == "bf16":
+        A, A2, W, W2 = map(_bf16_round, (A, A2, W, W2))
+    b = rng.standard_normal(N)
+    out = run_gemm(A, W, dtype, bias=b, A2=A2, W2=W2, mode="concat")
+    ref = O.dense(np.concatenate([A, A2], 1), np.concatenate([W, W2], 0), bias=b)
+    assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
+
+
+@pytest.mark.parametrize("F", [16, 64])
+def test_gemm_gru(F):
+    rng = np.random.default_rng(F)
+    M = 1001
+    a = rng.standard_normal((M, F)).astype(np.float32)
+    h = rng.standard_normal((M, F)).astype(np.float32)
+    Wih = (rng.standard_normal((F, 3 * F)) / 8).astype(np.float32)
+    Whh = (rng.standard_normal((F, 3 * F)) / 8).astype(np.float32)
+    bih = rng.standard_normal(3 * F)
+    bhh = rng.standard_normal(3 * F)
+    out = run_gemm(a, Wih, "f32", bias=bih, A2=h, W2=Whh, bias2=bhh, mode="gru", out_cols=F)
+    ref = O.gru_cell(a, h, Wih, bih, Whh, bhh)
+    assert rel_err(to_np(out), ref) <= FP32_TOL
