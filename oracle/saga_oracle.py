@@ -368,15 +368,13 @@ def sage_pool_layer(row_ptr, col_idx, X, W_pool, b_pool, W, b, rows=None):
     return dense(cat, W, bias=b)
 
 
-def gated_gru_layer(row_ptr, col_idx, H, E_feat, W_e, b_e, W_ih, b_ih, W_hh,
-                    b_hh, rows=None):
-    """Gated edge MPNN with GRU ApplyVertex (the GGNN example of Fig. 2 and
-    Table I, GGNN row; reading R5).
+def gated_gather(row_ptr, col_idx, H, E_feat, W_e, b_e, rows=None):
+    """Scatter + ApplyEdge + Gather of the gated edge MPNN (the GGNN example
+    of Fig. 2 and Table I, GGNN row; reading R5).
 
     Scatter: edge (u -> v) carries [h_u | h_v | e_uv];
     ApplyEdge: g = sigmoid([h_u | h_v | e_uv] W_e + b_e), m = g * h_u;
-    Gather: a_v = sum of m over v's in-edges;
-    ApplyVertex: GRU(input a_v, hidden h_v), gates (r, z, n).
+    Gather: a_v = sum of m over v's in-edges (0 if none).
     E_feat row e belongs to CSR entry e.
     """
     rp = np.asarray(row_ptr, dtype=np.int64)
@@ -394,6 +392,15 @@ def gated_gru_layer(row_ptr, col_idx, H, E_feat, W_e, b_e, W_ih, b_ih, W_hh,
         cat = np.concatenate([hu, hv, _f64(E_feat[lo:hi])], axis=1)
         gate = sigmoid(cat @ _f64(W_e) + _f64(b_e)[None, :])
         A[i] = (gate * hu).sum(axis=0)
+    return A
+
+
+def gated_gru_layer(row_ptr, col_idx, H, E_feat, W_e, b_e, W_ih, b_ih, W_hh,
+                    b_hh, rows=None):
+    """Gated edge MPNN layer: gated_gather, then the GRU ApplyVertex with
+    input a_v and hidden state h_v (Fig. 2: GGNN's ApplyVertex is a GRU)."""
+    rows = _rows_arg(rows, len(row_ptr) - 1)
+    A = gated_gather(row_ptr, col_idx, H, E_feat, W_e, b_e, rows=rows)
     return gru_cell(A, _f64(H[rows]), W_ih, b_ih, W_hh, b_hh)
 
 
