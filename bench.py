@@ -246,6 +246,9 @@ def main():
     ap.add_argument("--scale", type=int, default=21)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before timing, run one device-to-device copy of this many MiB "
+                         "(a known-size kernel for calibrating memory counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -265,6 +268,14 @@ def main():
         Cfg.add_bf16_variant(g)
     log(f"inputs: V={g['num_vertices']} E={g['num_edges']} in {time.time() - t0:.1f}s")
 
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 18
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {args.calib_copy_mib} MiB")
+        del a, b
     results = {}
     for dt in dtypes:
         step = Step(g, dt, dev)

@@ -18,6 +18,8 @@
 //     output row; segments of split rows (d_in > seg_len) write float32
 //     partials, merged in segment order by k_combine (deterministic: no
 //     floating-point atomics anywhere).
+#include <cstdlib>
+
 #include "saga_device.h"
 #include "saga_internal.h"
 
@@ -47,118 +49,121 @@ __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int 
 
 // ------------------------------------------------------------------------
 // COPY / SRC_NORM messages with SUM, MEAN or MAX
+//
+// Feature slicing: the row's 16-byte vectors are split into `nslices`
+// slices of LPR vectors; workgroup i works on block i / nslices, slice
+// i % nslices.  Workgroups are dispatched round-robin over the 8 XCDs, so
+// with nslices dividing 8 every XCD touches one slice only and its L2 keeps
+// nslices times more (hot) source rows than if it cached whole rows.  With
+// 128-byte slices each cached line is one row's slice.
+// Neighbour indices are read CPL per lane (LPR*CPL edges per batch) with
+// non-temporal loads (they are streamed once) and broadcast by cross-lane
+// permute; U source-row loads are kept in flight per lane.
 // ------------------------------------------------------------------------
-template <typename T, int LPR, int VPL, int U, bool MAXRED>
-__global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a) {
+template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, bool SRCNORM>
+__global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int nslices, int slice0) {
   constexpr int EPV = Vec16<T>::N;
   constexpr int NG = kThreads / LPR;
   const int32_t* __restrict__ counts = a.counts;
   if (counts[kErrFlags]) return;
   const int nb = counts[kNumBlocks];
+  const int b = blockIdx.x / nslices;
+  const int slice = slice0 + (blockIdx.x - b * nslices);
+  if (b >= nb) return;
   const int s_split = counts[kSSplit];
   const int gl = threadIdx.x % LPR;
   const int grp = threadIdx.x / LPR;
   const int gbase = (threadIdx.x & 63) - gl;
   const int nv = (int)((a.feat * (int64_t)sizeof(T) + 15) / 16);
-  const bool srcnorm = a.msg == SAGA_MSG_SRC_NORM;
-  const T* __restrict__ src = static_cast<const T*>(a.src);
+  const int v0 = slice * LPR * VPL;
+  // this lane's 16-byte vectors of every source row
+  const uint4* __restrict__ src = reinterpret_cast<const uint4*>(static_cast<const T*>(a.src));
+  const int64_t ld16 = a.ld_src * (int64_t)sizeof(T) / 16;
   const int32_t* __restrict__ col = a.col_idx;
   const float init = MAXRED ? -INFINITY : 0.0f;
 
-  for (int b = blockIdx.x; b < nb; b += gridDim.x) {
-    const int s0 = a.block_ptr[b], s1 = a.block_ptr[b + 1];
-    for (int s = s0 + grp; s < s1; s += NG) {
-      const int row = a.seg_row[s];
-      const int beg = a.seg_beg[s], end = a.seg_end[s];
-      float acc[VPL][EPV];
+  const int s0 = a.block_ptr[b], s1 = a.block_ptr[b + 1];
+  for (int s = s0 + grp; s < s1; s += NG) {
+    const int row = a.seg_row[s];
+    const int beg = a.seg_beg[s], end = a.seg_end[s];
+    float acc[VPL][EPV];
 #pragma unroll
-      for (int q = 0; q < VPL; ++q)
+    for (int q = 0; q < VPL; ++q)
 #pragma unroll
-        for (int i = 0; i < EPV; ++i) acc[q][i] = init;
+      for (int i = 0; i < EPV; ++i) acc[q][i] = init;
 
-      for (int e = beg; e < end; e += LPR) {
-        const int my = e + gl;
-        const int c = my < end ? col[my] : 0;
-        float w = 1.0f;
-        if (srcnorm) w = my < end ? rsqrt_deg(a.d_out[c]) : 0.0f;
-        const int n = (end - e) < LPR ? (end - e) : LPR;
-        int t = 0;
-        for (; t + U <= n; t += U) {
-          int u[U];
+    for (int e = beg; e < end; e += LPR * CPL) {
+      int c[CPL];
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) {
+        const int idx = e + j * LPR + gl;
+        c[j] = idx < end ? __builtin_nontemporal_load(col + idx) : 0;
+      }
+      const int n = (end - e) < LPR * CPL ? (end - e) : LPR * CPL;
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) {
+        const int nq = n - j * LPR < LPR ? n - j * LPR : LPR;
+        if (nq <= 0) break;
+        // U row loads in flight per lane; a short last batch is predicated
+        for (int t = 0; t < nq; t += U) {
+          uint4 raw[U][VPL];
           float wu[U];
 #pragma unroll
           for (int k = 0; k < U; ++k) {
-            u[k] = __shfl(c, gbase + t + k, 64);
-            wu[k] = srcnorm ? __shfl(w, gbase + t + k, 64) : 1.0f;
-          }
-          float x[U][VPL][EPV];
-#pragma unroll
-          for (int k = 0; k < U; ++k)
+            const int tk = t + k < nq ? t + k : t;
+            const int u = __shfl(c[j], gbase + tk, 64);
+            if (SRCNORM) wu[k] = rsqrt_deg(a.d_out[u]);
 #pragma unroll
             for (int q = 0; q < VPL; ++q) {
-              const int vi = gl + q * LPR;
-              if (vi < nv) Vec16<T>::load(src + (int64_t)u[k] * a.ld_src + vi * EPV, x[k][q]);
+              const int vi = v0 + gl + q * LPR;
+              if (vi < nv && t + k < nq) raw[k][q] = src[(int64_t)u * ld16 + vi];
             }
+          }
 #pragma unroll
-          for (int k = 0; k < U; ++k)
+          for (int k = 0; k < U; ++k) {
+            if (t + k < nq) {
 #pragma unroll
-            for (int q = 0; q < VPL; ++q)
+              for (int q = 0; q < VPL; ++q) {
+                float x[EPV];
+                Vec16<T>::widen(raw[k][q], x);
 #pragma unroll
-              for (int i = 0; i < EPV; ++i) {
-                if (MAXRED)
-                  acc[q][i] = fmaxf(acc[q][i], x[k][q][i] * wu[k]);
-                else
-                  acc[q][i] += x[k][q][i] * wu[k];
-              }
-        }
-        for (; t < n; ++t) {
-          const int uu = __shfl(c, gbase + t, 64);
-          const float ww = srcnorm ? __shfl(w, gbase + t, 64) : 1.0f;
-#pragma unroll
-          for (int q = 0; q < VPL; ++q) {
-            const int vi = gl + q * LPR;
-            float x[EPV];
-            if (vi < nv) {
-              Vec16<T>::load(src + (int64_t)uu * a.ld_src + vi * EPV, x);
-#pragma unroll
-              for (int i = 0; i < EPV; ++i) {
-                if (MAXRED)
-                  acc[q][i] = fmaxf(acc[q][i], x[i] * ww);
-                else
-                  acc[q][i] += x[i] * ww;
+                for (int i = 0; i < EPV; ++i) {
+                  const float v = SRCNORM ? x[i] * wu[k] : x[i];
+                  acc[q][i] = MAXRED ? fmaxf(acc[q][i], v) : acc[q][i] + v;
+                }
               }
             }
           }
         }
       }
+    }
 
-      if (s < s_split) {
-        float* p = a.partial + (int64_t)s * a.pstride;
+    if (s < s_split) {
+      float* p = a.partial + (int64_t)s * a.pstride;
 #pragma unroll
-        for (int q = 0; q < VPL; ++q) {
-          const int vi = gl + q * LPR;
-          if (vi < nv)
+      for (int q = 0; q < VPL; ++q) {
+        const int vi = v0 + gl + q * LPR;
+        if (vi < nv)
 #pragma unroll
-            for (int i = 0; i < EPV; ++i) p[vi * EPV + i] = acc[q][i];
-        }
-      } else {
-        const int d = end - beg;  // a whole row
-        float scale = 1.0f;
-        if (a.reduce == kMean) scale = d > 0 ? 1.0f / (float)d : 0.0f;
-        if (a.dst_norm) scale *= rsqrt_deg(d);
+          for (int i = 0; i < EPV; ++i) p[vi * EPV + i] = acc[q][i];
+      }
+    } else {
+      const int d = end - beg;  // a whole row
+      float scale = 1.0f;
+      if (a.reduce == kMean) scale = d > 0 ? 1.0f / (float)d : 0.0f;
+      if (a.dst_norm) scale *= rsqrt_deg(d);
 #pragma unroll
-        for (int q = 0; q < VPL; ++q) {
-          const int vi = gl + q * LPR;
-          if (vi < nv) {
-            float x[EPV];
+      for (int q = 0; q < VPL; ++q) {
+        const int vi = v0 + gl + q * LPR;
+        if (vi < nv) {
+          float x[EPV];
 #pragma unroll
-            for (int i = 0; i < EPV; ++i) {
-              float v = acc[q][i];
-              if (MAXRED && d == 0) v = 0.0f;
-              x[i] = v * scale;
-            }
-            store_out<T>(a, row, vi * EPV, x);
+          for (int i = 0; i < EPV; ++i) {
+            float v = acc[q][i];
+            if (MAXRED && d == 0) v = 0.0f;
+            x[i] = v * scale;
           }
+          store_out<T>(a, row, vi * EPV, x);
         }
       }
     }
@@ -483,27 +488,82 @@ inline int next_pow2(int x) {
   return p;
 }
 
+// slices processed concurrently by one launch (the rest run as further
+// launches); SAGA_GATHER_CONCURRENT_SLICES overrides it for tuning
+int concurrent_slices() {
+  static int v = [] {
+    const char* e = getenv("SAGA_GATHER_CONCURRENT_SLICES");
+    int x = e ? atoi(e) : 0;
+    return x > 0 ? x : 0;  // 0: all slices in one launch
+  }();
+  return v;
+}
+
 template <typename T, int LPR, int VPL>
-hipError_t launch_simple_lpr(const GatherArgs& a, unsigned grid, hipStream_t st) {
-  constexpr int U = LPR >= 8 ? (VPL == 1 ? 8 : 4) : 4;
-  if (a.reduce == kMax)
-    hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, true>), dim3(grid), dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, false>), dim3(grid), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, hipStream_t st) {
+  constexpr int U = LPR >= 8 ? (VPL == 1 ? 8 : 4) : LPR;
+  constexpr int CPL = LPR >= 32 ? 1 : (LPR >= 8 ? 4 : 8);
+  int conc = concurrent_slices();
+  if (conc <= 0 || conc > nslices || nslices % conc != 0) conc = nslices;
+  const dim3 grid(blocks * conc);
+  const bool srcnorm = a.msg == SAGA_MSG_SRC_NORM;
+  for (int s0 = 0; s0 < nslices; s0 += conc) {
+    if (a.reduce == kMax) {
+      if (srcnorm)
+        hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, true, true>), grid, dim3(kThreads),
+                           0, st, a, conc, s0);
+      else
+        hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, true, false>), grid, dim3(kThreads),
+                           0, st, a, conc, s0);
+    } else {
+      if (srcnorm)
+        hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, false, true>), grid, dim3(kThreads),
+                           0, st, a, conc, s0);
+      else
+        hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, false, false>), grid,
+                           dim3(kThreads), 0, st, a, conc, s0);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// bytes of each source row one slice covers (128 = one cache line); the
+// SAGA_GATHER_SLICE_BYTES environment variable overrides it for tuning
+int slice_bytes() {
+  static int v = [] {
+    const char* e = getenv("SAGA_GATHER_SLICE_BYTES");
+    int x = e ? atoi(e) : 128;
+    return x >= 16 ? x : 128;
+  }();
+  return v;
 }
 
 template <typename T>
-hipError_t launch_simple(const GatherArgs& a, int nv, unsigned grid, hipStream_t st) {
-  if (nv > 64) return launch_simple_lpr<T, 64, 2>(a, grid, st);
+hipError_t launch_simple(const GatherArgs& a, int nv, unsigned blocks, hipStream_t st) {
+  const int sv = slice_bytes() / 16;
+  if (sv >= 1 && nv > sv && nv % sv == 0 && (sv & (sv - 1)) == 0 && sv <= 64) {
+    const int ns = nv / sv;
+    switch (sv) {
+      case 1: return launch_simple_lpr<T, 1, 1>(a, blocks, ns, st);
+      case 2: return launch_simple_lpr<T, 2, 1>(a, blocks, ns, st);
+      case 4: return launch_simple_lpr<T, 4, 1>(a, blocks, ns, st);
+      case 8: return launch_simple_lpr<T, 8, 1>(a, blocks, ns, st);
+      case 16: return launch_simple_lpr<T, 16, 1>(a, blocks, ns, st);
+      case 32: return launch_simple_lpr<T, 32, 1>(a, blocks, ns, st);
+      default: return launch_simple_lpr<T, 64, 1>(a, blocks, ns, st);
+    }
+  }
+  if (nv > 64) return launch_simple_lpr<T, 64, 2>(a, blocks, 1, st);
   switch (next_pow2(nv)) {
-    case 1: return launch_simple_lpr<T, 1, 1>(a, grid, st);
-    case 2: return launch_simple_lpr<T, 2, 1>(a, grid, st);
-    case 4: return launch_simple_lpr<T, 4, 1>(a, grid, st);
-    case 8: return launch_simple_lpr<T, 8, 1>(a, grid, st);
-    case 16: return launch_simple_lpr<T, 16, 1>(a, grid, st);
-    case 32: return launch_simple_lpr<T, 32, 1>(a, grid, st);
-    default: return launch_simple_lpr<T, 64, 1>(a, grid, st);
+    case 1: return launch_simple_lpr<T, 1, 1>(a, blocks, 1, st);
+    case 2: return launch_simple_lpr<T, 2, 1>(a, blocks, 1, st);
+    case 4: return launch_simple_lpr<T, 4, 1>(a, blocks, 1, st);
+    case 8: return launch_simple_lpr<T, 8, 1>(a, blocks, 1, st);
+    case 16: return launch_simple_lpr<T, 16, 1>(a, blocks, 1, st);
+    case 32: return launch_simple_lpr<T, 32, 1>(a, blocks, 1, st);
+    default: return launch_simple_lpr<T, 64, 1>(a, blocks, 1, st);
   }
 }
 

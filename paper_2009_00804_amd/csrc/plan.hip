@@ -88,13 +88,16 @@ __global__ void k_zero(int32_t* p, int64_t n) {
 }
 
 // d_in, d_out and CSR validation; error bits go to counts[kErrFlags]
+// (edges_too: also count d_out with global atomics -- only used when the
+// source range is too large for the bucketed count below)
 __global__ __launch_bounds__(kThreads) void k_degrees(const int32_t* __restrict__ rp,
                                                       const int32_t* __restrict__ col, int32_t V,
-                                                      int32_t Vs, int64_t E, int32_t* d_in,
-                                                      int32_t* d_out, int32_t* counts) {
+                                                      int32_t Vs, int64_t E, int edges_too,
+                                                      int32_t* d_in, int32_t* d_out,
+                                                      int32_t* counts) {
   int err = 0;
   int maxd = 0;
-  const int64_t n = V > E ? (int64_t)V : E;
+  const int64_t n = (V > E || !edges_too) ? (int64_t)V : E;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
     if (i < V) {
@@ -109,7 +112,7 @@ __global__ __launch_bounds__(kThreads) void k_degrees(const int32_t* __restrict_
         if ((int64_t)rp[V] != E) err |= 4;
       }
     }
-    if (i < E) {
+    if (edges_too && i < E) {
       int32_t c = col[i];
       if (c < 0 || c >= Vs)
         err |= 8;
@@ -123,9 +126,139 @@ __global__ __launch_bounds__(kThreads) void k_degrees(const int32_t* __restrict_
     int m = __shfl_xor(maxd, off, 64);
     maxd = m > maxd ? m : maxd;
   }
+  // one atomic per workgroup (same-address atomics serialize)
+  __shared__ int s_err[kThreads / 64], s_max[kThreads / 64];
   if ((threadIdx.x & 63) == 0) {
+    s_err[threadIdx.x >> 6] = err;
+    s_max[threadIdx.x >> 6] = maxd;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < kThreads / 64; ++k) {
+      err |= s_err[k];
+      maxd = s_max[k] > maxd ? s_max[k] : maxd;
+    }
     if (err) atomicOr(&counts[kErrFlags], err);
-    atomicMax(&counts[kMaxDegree], maxd);
+    if (maxd) atomicMax(&counts[kMaxDegree], maxd);
+  }
+}
+
+// ------------------------------------------------------------------------
+// Out-degrees without global atomics.  A power-law graph sends a large share
+// of all edges to a few hub sources, and same-address atomics serialize, so
+// instead: (1) histogram the CSR source ids by bucket (32768 ids per bucket)
+// per tile, (2) scan, (3) scatter the ids into bucket order, (4) count each
+// bucket in a 128 KB LDS histogram and store the counts.
+// ------------------------------------------------------------------------
+constexpr int kBucketBits = 15;
+constexpr int kBucketSize = 1 << kBucketBits;
+constexpr int kMaxBuckets = 4096;
+constexpr int kEdgeItems = 32;
+constexpr int kEdgeTile = kThreads * kEdgeItems;  // 8192 edges per tile
+
+__global__ __launch_bounds__(kThreads) void k_outdeg_hist(const int32_t* __restrict__ col,
+                                                          int64_t E, int32_t Vs, int nb,
+                                                          int32_t* __restrict__ hist,
+                                                          int64_t ntiles, int32_t* counts) {
+  __shared__ int32_t h[kMaxBuckets];
+  for (int b = threadIdx.x; b < nb; b += kThreads) h[b] = 0;
+  __syncthreads();
+  int err = 0;
+  const int64_t base = blockIdx.x * (int64_t)kEdgeTile;
+  int32_t c[kEdgeItems];
+#pragma unroll
+  for (int j = 0; j < kEdgeItems; ++j) {
+    const int64_t i = base + j * kThreads + threadIdx.x;
+    c[j] = i < E ? __builtin_nontemporal_load(col + i) : -1;
+  }
+#pragma unroll
+  for (int j = 0; j < kEdgeItems; ++j) {
+    const int64_t i = base + j * kThreads + threadIdx.x;
+    if (i < E) {
+      if (c[j] < 0 || c[j] >= Vs)
+        err |= 8;
+      else
+        atomicAdd(&h[c[j] >> kBucketBits], 1);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) err |= __shfl_xor(err, off, 64);
+  if ((threadIdx.x & 63) == 0 && err) atomicOr(&counts[kErrFlags], err);
+  __syncthreads();
+  for (int b = threadIdx.x; b < nb; b += kThreads) hist[(int64_t)b * ntiles + blockIdx.x] = h[b];
+}
+
+__global__ __launch_bounds__(kThreads) void k_outdeg_scatter(const int32_t* __restrict__ col,
+                                                             int64_t E, int nb,
+                                                             const int32_t* __restrict__ offs,
+                                                             int64_t ntiles,
+                                                             int32_t* __restrict__ out,
+                                                             int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  __shared__ int32_t cur[kMaxBuckets];
+  for (int b = threadIdx.x; b < nb; b += kThreads) cur[b] = offs[(int64_t)b * ntiles + blockIdx.x];
+  __syncthreads();
+  const int64_t base = blockIdx.x * (int64_t)kEdgeTile;
+  int32_t c[kEdgeItems];
+#pragma unroll
+  for (int j = 0; j < kEdgeItems; ++j) {
+    const int64_t i = base + j * kThreads + threadIdx.x;
+    c[j] = i < E ? __builtin_nontemporal_load(col + i) : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < kEdgeItems; ++j) {
+    const int64_t i = base + j * kThreads + threadIdx.x;
+    if (i < E) {
+      const int32_t p = atomicAdd(&cur[c[j] >> kBucketBits], 1);
+      if (p >= 0 && p < E)
+        out[p] = c[j];
+      else
+        atomicOr(&counts[kErrFlags], kErrInternal);
+    }
+  }
+}
+
+// kOutdegSplit workgroups per bucket, each counting one slice of the
+// bucket into LDS and storing its partial histogram (a hub's occurrences are
+// split over the workgroups, so same-address LDS atomics stay few per CU)
+constexpr int kOutdegSplit = 16;
+
+__global__ __launch_bounds__(1024) void k_outdeg_count(const int32_t* __restrict__ bucketed,
+                                                       const int32_t* __restrict__ offs,
+                                                       int64_t ntiles, int nb, int64_t E,
+                                                       int32_t Vs, int32_t* __restrict__ part,
+                                                       const int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  __shared__ int32_t h[kBucketSize];
+  const int b = blockIdx.y, w = blockIdx.x;
+  for (int i = threadIdx.x; i < kBucketSize; i += 1024) h[i] = 0;
+  __syncthreads();
+  int64_t lo = offs[(int64_t)b * ntiles];
+  int64_t hi = b + 1 < nb ? (int64_t)offs[(int64_t)(b + 1) * ntiles] : E;
+  lo = lo < 0 ? 0 : (lo > E ? E : lo);
+  hi = hi < lo ? lo : (hi > E ? E : hi);
+  const int64_t n = hi - lo;
+  const int64_t s0 = lo + n * w / kOutdegSplit, s1 = lo + n * (w + 1) / kOutdegSplit;
+  for (int64_t i = s0 + threadIdx.x; i < s1; i += 1024)
+    atomicAdd(&h[__builtin_nontemporal_load(bucketed + i) & (kBucketSize - 1)], 1);
+  __syncthreads();
+  const int64_t v0 = (int64_t)b << kBucketBits;
+  int32_t* pw = part + (int64_t)w * nb * kBucketSize + v0;
+  for (int i = threadIdx.x; i < kBucketSize; i += 1024) pw[i] = h[i];
+}
+
+__global__ __launch_bounds__(kThreads) void k_outdeg_reduce(const int32_t* __restrict__ part,
+                                                            int nb, int32_t Vs,
+                                                            int32_t* __restrict__ d_out,
+                                                            const int32_t* counts) {
+  if (counts[kErrFlags]) return;
+  const int64_t stride = (int64_t)nb * kBucketSize;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < Vs;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    int32_t s = 0;
+#pragma unroll
+    for (int w = 0; w < kOutdegSplit; ++w) s += part[w * stride + v];
+    d_out[v] = s;
   }
 }
 
@@ -378,7 +511,12 @@ bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t
   L->scan_tiles_rows = cdiv(V, kTile);
   L->scan_tiles_segs = cdiv(L->max_segments, kTile);
   const int64_t hist_n = (int64_t)kBins * L->radix_tiles;
+  L->outdeg_nb = cdiv(Vs, kBucketSize);
+  L->edge_tiles = cdiv(E, kEdgeTile);
+  L->outdeg_bucketed = L->outdeg_nb <= kMaxBuckets && E > 0;
   int64_t scan_tiles = cdiv(hist_n, kTile);
+  if (L->outdeg_bucketed && cdiv(L->outdeg_nb * L->edge_tiles, kTile) > scan_tiles)
+    scan_tiles = cdiv(L->outdeg_nb * L->edge_tiles, kTile);
   if (L->scan_tiles_rows > scan_tiles) scan_tiles = L->scan_tiles_rows;
   if (L->scan_tiles_segs > scan_tiles) scan_tiles = L->scan_tiles_segs;
 
@@ -398,11 +536,15 @@ bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t
   L->off_block_ptr = take(L->max_blocks + 1);
   L->off_counts = take(kCountSlots);
   L->off_scratch = o;
-  // scratch: keysA, valsA, keysB, valsB, hist, tile sums, cost prefix
+  // scratch: keysA, valsA, keysB, valsB, hist, tile sums, cost prefix,
+  // bucketed source ids, bucket histogram
   take(V); take(V); take(V); take(V);
   take(hist_n);
   take(scan_tiles + 1);
   take(L->max_segments);
+  take(L->outdeg_bucketed ? E : 0);
+  take(L->outdeg_bucketed ? L->outdeg_nb * L->edge_tiles : 0);
+  take(L->outdeg_bucketed ? (int64_t)kOutdegSplit * L->outdeg_nb * kBucketSize : 0);
   L->scratch_bytes = o - L->off_scratch;
   L->total = o;
   return true;
@@ -427,14 +569,35 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   int64_t scan_tiles = cdiv((int64_t)kBins * ntiles, kTile);
   if (L.scan_tiles_rows > scan_tiles) scan_tiles = L.scan_tiles_rows;
   if (L.scan_tiles_segs > scan_tiles) scan_tiles = L.scan_tiles_segs;
+  if (L.outdeg_bucketed && cdiv(L.outdeg_nb * L.edge_tiles, kTile) > scan_tiles)
+    scan_tiles = cdiv(L.outdeg_nb * L.edge_tiles, kTile);
   int32_t* tile_sums = reinterpret_cast<int32_t*>(take(scan_tiles + 1));
   int32_t* P = reinterpret_cast<int32_t*>(take(L.max_segments));
+  int32_t* bucketed = reinterpret_cast<int32_t*>(take(L.outdeg_bucketed ? E : 0));
+  int32_t* ohist = reinterpret_cast<int32_t*>(take(L.outdeg_bucketed ? L.outdeg_nb * L.edge_tiles : 0));
+  int32_t* opart = reinterpret_cast<int32_t*>(
+      take(L.outdeg_bucketed ? (int64_t)kOutdegSplit * L.outdeg_nb * kBucketSize : 0));
 
   hipLaunchKernelGGL(k_zero, dim3(1), dim3(64), 0, st, p.counts, (int64_t)kCountSlots);
-  if (Vs > 0) hipLaunchKernelGGL(k_zero, dim3(grid_for(Vs)), dim3(kThreads), 0, st, p.d_out, (int64_t)Vs);
+  if (Vs > 0 && !L.outdeg_bucketed)
+    hipLaunchKernelGGL(k_zero, dim3(grid_for(Vs)), dim3(kThreads), 0, st, p.d_out, (int64_t)Vs);
   if (V == 0) return hipGetLastError();
-  hipLaunchKernelGGL(k_degrees, dim3(grid_for(V > E ? V : E)), dim3(kThreads), 0, st, p.row_ptr,
-                     p.col_idx, V, Vs, E, p.d_in, p.d_out, p.counts);
+  const int edges_too = L.outdeg_bucketed ? 0 : 1;
+  hipLaunchKernelGGL(k_degrees, dim3(grid_for(edges_too && E > V ? E : V)), dim3(kThreads), 0, st,
+                     p.row_ptr, p.col_idx, V, Vs, E, edges_too, p.d_in, p.d_out, p.counts);
+  if (L.outdeg_bucketed) {
+    const int nb = (int)L.outdeg_nb;
+    const int64_t et = L.edge_tiles;
+    hipLaunchKernelGGL(k_outdeg_hist, dim3(et), dim3(kThreads), 0, st, p.col_idx, E, Vs, nb,
+                       ohist, et, p.counts);
+    scan(ArrF{ohist}, (int64_t)nb * et, nullptr, ohist, nullptr, tile_sums, p.counts, st);
+    hipLaunchKernelGGL(k_outdeg_scatter, dim3(et), dim3(kThreads), 0, st, p.col_idx, E, nb, ohist,
+                       et, bucketed, p.counts);
+    hipLaunchKernelGGL(k_outdeg_count, dim3(kOutdegSplit, nb), dim3(1024), 0, st, bucketed, ohist,
+                       et, nb, E, Vs, opart, p.counts);
+    hipLaunchKernelGGL(k_outdeg_reduce, dim3(grid_for(Vs)), dim3(kThreads), 0, st, opart, nb, Vs,
+                       p.d_out, p.counts);
+  }
 
   // degree order: 4 stable passes of 8 bits over key = 0x7fffffff - d_in
   const uint32_t* kin[4] = {nullptr, keysA, keysB, keysA};

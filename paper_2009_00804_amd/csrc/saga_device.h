@@ -9,6 +9,7 @@ namespace saga {
 constexpr int kWave = 64;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 // --------------------------------------------------------------------------
@@ -31,12 +32,17 @@ template <typename T> struct Vec16;
 
 template <> struct Vec16<float> {
   static constexpr int N = 4;
+  __device__ __forceinline__ static void widen(const uint4& v, float (&x)[4]) {
+    x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y);
+    x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
+  }
   __device__ __forceinline__ static void load(const float* p, float (&x)[4]) {
     float4 v = *reinterpret_cast<const float4*>(p);
     x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
   }
   __device__ __forceinline__ static void store(float* p, const float (&x)[4]) {
-    *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+    // non-temporal: output rows are written once and not re-read here
+    __builtin_nontemporal_store(f32x4{x[0], x[1], x[2], x[3]}, reinterpret_cast<f32x4*>(p));
   }
   __device__ __forceinline__ static void store_n(float* p, const float (&x)[4], int n) {
     for (int i = 0; i < 4; ++i)
@@ -46,6 +52,14 @@ template <> struct Vec16<float> {
 
 template <> struct Vec16<uint16_t> {
   static constexpr int N = 8;
+  __device__ __forceinline__ static void widen(const uint4& v, float (&x)[8]) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
   __device__ __forceinline__ static void load(const uint16_t* p, float (&x)[8]) {
     uint4 v = *reinterpret_cast<const uint4*>(p);
     uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -61,7 +75,7 @@ template <> struct Vec16<uint16_t> {
     for (int i = 0; i < 4; ++i)
       w[i] = static_cast<uint32_t>(f32_to_bf16(x[2 * i])) |
              (static_cast<uint32_t>(f32_to_bf16(x[2 * i + 1])) << 16);
-    *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+    __builtin_nontemporal_store(u32x4{w[0], w[1], w[2], w[3]}, reinterpret_cast<u32x4*>(p));
   }
   __device__ __forceinline__ static void store_n(uint16_t* p, const float (&x)[8], int n) {
     for (int i = 0; i < 8; ++i)

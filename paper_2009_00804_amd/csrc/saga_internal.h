@@ -29,6 +29,8 @@ struct PlanLayout {
       off_block_ptr, off_counts, off_scratch, scratch_bytes, total;
   int64_t max_segments, max_blocks, max_split, max_split_segments;
   int64_t radix_tiles, scan_tiles_rows, scan_tiles_segs;
+  int64_t outdeg_nb, edge_tiles;
+  bool outdeg_bucketed;
 };
 
 bool plan_layout(int32_t num_dst, int32_t num_src, int64_t num_edges, int32_t seg_len,
