@@ -89,9 +89,9 @@ class Step:
         es = 4 if dtype == "f32" else 2
         al = 16 // es
         ld = lambda c: (c + al - 1) // al * al  # noqa: E731
-        self.Z1 = torch.empty((self.V, ld(hid)), dtype=tdt, device=dev)[:, :hid]
+        self.Z1 = torch.empty((self.V, S.gather_ld(hid, es)), dtype=tdt, device=dev)[:, :hid]
         self.H1 = torch.empty((self.V, ld(hid)), dtype=tdt, device=dev)[:, :hid]
-        self.Z2 = torch.empty((self.V, ld(f_out)), dtype=tdt, device=dev)[:, :f_out]
+        self.Z2 = torch.empty((self.V, S.gather_ld(f_out, es)), dtype=tdt, device=dev)[:, :f_out]
         self.Y = torch.empty((self.V, ld(f_out)), dtype=tdt, device=dev)[:, :f_out]
         self.graph = S.Graph(self.rp, self.col)     # allocates + builds + checks once
         self.plan_ws = self.graph.ws
@@ -312,8 +312,14 @@ def main():
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = load_traffic(f"{dom}", args.dtype)
     roof["kernel"] = f"{dom} ({kernel_name})"
+    roof["launch_ms"] = r["mean"][dom]
+    roof["algorithmic_bytes"] = byts
     roof["algorithmic"] = ("compulsory bytes: 4 B per CSR index + row_ptr + source matrix "
                            "and output once" if roof["bound"] == "hbm" else "2 M K N flops")
+    if roof["traffic"]:
+        # measured HBM traffic (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)
+        roof["counter_GBps"] = roof["traffic"] / dur / 1e9
+        roof["counter_frac_of_8TBps"] = roof["counter_GBps"] / (PEAK_HBM / 1e9)
     stage_ms = {n: round(r["mean"][n], 4) for n in step.names}
     out = {
         "metric": "GNN layer throughput: edges/s (GTEPS) + achieved HBM GB/s fraction, 1 MI355X",

@@ -315,7 +315,22 @@ struct LayerPlanWs {
   size_t bytes;
 };
 
-int64_t ld_for(int64_t cols, saga_dtype t) { return round_up(cols, t == SAGA_BF16 ? 8 : 4); }
+// Leading dimension of a layer intermediate that the gather reads by rows:
+// rows of up to 128 bytes are padded to a power of two (never straddling a
+// 128-byte L2 line), longer rows to a multiple of 64 bytes (each row then
+// touches a whole number of lines).
+int64_t ld_for(int64_t cols, saga_dtype t) {
+  const int64_t es = t == SAGA_BF16 ? 2 : 4;
+  int64_t bytes = cols * es;
+  if (bytes <= 128) {
+    int64_t p = 16;
+    while (p < bytes) p <<= 1;
+    bytes = p;
+  } else {
+    bytes = round_up(bytes, 64);
+  }
+  return bytes / es;
+}
 
 saga_status layer_check_desc(const saga_plan& p, const saga_layer_desc& d) {
   if (p.num_dst != p.num_src) return fail(SAGA_EINVAL, "layers need num_src == num_dst");

@@ -239,8 +239,18 @@ __global__ __launch_bounds__(1024) void k_outdeg_count(const int32_t* __restrict
   hi = hi < lo ? lo : (hi > E ? E : hi);
   const int64_t n = hi - lo;
   const int64_t s0 = lo + n * w / kOutdegSplit, s1 = lo + n * (w + 1) / kOutdegSplit;
-  for (int64_t i = s0 + threadIdx.x; i < s1; i += 1024)
-    atomicAdd(&h[__builtin_nontemporal_load(bucketed + i) & (kBucketSize - 1)], 1);
+  constexpr int kB = 8;  // loads in flight per thread before the LDS atomics
+  for (int64_t i0 = s0; i0 < s1; i0 += 1024 * kB) {
+    int32_t v[kB];
+#pragma unroll
+    for (int j = 0; j < kB; ++j) {
+      const int64_t i = i0 + j * 1024 + threadIdx.x;
+      v[j] = i < s1 ? __builtin_nontemporal_load(bucketed + i) : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < kB; ++j)
+      if (v[j] >= 0) atomicAdd(&h[v[j] & (kBucketSize - 1)], 1);
+  }
   __syncthreads();
   const int64_t v0 = (int64_t)b << kBucketBits;
   int32_t* pw = part + (int64_t)w * nb * kBucketSize + v0;

@@ -238,6 +238,22 @@ def mat(t, rows=None, cols=None):
                     cols if cols is not None else t.shape[1], t.stride(0))
 
 
+def gather_ld(cols, elem_size):
+    """Leading dimension (elements) for a matrix whose rows the gather
+    fetches: rows up to 128 bytes padded to a power of two, longer rows to a
+    multiple of 64 bytes, so a row never touches more 128-byte L2 lines than
+    it must (the rule saga_layer uses for its intermediates)."""
+    b = cols * elem_size
+    if b <= 128:
+        p = 16
+        while p < b:
+            p <<= 1
+        b = p
+    else:
+        b = (b + 63) // 64 * 64
+    return b // elem_size
+
+
 def padded_empty(rows, cols, dtype, device, align_elems=None):
     """rows x cols view of a buffer whose rows are padded to 16 bytes."""
     es = torch.tensor([], dtype=dtype).element_size()
