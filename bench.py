@@ -106,6 +106,9 @@ class Step:
         n2 = S.saga_gather_workspace_size(p, self.op2, f_out)
         self.gws = S.workspace(max(n1, n2), dev)
         self.gop = S.saga_gemm_op(S.dtype_code(tdt), S.SAGA_GEMM_PLAIN, S.SAGA_ACT_NONE, p.d_out)
+        m1 = S.saga_apply_vertex_workspace_size(self.gop, self.W1.shape[0], 0, self.W1.shape[1])
+        m2 = S.saga_apply_vertex_workspace_size(self.gop, self.W2.shape[0], 0, self.W2.shape[1])
+        self.mws = S.workspace(max(m1, m2), dev)
         self.none = S.saga_cmat(None, 0, 0, 0)
         self.in1 = S.saga_edge_inputs()
         self.in1.src = S.cmat(self.Z1)
@@ -131,7 +134,8 @@ class Step:
             ev[1].record(self.stream)
         p = g.plan
         S.saga_apply_vertex(self.gop, S.cmat(self.X), S.cmat(self.W1), self.none, self.none, None,
-                            None, S.mat(self.Z1), self.sh)
+                            None, S.mat(self.Z1), C.c_void_p(self.mws.data_ptr()), self.mws.numel(),
+                            self.sh)
         if ev:
             ev[2].record(self.stream)
         S.saga_scatter_apply_edge_gather(p, self.op1, self.in1, S.mat(self.H1),
@@ -139,7 +143,8 @@ class Step:
         if ev:
             ev[3].record(self.stream)
         S.saga_apply_vertex(self.gop, S.cmat(self.H1), S.cmat(self.W2), self.none, self.none, None,
-                            None, S.mat(self.Z2), self.sh)
+                            None, S.mat(self.Z2), C.c_void_p(self.mws.data_ptr()), self.mws.numel(),
+                            self.sh)
         if ev:
             ev[4].record(self.stream)
         S.saga_scatter_apply_edge_gather(p, self.op2, self.in2, S.mat(self.Y),

@@ -261,7 +261,14 @@ saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edg
  *              n = tanh(gi_n + r * gh_n), out = (1 - z) n + z a2.
  * rs = row_scale_deg ? (deg[i] > 0 ? deg[i]^-1/2 : 0) : 1  (row i).
  * a: M x K, w: K x N (dense weights, ld may exceed N), out: M x N; bf16 or
- * f32 storage per op->dtype, float32 accumulation; N <= 256 per call.
+ * f32 storage per op->dtype, float32 accumulation; N <= 4096 per call.
+ *
+ * Workspace: device memory of at least saga_apply_vertex_workspace_size()
+ * bytes, 256-byte aligned, owned by the caller and not overlapping any
+ * argument.  Each call first writes w (and w2) into it transposed and
+ * zero-padded to whole tiles, the layout the matrix-core kernel streams;
+ * its contents are scratch afterwards.  Calls that share one workspace
+ * must be ordered (same stream).  Missing or too small: SAGA_EWORKSPACE.
  */
 typedef enum saga_gemm_mode { SAGA_GEMM_PLAIN = 0, SAGA_GEMM_CONCAT = 1, SAGA_GEMM_GRU = 2 } saga_gemm_mode;
 
@@ -272,9 +279,15 @@ typedef struct saga_gemm_op {
   const int32_t* row_scale_deg;   /* nullable, int32[M] */
 } saga_gemm_op;
 
+/* Workspace bytes for saga_apply_vertex with op's dtype and mode, k =
+ * a.cols, k2 = a2.cols (CONCAT and GRU; ignored for PLAIN), n = w.cols. */
+saga_status saga_apply_vertex_workspace_size(const saga_gemm_op* op, int64_t k, int64_t k2,
+                                             int64_t n, size_t* bytes);
+
 saga_status saga_apply_vertex(const saga_gemm_op* op, saga_cmat a, saga_cmat w,
                               saga_cmat a2, saga_cmat w2, const float* bias,
-                              const float* bias2, saga_mat out, void* stream);
+                              const float* bias2, saga_mat out, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* ======================================================================
  * One whole layer (Table I models)

@@ -2,6 +2,7 @@
 // to the kernel launchers; whole-layer composition of the Table I models.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -276,11 +277,29 @@ saga_status validate_gemm(const saga_gemm_op& op, const saga_cmat& a, const saga
   return SAGA_OK;
 }
 
+size_t gemm_ws_bytes(const saga_gemm_op& op, int64_t k, int64_t k2, int64_t n) {
+  return saga::gemm_workspace_bytes(op.dtype, op.mode, n, k, op.mode == SAGA_GEMM_PLAIN ? 0 : k2);
+}
+
 saga_status run_gemm(const saga_gemm_op& op, const saga_cmat& a, const saga_cmat& w,
                      const saga_cmat& a2, const saga_cmat& w2, const float* bias,
-                     const float* bias2, const saga_mat& out, hipStream_t st) {
+                     const float* bias2, const saga_mat& out, void* ws, size_t ws_bytes,
+                     hipStream_t st) {
   saga_status s = validate_gemm(op, a, w, a2, w2, out);
   if (s) return s;
+  const size_t need = gemm_ws_bytes(op, a.cols, a2.cols, w.cols);
+  if (!ws || ws_bytes < need)
+    return fail(SAGA_EWORKSPACE, "apply_vertex workspace: need %zu bytes, got %zu", need, ws_bytes);
+  if ((uintptr_t)ws % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
+  {
+    const size_t es = esize(op.dtype);
+    if (range_overlap(ws, need, out.ptr, mat_bytes(out.rows, out.cols, out.ld, es)) ||
+        range_overlap(ws, need, a.ptr, mat_bytes(a.rows, a.cols, a.ld, es)) ||
+        range_overlap(ws, need, w.ptr, mat_bytes(w.rows, w.cols, w.ld, es)) ||
+        range_overlap(ws, need, a2.ptr, mat_bytes(a2.rows, a2.cols, a2.ld, es)) ||
+        range_overlap(ws, need, w2.ptr, mat_bytes(w2.rows, w2.cols, w2.ld, es)))
+      return fail(SAGA_EINVAL, "workspace overlaps an argument");
+  }
   saga::GemmArgs g;
   memset(&g, 0, sizeof(g));
   g.dtype = op.dtype;
@@ -303,6 +322,8 @@ saga_status run_gemm(const saga_gemm_op& op, const saga_cmat& a, const saga_cmat
   g.row_scale_deg = op.row_scale_deg;
   g.out = out.ptr;
   g.ldo = out.ld;
+  g.ws = ws;
+  g.ws_bytes = ws_bytes;
   hipError_t e = saga::launch_gemm(g, st);
   if (e != hipSuccess) return dev_fail(e, "gemm launch");
   return ok();
@@ -368,6 +389,8 @@ struct LayerBufs {
   float* wext = nullptr; int64_t ldw = 0;  // GAT folded weights
   void* part = nullptr;
   size_t part_bytes = 0;
+  void* gws = nullptr;                     // packed weights of the layer's GEMMs
+  size_t gws_bytes = 0;
 };
 
 bool gcn_transform_first(const saga_layer_desc& d) { return d.out_feat <= d.in_feat; }
@@ -428,6 +451,37 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
   gather_ws_bytes(p, op, gfeat, &pb);
   b->part_bytes = pb;
   b->part = c.take(pb);
+  // one region for the packed weights, sized for the largest GEMM of the layer
+  saga_gemm_op g;
+  memset(&g, 0, sizeof(g));
+  g.dtype = t;
+  g.mode = SAGA_GEMM_PLAIN;
+  const int64_t Fi = d.in_feat, Fo = d.out_feat;
+  size_t gb = 0;
+  switch (d.kind) {
+    case SAGA_LAYER_GCN:
+      gb = gemm_ws_bytes(g, Fi, 0, Fo);
+      break;
+    case SAGA_LAYER_GAT: {
+      const int64_t F = d.head_mean ? Fo * d.heads : Fo;
+      gb = gemm_ws_bytes(g, Fi, 0, F + 2 * d.heads);
+      break;
+    }
+    case SAGA_LAYER_SAGE_POOL: {
+      gb = gemm_ws_bytes(g, Fi, 0, Fi);
+      g.mode = SAGA_GEMM_CONCAT;
+      gb = std::max(gb, gemm_ws_bytes(g, Fi, Fi, Fo));
+      break;
+    }
+    case SAGA_LAYER_GATED_GRU: {
+      gb = gemm_ws_bytes(g, Fi, 0, Fi);
+      g.mode = SAGA_GEMM_GRU;
+      gb = std::max(gb, gemm_ws_bytes(g, Fi, Fi, 3 * Fi));
+      break;
+    }
+  }
+  b->gws_bytes = gb;
+  b->gws = c.take(gb);
   return c.used;
 }
 
@@ -469,7 +523,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
         g.mode = SAGA_GEMM_PLAIN;
         g.row_scale_deg = p.d_out;
         s = run_gemm(g, x, saga_cmat{d.w, Fi, Fo, Fo}, none, none, nullptr, nullptr,
-                     saga_mat{b.z, V, Fo, b.ldz}, st);
+                     saga_mat{b.z, V, Fo, b.ldz}, b.gws, b.gws_bytes, st);
         if (s) return s;
         op.msg = SAGA_MSG_COPY;
         op.reduce = SAGA_RED_SUM;
@@ -489,7 +543,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       g.mode = SAGA_GEMM_PLAIN;
       g.act = d.act;
       return run_gemm(g, saga_cmat{b.z2, V, Fi, b.ldz2}, saga_cmat{d.w, Fi, Fo, Fo}, none, none,
-                      d.b, nullptr, out, st);
+                      d.b, nullptr, out, b.gws, b.gws_bytes, st);
     }
     case SAGA_LAYER_GAT: {
       const int64_t H = d.heads;
@@ -500,7 +554,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       if (e != hipSuccess) return dev_fail(e, "fold launch");
       g.mode = SAGA_GEMM_PLAIN;
       s = run_gemm(g, x, saga_cmat{b.wext, Fi, cols, b.ldw}, none, none, nullptr, nullptr,
-                   saga_mat{b.z, V, cols, b.ldz}, st);
+                   saga_mat{b.z, V, cols, b.ldz}, b.gws, b.gws_bytes, st);
       if (s) return s;
       const float* z = static_cast<const float*>(b.z);
       op.msg = SAGA_MSG_GAT;
@@ -519,7 +573,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       g.mode = SAGA_GEMM_PLAIN;
       g.act = SAGA_ACT_RELU;
       s = run_gemm(g, x, saga_cmat{d.w_pool, Fi, Fi, Fi}, none, none, d.b_pool, nullptr,
-                   saga_mat{b.z, V, Fi, b.ldz}, st);
+                   saga_mat{b.z, V, Fi, b.ldz}, b.gws, b.gws_bytes, st);
       if (s) return s;
       op.msg = SAGA_MSG_COPY;
       op.reduce = SAGA_RED_MAX;
@@ -530,16 +584,16 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       g.mode = SAGA_GEMM_CONCAT;
       g.act = SAGA_ACT_NONE;
       return run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, Fi, b.ldz2},
-                      saga_cmat{w + (size_t)Fi * Fo * es, Fi, Fo, Fo}, d.b, nullptr, out, st);
+                      saga_cmat{w + (size_t)Fi * Fo * es, Fi, Fo, Fo}, d.b, nullptr, out, b.gws, b.gws_bytes, st);
     }
     case SAGA_LAYER_GATED_GRU: {
       const int64_t F = Fi, Fe = d.edge_feat;
       g.mode = SAGA_GEMM_PLAIN;
       s = run_gemm(g, x, saga_cmat{d.w_e, F, F, F}, none, none, nullptr, nullptr,
-                   saga_mat{b.z, V, F, b.ldz}, st);
+                   saga_mat{b.z, V, F, b.ldz}, b.gws, b.gws_bytes, st);
       if (s) return s;
       s = run_gemm(g, x, saga_cmat{d.w_e + F * F, F, F, F}, none, none, nullptr, nullptr,
-                   saga_mat{b.z2, V, F, b.ldz2}, st);
+                   saga_mat{b.z2, V, F, b.ldz2}, b.gws, b.gws_bytes, st);
       if (s) return s;
       op.msg = SAGA_MSG_GATED;
       op.reduce = SAGA_RED_SUM;
@@ -554,7 +608,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       if (s) return s;
       g.mode = SAGA_GEMM_GRU;
       return run_gemm(g, saga_cmat{b.z3, V, F, b.ldz3}, saga_cmat{d.w_ih, F, 3 * F, 3 * F}, x,
-                      saga_cmat{d.w_hh, F, 3 * F, 3 * F}, d.b_ih, d.b_hh, out, st);
+                      saga_cmat{d.w_hh, F, 3 * F, 3 * F}, d.b_ih, d.b_hh, out, b.gws, b.gws_bytes, st);
     }
   }
   return fail(SAGA_EINVAL, "bad layer kind");
@@ -707,12 +761,28 @@ saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edg
   }
 }
 
+saga_status saga_apply_vertex_workspace_size(const saga_gemm_op* op, int64_t k, int64_t k2,
+                                             int64_t n, size_t* bytes) {
+  try {
+    if (!op || !bytes) return fail(SAGA_EINVAL, "null argument");
+    if (op->dtype != SAGA_F32 && op->dtype != SAGA_BF16) return fail(SAGA_EINVAL, "bad dtype");
+    if (op->mode < SAGA_GEMM_PLAIN || op->mode > SAGA_GEMM_GRU) return fail(SAGA_EINVAL, "bad mode");
+    if (k <= 0 || n <= 0 || (op->mode != SAGA_GEMM_PLAIN && k2 <= 0))
+      return fail(SAGA_EINVAL, "k, n (and k2 for concat/GRU) must be > 0");
+    *bytes = gemm_ws_bytes(*op, k, k2, n);
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
 saga_status saga_apply_vertex(const saga_gemm_op* op, saga_cmat a, saga_cmat w, saga_cmat a2,
                               saga_cmat w2, const float* bias, const float* bias2, saga_mat out,
-                              void* stream) {
+                              void* workspace, size_t workspace_bytes, void* stream) {
   try {
     if (!op) return fail(SAGA_EINVAL, "op is null");
-    return run_gemm(*op, a, w, a2, w2, bias, bias2, out, static_cast<hipStream_t>(stream));
+    return run_gemm(*op, a, w, a2, w2, bias, bias2, out, workspace, workspace_bytes,
+                    static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(SAGA_EINTERNAL, "exception");
   }

@@ -4,16 +4,31 @@
 // activation, the two-operand concat form [a | a2][w ; w2], and the GRU
 // gate math of GGNN's ApplyVertex, Fig. 2).
 //
-// Tiling: a workgroup of 4 waves owns BM = 4 * MT * 16 rows and NT * 16
-// columns.  A wave computes MT x NT tiles of 16 x 16 with
+// Tiling: a workgroup of 4 waves owns BM = 64 MT rows and BN = 16 NT
+// columns; wave w computes rows [16 MT w, 16 MT (w + 1)) of the tile as
+// MT x NT blocks of 16 x 16 with
 //   float32 : v_mfma_f32_16x16x4f32   (4 k per instruction)
-//   bfloat16: v_mfma_f32_16x16x32_bf16 (32 k per instruction, gfx950)
-// A fragments come straight from global memory as 16-byte row slices (lane
-// l reads row l % 16 at k offset (l / 16) * EPL, which is the operand layout
-// up to a permutation of k that A and B share); the weight chunk of KC rows
-// is staged transposed in LDS so each lane reads its B fragment as one
-// 16-byte LDS load.
+//   bfloat16: v_mfma_f32_16x16x32_bf16 (32 k per instruction)
+//
+// Data path.  K is cut into chunks of 128 bytes per row (32 float32 or 64
+// bfloat16 values).  For every chunk the BM rows of A and the BN rows of the
+// packed weights Wt (W transposed, zero-padded to whole tiles, built in the
+// workspace by k_pack_wt) go straight from global memory into one stage of
+// an S-stage LDS ring with direct-to-LDS loads (global_load_lds_dwordx4).
+// Nothing is staged through registers, so the loads of later stages never
+// wait behind one another and S - 1 chunks stay in flight while one is
+// multiplied.  Inside a 128-byte row the eight 16-byte pieces are XOR
+// swizzled (piece p of row r at slot 8 r + (p ^ ((r >> 1) & 7))), so that a
+// fragment read -- 16 rows at one k offset -- touches every LDS bank once.
+// A lane's 16-byte fragment holds EPL consecutive k of one row; A and Wt
+// use the same k order, so the products are exact sums over k.
+//
+// The chunk holding the end of K is loaded first, through registers, with
+// zeros past column K and past row M; every later chunk is a whole 128-byte
+// row segment and needs no masking in k.
+#include <algorithm>
 #include <cstdlib>
+#include <cstring>
 
 #include "saga_device.h"
 #include "saga_internal.h"
@@ -23,252 +38,447 @@ namespace {
 
 constexpr int kThreads = 256;
 
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
 template <typename T> struct Mma;
 
 template <> struct Mma<float> {
-  static constexpr int EPL = 4;     // elements per lane per fragment
-  static constexpr int KSTEP = 16;  // k covered by one fragment set
-  static constexpr int KC = 32;     // k rows of W staged per LDS chunk
-  static constexpr int PAD = 4;
+  static constexpr int EPL = 4;     // elements per 16-byte fragment
+  static constexpr int KC = 32;     // k per 128-byte chunk
   typedef f32x4 Frag;
-  __device__ __forceinline__ static void mma(const Frag& a, const Frag& b, f32x4& c) {
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
-  }
-  __device__ __forceinline__ static Frag zero() { return Frag{0.f, 0.f, 0.f, 0.f}; }
   __device__ __forceinline__ static float to_f(float x) { return x; }
   __device__ __forceinline__ static float from_f(float x) { return x; }
 };
 
 template <> struct Mma<uint16_t> {
   static constexpr int EPL = 8;
-  static constexpr int KSTEP = 32;
   static constexpr int KC = 64;
-  static constexpr int PAD = 8;
   typedef bf16x8 Frag;
-  __device__ __forceinline__ static void mma(const Frag& a, const Frag& b, f32x4& c) {
-    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  }
-  __device__ __forceinline__ static Frag zero() {
-    Frag f;
-    uint4 z = make_uint4(0, 0, 0, 0);
-    __builtin_memcpy(&f, &z, 16);
-    return f;
-  }
   __device__ __forceinline__ static float to_f(uint16_t x) { return bf16_to_f32(x); }
   __device__ __forceinline__ static uint16_t from_f(float x) { return f32_to_bf16(x); }
 };
 
-// 16-byte fragment of row r, columns [k, k + EPL), zero outside [0,M) x [0,K)
-template <typename T>
-__device__ __forceinline__ typename Mma<T>::Frag load_a(const T* __restrict__ A, int64_t lda,
-                                                        int64_t r, int64_t k, int64_t M,
-                                                        int64_t K) {
-  constexpr int EPL = Mma<T>::EPL;
-  typename Mma<T>::Frag f = Mma<T>::zero();
-  if (r < M && k < K) {
-    const T* p = A + r * lda + k;
-    if (k + EPL <= K) {
-      __builtin_memcpy(&f, p, 16);
-    } else {
-      T tmp[EPL];
-#pragma unroll
-      for (int i = 0; i < EPL; ++i) tmp[i] = (k + i < K) ? p[i] : T(0);
-      __builtin_memcpy(&f, tmp, 16);
-    }
-  }
-  return f;
+__device__ __forceinline__ int swz(int r, int p) { return r * 8 + (p ^ ((r >> 1) & 7)); }
+
+// s_waitcnt vmcnt(N) (gfx9 encoding; expcnt and lgkmcnt left at their maxima)
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt out of range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// ---------------------------------------------------------------------------
-// Software pipeline (per workgroup, per K chunk of KC):
-//   * the A fragments of chunk i+1 are loaded into registers while the MFMAs
-//     of chunk i run (A streams from HBM once, straight into registers);
-//   * the W rows of chunk i+1 are loaded into registers, then written
-//     transposed into the other half of a double-buffered LDS tile after
-//     the MFMAs of chunk i, so there is one barrier per chunk;
-//   * MFMAs are issued k-step-major, then n-tile, then m-tile, so that
-//     consecutive updates of one accumulator are MT*NT instructions apart.
-// ---------------------------------------------------------------------------
-// A K chunk of W (KC rows x BN columns) passes through registers into the
-// transposed LDS tile Bt[n][k].  Thread t owns K-row group t % KG and a
-// column block t / KG, so that for every column the lanes of a half-wave
-// write consecutive LDS words (no bank conflicts beyond 2-way).
-//   float32 : KG = KC = 32 rows, one row per thread
-//   bfloat16: KG = KC / 2 = 32 row pairs, packed as one 32-bit word
-template <typename T, int NT>
-struct BStage {
-  static constexpr int KC = Mma<T>::KC;
-  static constexpr int BN = NT * 16;
-  static constexpr int RPT = sizeof(T) == 4 ? 1 : 2;  // K rows per thread
-  static constexpr int KG = KC / RPT;                 // 32
-  static constexpr int NBLK = kThreads / KG;          // 8 column blocks
-  static constexpr int CPT = (BN + NBLK - 1) / NBLK;  // columns per thread
-  T v[RPT][CPT];
+// Workgroup barrier for the LDS ring.  A plain __syncthreads() would also
+// wait for every direct-to-LDS load in flight (its release fence covers LDS
+// writes, and those loads write LDS), which would drain the ring at every
+// chunk.  Here the caller has already waited for the stage it needs; the
+// barrier only orders this wave's own LDS reads and writes.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
-  __device__ __forceinline__ void load(const T* __restrict__ W, int64_t ldw, int64_t K, int64_t N,
-                                       int64_t k0, int64_t n0, bool vec_ok) {
-    const int kg = threadIdx.x % KG, nb = threadIdx.x / KG;
-    const int64_t nbase = n0 + (int64_t)nb * CPT;
+template <typename T, int MT, int NT, int S>
+struct Ring {
+  static constexpr int BM = 64 * MT, BN = 16 * NT;
+  static constexpr int A_SLOTS = BM * 8, B_SLOTS = BN * 8;  // 16-byte slots
+  static constexpr int STAGE = A_SLOTS + B_SLOTS;
+  static constexpr int RING_SLOTS = S * STAGE;
+  static constexpr int THREADS = kThreads;
+  static constexpr int LA = A_SLOTS / kThreads;              // loads per thread per stage
+  static constexpr int LB = (B_SLOTS + kThreads - 1) / kThreads;
+  // fewest loads any wave issues per stage (waves past the end of a partial
+  // B row skip the last one); waiting on this count is exact or conservative
+  static constexpr int LMIN = LA + B_SLOTS / kThreads;
+  static_assert(A_SLOTS % kThreads == 0, "A tile must be whole wave loads");
+  static_assert(B_SLOTS % 64 == 0, "B tile must be whole wave loads");
+  static_assert((S - 2) * LMIN < 64, "vmcnt range");
+  static_assert(S >= 2, "at least two stages");
+  static constexpr size_t LDS_BYTES = (size_t)S * STAGE * 16;
+
+  // direct-to-LDS loads of chunk k0 of rows [row0, row0 + BM) of A (rows
+  // >= M skipped) and rows [n0, n0 + BN) of Wt into one stage
+  __device__ __forceinline__ static void issue_a(const T* __restrict__ A, int64_t lda, int64_t M,
+                                                 int64_t row0, int64_t k0, uint4* st) {
+    constexpr int EPL = Mma<T>::EPL;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int r = 0; r < RPT; ++r) {
-      const int64_t k = k0 + (int64_t)kg * RPT + r;
-      const bool kin = k < K;
-      if (kin && vec_ok && (CPT * sizeof(T)) % 16 == 0 && nbase + CPT <= N && nb * CPT < BN) {
+    for (int j = 0; j < LA; ++j) {
+      const int s0 = j * kThreads + wave * 64;
+      const int s = s0 + lane, r = s >> 3, p = (s & 7) ^ ((r >> 1) & 7);
+      if (row0 + r < M)
+        __builtin_amdgcn_global_load_lds(A + (row0 + r) * lda + k0 + p * EPL, (lds_ptr)(st + s0), 16, 0, 0);
+    }
+  }
+  __device__ __forceinline__ static void issue_b(const T* __restrict__ Wt, int64_t kp, int64_t n0,
+                                                 int64_t k0, uint4* st) {
+    constexpr int EPL = Mma<T>::EPL;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-        for (int c = 0; c < CPT; c += 16 / (int)sizeof(T))
-          __builtin_memcpy(&v[r][c], W + k * ldw + nbase + c, 16);
-      } else {
-#pragma unroll
-        for (int c = 0; c < CPT; ++c)
-          v[r][c] = (kin && nbase + c < N && nb * CPT + c < BN) ? W[k * ldw + nbase + c] : T(0);
+    for (int j = 0; j < LB; ++j) {
+      const int s0 = j * kThreads + wave * 64;
+      if (s0 < B_SLOTS) {
+        const int s = s0 + lane, n = s >> 3, p = (s & 7) ^ ((n >> 1) & 7);
+        __builtin_amdgcn_global_load_lds(Wt + (n0 + n) * kp + k0 + p * EPL,
+                                         (lds_ptr)(st + A_SLOTS + s0), 16, 0, 0);
       }
     }
   }
-  __device__ __forceinline__ void store(T* Bt) const {
-    constexpr int LDB = KC + Mma<T>::PAD;
-    const int kg = threadIdx.x % KG, nb = threadIdx.x / KG;
+
+  // vmcnt wait that leaves only the loads of the next `later` stages pending;
+  // `tail` says the last of them is the K-tail stage, which issues only its
+  // B loads (its A part was loaded into registers before every other load)
+  static constexpr int LBMIN = B_SLOTS / kThreads;
+  __device__ __forceinline__ static void wait_stages(int later, bool tail) {
+    if constexpr (S >= 4) {
+      if (later >= 2) {
+        if (tail) wait_vm<LMIN + LBMIN>(); else wait_vm<2 * LMIN>();
+        return;
+      }
+    }
+    if constexpr (S >= 3) {
+      if (later == 1) {
+        if (tail) wait_vm<LBMIN>(); else wait_vm<LMIN>();
+        return;
+      }
+    }
+    wait_vm<0>();
+  }
+
+  // The A tail chunk through registers.  A piece that starts below K is
+  // loaded whole (it ends within the row's ld, which is a multiple of 16
+  // bytes); the values at columns >= K, and whole pieces past row M or
+  // column K, are zeroed when the piece is written to LDS.  The loads are
+  // unconditional, so nothing has to wait for them before the stage opens.
+  struct Tail {
+    uint4 v[LA];
+    int nv[LA];  // valid elements of each piece (0 .. EPL)
+    __device__ __forceinline__ void load(const T* __restrict__ A, int64_t lda, int64_t M, int64_t K,
+                                         int64_t row0, int64_t k0) {
+      constexpr int EPL = Mma<T>::EPL;
+      const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int n = nb * CPT + c;
-      if (n < BN) {
-        if constexpr (RPT == 1) {
-          Bt[n * LDB + kg] = v[0][c];
-        } else {
-          const uint32_t w = (uint32_t)v[0][c] | ((uint32_t)v[1][c] << 16);
-          *reinterpret_cast<uint32_t*>(Bt + n * LDB + kg * 2) = w;
+      for (int j = 0; j < LA; ++j) {
+        const int s = j * kThreads + wave * 64 + lane, r = s >> 3, p = (s & 7) ^ ((r >> 1) & 7);
+        const int64_t row = row0 + r, k = k0 + p * EPL;
+        const int64_t left = K - k;
+        nv[j] = row < M ? (int)(left <= 0 ? 0 : left >= EPL ? EPL : left) : 0;
+        // pieces with nothing valid read an in-range piece instead (no branch)
+        const int64_t rr = row < M ? row : M - 1;
+        const int64_t kk = left > 0 ? k : (K - 1) / EPL * EPL;
+        v[j] = *reinterpret_cast<const uint4*>(A + rr * lda + kk);
+      }
+    }
+    __device__ __forceinline__ void store(uint4* st) const {
+      constexpr int EPL = Mma<T>::EPL;
+      const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+      for (int j = 0; j < LA; ++j) {
+        uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          if constexpr (EPL == 4) {
+            if (d >= nv[j]) w[d] = 0;
+          } else {  // two bfloat16 per word
+            if (2 * d >= nv[j]) w[d] = 0;
+            else if (2 * d + 1 >= nv[j]) w[d] &= 0xffffu;
+          }
         }
+        st[j * kThreads + wave * 64 + lane] = make_uint4(w[0], w[1], w[2], w[3]);
       }
     }
-  }
-};
+  };
 
-template <typename T, int MT>
-__device__ __forceinline__ void load_a_chunk(const T* __restrict__ A, int64_t lda, int64_t M,
-                                             int64_t K, int64_t row0, int64_t k0,
-                                             typename Mma<T>::Frag (&af)[Mma<T>::KC / Mma<T>::KSTEP][MT]) {
-  constexpr int EPL = Mma<T>::EPL;
-  constexpr int NS = Mma<T>::KC / Mma<T>::KSTEP;
-  const int lane = threadIdx.x & 63;
-  const int lr = lane & 15, lg = lane >> 4;
+  // acc += (one chunk of A rows of this wave) x (chunk of Wt).  All
+  // fragments of the chunk are read before the first MFMA, so the reads of
+  // the second k-step complete under the MFMAs of the first.
+  __device__ __forceinline__ static void compute(const uint4* st, f32x4 (&acc)[MT][NT]) {
+    typedef typename Mma<T>::Frag Frag;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lr = lane & 15, lg = lane >> 4;
+    const uint4* As = st;
+    const uint4* Bs = st + A_SLOTS;
+    Frag a[2][MT], b[2][NT];
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
+    for (int h = 0; h < 2; ++h) {  // two k-steps of 64 bytes
+      const int p = h * 4 + lg;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-      af[s][mt] = load_a<T>(A, lda, row0 + mt * 16 + lr, k0 + s * Mma<T>::KSTEP + lg * EPL, M, K);
-}
-
-template <typename T, int MT, int NT>
-__device__ __forceinline__ void mma_chunk(const T* Bt,
-                                          const typename Mma<T>::Frag (&af)[Mma<T>::KC / Mma<T>::KSTEP][MT],
-                                          f32x4 (&acc)[MT][NT]) {
-  constexpr int EPL = Mma<T>::EPL;
-  constexpr int KSTEP = Mma<T>::KSTEP;
-  constexpr int NS = Mma<T>::KC / KSTEP;
-  constexpr int LDB = Mma<T>::KC + Mma<T>::PAD;
-  const int lane = threadIdx.x & 63;
-  const int lr = lane & 15, lg = lane >> 4;
+      for (int mt = 0; mt < MT; ++mt) {
+        const uint4 v = As[swz(wave * MT * 16 + mt * 16 + lr, p)];
+        __builtin_memcpy(&a[h][mt], &v, 16);
+      }
 #pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    typename Mma<T>::Frag bf[NT];
+      for (int nt = 0; nt < NT; ++nt) {
+        const uint4 v = Bs[swz(nt * 16 + lr, p)];
+        __builtin_memcpy(&b[h][nt], &v, 16);
+      }
+    }
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      __builtin_memcpy(&bf[nt], Bt + (nt * 16 + lr) * LDB + s * KSTEP + lg * EPL, 16);
-    if constexpr (sizeof(T) == 4) {
+    for (int h = 0; h < 2; ++h) {
+      if constexpr (sizeof(T) == 4) {
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[h][mt][c], b[h][nt][c], acc[mt][nt], 0, 0, 0);
+      } else {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
-            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[s][mt][c], bf[nt][c], acc[mt][nt], 0, 0, 0);
-    } else {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) Mma<T>::mma(af[s][mt], bf[nt], acc[mt][nt]);
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[h][mt], b[h][nt], acc[mt][nt], 0, 0, 0);
+      }
     }
   }
-}
 
-// acc += A[row0 .. row0 + 16 MT) x W[:, n0 .. n0 + 16 NT)
-//
-// The A fragments of chunks ci+1 .. ci+PD-1 are in flight (registers) while
-// chunk ci is multiplied; the loop is unrolled by PD so every register slot
-// has a compile-time index.  The W chunk ci+1 is loaded into registers at the
-// top of step ci and written (transposed) into the other LDS half after the
-// MFMAs; one barrier per chunk.
-template <typename T, int MT, int NT, int PD>
-struct Pipe {
-  typedef typename Mma<T>::Frag Frag;
-  static constexpr int KC = Mma<T>::KC;
-  static constexpr int NS = KC / Mma<T>::KSTEP;
-  const T* A; int64_t lda; const T* W; int64_t ldw; int64_t M, N, K, row0, n0;
-  bool vec_ok; int nchunks;
-  T* Bt0; T* Bt1;
-  BStage<T, NT> bs;
-
-  __device__ __forceinline__ void step(int ci, Frag (&a)[NS][MT], f32x4 (&acc)[MT][NT]) {
-    const bool more = ci + 1 < nchunks;
-    if (more) bs.load(W, ldw, K, N, (int64_t)(ci + 1) * KC, n0, vec_ok);
-    mma_chunk<T, MT, NT>((ci & 1) ? Bt1 : Bt0, a, acc);
-    if (ci + PD < nchunks) load_a_chunk<T, MT>(A, lda, M, K, row0, (int64_t)(ci + PD) * KC, a);
-    if (more) bs.store((ci & 1) ? Bt0 : Bt1);
-    __syncthreads();
+  // acc += A[row0 .. row0 + BM) x W[:, n0 .. n0 + BN), W given packed as Wt
+  // (ld kp, zero-padded).  Stage j holds chunk j.  Chunks 0 .. nch-2 are
+  // whole and loaded direct-to-LDS.  The A part of the last one (the K tail)
+  // is loaded into registers before anything else and written to LDS just
+  // before the barrier that opens its stage; its B part is loaded like the
+  // others.  Loads complete in issue order, so waiting until at most the
+  // loads of the stages issued after stage i are pending means stage i has
+  // landed; the counts used are the fewest any wave issues.
+  __device__ __forceinline__ static void phase(const T* __restrict__ A, int64_t lda, int64_t M,
+                                               int64_t K, const T* __restrict__ Wt, int64_t kp,
+                                               int64_t row0, int64_t n0, uint4* ring,
+                                               f32x4 (&acc)[MT][NT]) {
+    constexpr int KC = Mma<T>::KC;
+    const int nch = (int)((K + KC - 1) / KC);
+    const int last = nch - 1;
+    Tail tail;
+    tail.load(A, lda, M, K, row0, (int64_t)last * KC);
+    auto issue = [&](int j) {
+      uint4* st = ring + (j % S) * STAGE;
+      if (j < last) issue_a(A, lda, M, row0, (int64_t)j * KC, st);
+      issue_b(Wt, kp, n0, (int64_t)j * KC, st);
+    };
+    for (int j = 0; j < S - 1 && j < nch; ++j) issue(j);
+    for (int i = 0; i < nch; ++i) {
+      const int ahead = last - i;
+      const int later = ahead < S - 2 ? ahead : S - 2;
+      wait_stages(later, later > 0 && ahead <= S - 2);  // this wave's loads of stage i landed
+      if (i == last) tail.store(ring + (i % S) * STAGE);
+      ring_barrier();  // ... and every wave's; stage i - 1 is free again
+      if (i + S - 1 < nch) issue(i + S - 1);
+      compute(ring + (i % S) * STAGE, acc);
+    }
+    ring_barrier();  // the ring may be refilled by a following phase
   }
 };
 
-template <typename T, int MT, int NT>
-__device__ __forceinline__ void mma_phase(const T* __restrict__ A, int64_t lda,
-                                          const T* __restrict__ W, int64_t ldw, int64_t M,
-                                          int64_t N, int64_t K, int64_t row0, int64_t n0,
-                                          T* Bt0, T* Bt1, f32x4 (&acc)[MT][NT]) {
-  constexpr int PD = 3;  // chunks of A in flight
-  constexpr int KC = Mma<T>::KC;
-  constexpr int NS = KC / Mma<T>::KSTEP;
+// Second data path: A straight from global memory into registers, only
+// the packed weights through the LDS ring.  Each wave owns its A rows, so
+// A needs no sharing through LDS; the ring then holds only the BN x 128-byte
+// weight chunks (16 KB per stage for BN = 128), which leaves LDS room for
+// more resident workgroups.  A chunk's A and Wt loads are issued together,
+// S - 1 chunks ahead, so one vmcnt wait covers both.
+template <typename T, int MT, int NT, int S, int NW = 4>
+struct RegA {
   typedef typename Mma<T>::Frag Frag;
-  Pipe<T, MT, NT, PD> p;
-  p.A = A; p.lda = lda; p.W = W; p.ldw = ldw; p.M = M; p.N = N; p.K = K; p.row0 = row0; p.n0 = n0;
-  p.vec_ok = ((ldw * (int64_t)sizeof(T)) % 16 == 0) && ((uintptr_t)W % 16 == 0);
-  p.nchunks = (int)((K + KC - 1) / KC);
-  p.Bt0 = Bt0;
-  p.Bt1 = Bt1;
-  Frag a0[NS][MT], a1[NS][MT], a2[NS][MT];
-  p.bs.load(W, ldw, K, N, 0, n0, p.vec_ok);
-  load_a_chunk<T, MT>(A, lda, M, K, row0, 0, a0);
-  if (p.nchunks > 1) load_a_chunk<T, MT>(A, lda, M, K, row0, KC, a1);
-  if (p.nchunks > 2) load_a_chunk<T, MT>(A, lda, M, K, row0, 2 * KC, a2);
-  __syncthreads();  // the LDS tiles may still be read by a previous phase
-  p.bs.store(Bt0);
-  __syncthreads();
-  for (int ci = 0; ci < p.nchunks; ci += PD) {
-    p.step(ci, a0, acc);
-    if (ci + 1 < p.nchunks) p.step(ci + 1, a1, acc);
-    if (ci + 2 < p.nchunks) p.step(ci + 2, a2, acc);
+  static constexpr int THREADS = 64 * NW;  // NW waves, each 16 MT rows
+  static constexpr int BM = 16 * MT * NW, BN = 16 * NT;
+  static constexpr int B_SLOTS = BN * 8;
+  static constexpr int STAGE = B_SLOTS;
+  static constexpr int RING_SLOTS = S * STAGE;
+  static constexpr int LA = 2 * MT;  // 16-byte A loads per lane per chunk
+  static constexpr int LB = (B_SLOTS + THREADS - 1) / THREADS;
+  static constexpr int LMIN = LA + B_SLOTS / THREADS;
+  static_assert(B_SLOTS % 64 == 0, "B tile must be whole wave loads");
+  static_assert(S >= 2 && (S - 2) * LMIN < 64, "vmcnt range");
+  static constexpr size_t LDS_BYTES = (size_t)RING_SLOTS * 16;
+
+  // fragment (h, mt) of chunk k0: row r0 + 16 mt + lane % 16, columns
+  // k0 + (4 h + lane / 16) EPL ..  Rows >= M read row M - 1 (their results
+  // are never stored); a piece that starts at or past K reads the last piece
+  // of the row instead and is zeroed by mask() before use.  A piece that
+  // starts below K ends within the row's ld (a multiple of 16 bytes).
+  __device__ __forceinline__ static void load_a(const T* __restrict__ A, int64_t lda, int64_t M,
+                                                int64_t K, int64_t r0, int64_t k0,
+                                                Frag (&a)[2][MT]) {
+    constexpr int EPL = Mma<T>::EPL;
+    const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int64_t row = r0 + mt * 16 + lr, k = k0 + (h * 4 + lg) * EPL;
+        const int64_t rr = row < M ? row : M - 1;
+        const int64_t kk = k < K ? k : (K - 1) / EPL * EPL;
+        const uint4 v = *reinterpret_cast<const uint4*>(A + rr * lda + kk);
+        __builtin_memcpy(&a[h][mt], &v, 16);
+      }
+  }
+  // zero the values at columns >= K (the tail chunk)
+  __device__ __forceinline__ static void mask(int64_t K, int64_t k0, Frag (&a)[2][MT]) {
+    constexpr int EPL = Mma<T>::EPL;
+    const int lg = (threadIdx.x & 63) >> 4;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t left = K - (k0 + (h * 4 + lg) * EPL);
+      const int nv = left <= 0 ? 0 : left >= EPL ? EPL : (int)left;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        uint32_t w[4];
+        __builtin_memcpy(w, &a[h][mt], 16);
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          if constexpr (EPL == 4) {
+            if (d >= nv) w[d] = 0;
+          } else {
+            if (2 * d >= nv) w[d] = 0;
+            else if (2 * d + 1 >= nv) w[d] &= 0xffffu;
+          }
+        }
+        __builtin_memcpy(&a[h][mt], w, 16);
+      }
+    }
+  }
+  __device__ __forceinline__ static void issue_b(const T* __restrict__ Wt, int64_t kp, int64_t n0,
+                                                 int64_t k0, uint4* st) {
+    constexpr int EPL = Mma<T>::EPL;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int j = 0; j < LB; ++j) {
+      const int s0 = j * THREADS + wave * 64;
+      if (s0 < B_SLOTS) {
+        const int s = s0 + lane, n = s >> 3, p = (s & 7) ^ ((n >> 1) & 7);
+        __builtin_amdgcn_global_load_lds(Wt + (n0 + n) * kp + k0 + p * EPL, (lds_ptr)(st + s0), 16, 0, 0);
+      }
+    }
+  }
+  __device__ __forceinline__ static void wait_stages(int later) {
+    if constexpr (S >= 4) {
+      if (later >= 2) { wait_vm<2 * LMIN>(); return; }
+    }
+    if constexpr (S >= 3) {
+      if (later == 1) { wait_vm<LMIN>(); return; }
+    }
+    wait_vm<0>();
+  }
+  __device__ __forceinline__ static void compute(const uint4* Bs, const Frag (&a)[2][MT],
+                                                 f32x4 (&acc)[MT][NT]) {
+    const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+    Frag b[2][NT];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const uint4 v = Bs[swz(nt * 16 + lr, h * 4 + lg)];
+        __builtin_memcpy(&b[h][nt], &v, 16);
+      }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[h][mt][c], b[h][nt][c], acc[mt][nt], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[h][mt], b[h][nt], acc[mt][nt], 0, 0, 0);
+      }
+    }
+  }
+
+  struct Ctx {
+    const T* A; int64_t lda, M, K;
+    const T* Wt; int64_t kp, n0, r0;
+    uint4* ring;
+    int nch, last;
+  };
+
+  // chunk i = i0 + U: uses register slot U and ring stage U
+  template <int U>
+  __device__ __forceinline__ static void step(const Ctx& c, int i0, Frag (&a)[S][2][MT],
+                                              f32x4 (&acc)[MT][NT]) {
+    constexpr int KC = Mma<T>::KC;
+    constexpr int NU = (U + S - 1) % S;
+    const int i = i0 + U;
+    if (i >= c.nch) return;
+    wait_stages(c.last - i < S - 2 ? c.last - i : S - 2);  // chunk i's loads landed
+    ring_barrier();  // every wave's; stage i - 1 is free again
+    if (i + S - 1 < c.nch) {
+      load_a(c.A, c.lda, c.M, c.K, c.r0, (int64_t)(i + S - 1) * KC, a[NU]);
+      issue_b(c.Wt, c.kp, c.n0, (int64_t)(i + S - 1) * KC, c.ring + NU * STAGE);
+    }
+    if (i == c.last) mask(c.K, (int64_t)i * KC, a[U]);
+    compute(c.ring + U * STAGE, a[U], acc);
+  }
+
+  // acc += A[tile0 .. tile0 + BM) x W[:, n0 .. n0 + BN); chunk i uses
+  // register slot i % S and ring stage i % S (the loop is unrolled by S so
+  // both are compile-time)
+  __device__ __forceinline__ static void phase(const T* __restrict__ A, int64_t lda, int64_t M,
+                                               int64_t K, const T* __restrict__ Wt, int64_t kp,
+                                               int64_t tile0, int64_t n0, uint4* ring,
+                                               f32x4 (&acc)[MT][NT]) {
+    static_assert(S <= 4, "unrolled for at most four stages");
+    constexpr int KC = Mma<T>::KC;
+    Ctx c;
+    c.A = A; c.lda = lda; c.M = M; c.K = K; c.Wt = Wt; c.kp = kp; c.n0 = n0;
+    c.r0 = tile0 + (threadIdx.x >> 6) * MT * 16;
+    c.ring = ring;
+    c.nch = (int)((K + KC - 1) / KC);
+    c.last = c.nch - 1;
+    Frag a[S][2][MT];
+#pragma unroll
+    for (int j = 0; j < S - 1; ++j)
+      if (j < c.nch) {
+        load_a(A, lda, M, K, c.r0, (int64_t)j * KC, a[j]);
+        issue_b(Wt, kp, n0, (int64_t)j * KC, ring + j * STAGE);
+      }
+    for (int i0 = 0; i0 < c.nch; i0 += S) {
+      step<0>(c, i0, a, acc);
+      step<1>(c, i0, a, acc);
+      if constexpr (S > 2) step<2>(c, i0, a, acc);
+      if constexpr (S > 3) step<3>(c, i0, a, acc);
+    }
+    ring_barrier();  // the ring may be refilled by a following phase
+  }
+};
+
+// Wt[n][k] = W[k][n] for n < N, k < K, else 0; Wt is Np x Kp with ld Kp
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_pack_wt(const T* __restrict__ W, int64_t ldw,
+                                                      int64_t K, int64_t N, T* __restrict__ Wt,
+                                                      int64_t Kp, int64_t Np) {
+  const int64_t total = Np * Kp;
+  for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kThreads) {
+    const int64_t n = i / Kp, k = i - n * Kp;
+    Wt[i] = (n < N && k < K) ? W[k * ldw + n] : T(0);
   }
 }
 
 // PLAIN / CONCAT
-template <typename T, int MT, int NT>
-__global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
-  constexpr int LDB = Mma<T>::KC + Mma<T>::PAD;
-  __shared__ __attribute__((aligned(16))) T Bt[2][NT * 16 * LDB];
+template <typename T, int MT, int NT, typename R>
+__global__ __launch_bounds__(R::THREADS) void k_gemm(GemmArgs g) {
+  __shared__ uint4 ring[R::RING_SLOTS];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t row0 = (int64_t)blockIdx.x * (4 * MT * 16) + wave * MT * 16;
-  const int64_t n0 = (int64_t)blockIdx.y * NT * 16;
+  const int64_t tile0 = (int64_t)blockIdx.x * R::BM;
+  const int64_t n0 = (int64_t)blockIdx.y * R::BN;
   f32x4 acc[MT][NT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  mma_phase<T, MT, NT>(static_cast<const T*>(g.a), g.lda, static_cast<const T*>(g.w), g.ldw, g.M,
-                       g.N, g.K, row0, n0, Bt[0], Bt[1], acc);
+  R::phase(static_cast<const T*>(g.a), g.lda, g.M, g.K, static_cast<const T*>(g.wt), g.kp, tile0,
+           n0, ring, acc);
   if (g.mode == SAGA_GEMM_CONCAT)
-    mma_phase<T, MT, NT>(static_cast<const T*>(g.a2), g.lda2, static_cast<const T*>(g.w2), g.ldw2,
-                         g.M, g.N, g.K2, row0, n0, Bt[0], Bt[1], acc);
+    R::phase(static_cast<const T*>(g.a2), g.lda2, g.M, g.K2, static_cast<const T*>(g.wt2), g.kp2,
+             tile0, n0, ring, acc);
   // epilogue: lane holds rows 4*(lane/16) + r, column lane % 16 of each tile
+  const int64_t row0 = tile0 + wave * MT * 16;
   T* out = static_cast<T*>(g.out);
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
@@ -290,26 +500,25 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
 
 // GRU: acc1 = a w (input gates), acc2 = a2 w2 (hidden gates), column blocks
 // (r, z, n) of width F = NT3 * 16; hidden state h = a2
-template <typename T, int NT3>
+template <typename T, int NT3, int S>
 __global__ __launch_bounds__(kThreads) void k_gemm_gru(GemmArgs g) {
   constexpr int NT = 3 * NT3;
-  constexpr int LDB = Mma<T>::KC + Mma<T>::PAD;
-  __shared__ __attribute__((aligned(16))) T Bt[2][NT * 16 * LDB];
+  typedef RegA<T, 1, NT, S> R;
+  __shared__ uint4 ring[R::RING_SLOTS];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t row0 = (int64_t)blockIdx.x * (4 * 16) + wave * 16;
+  const int64_t tile0 = (int64_t)blockIdx.x * R::BM;
   f32x4 acc1[1][NT], acc2[1][NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     acc1[0][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     acc2[0][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const T* a = static_cast<const T*>(g.a);
   const T* h = static_cast<const T*>(g.a2);
-  mma_phase<T, 1, NT>(a, g.lda, static_cast<const T*>(g.w), g.ldw, g.M, g.N, g.K, row0, 0, Bt[0],
-                      Bt[1], acc1);
-  mma_phase<T, 1, NT>(h, g.lda2, static_cast<const T*>(g.w2), g.ldw2, g.M, g.N, g.K2, row0, 0,
-                      Bt[0], Bt[1], acc2);
+  R::phase(static_cast<const T*>(g.a), g.lda, g.M, g.K, static_cast<const T*>(g.wt), g.kp, tile0,
+           0, ring, acc1);
+  R::phase(h, g.lda2, g.M, g.K2, static_cast<const T*>(g.wt2), g.kp2, tile0, 0, ring, acc2);
   const int F = NT3 * 16;
+  const int64_t row0 = tile0 + wave * 16;
   T* out = static_cast<T*>(g.out);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
@@ -331,63 +540,159 @@ __global__ __launch_bounds__(kThreads) void k_gemm_gru(GemmArgs g) {
   }
 }
 
-template <typename T, int MT, int NT>
+// ---------------------------------------------------------------------------
+// host side: tiling choice, weight packing, launch
+// ---------------------------------------------------------------------------
+struct Tiling {
+  int mt, nt, stages;
+  bool ring_a;  // A through the LDS ring (Ring) instead of registers (RegA)
+  int nw = 4;   // waves per workgroup (RegA)
+};
+
+// SAGA_GEMM_CFG overrides the tile shape of the N <= 128 kernels for tuning:
+// "aMxS" = A through registers, M = rows per wave / 16, S stages;
+// "rMxS" = A through the LDS ring
+Tiling cfg_override(Tiling t) {
+  static const char* e = getenv("SAGA_GEMM_CFG");
+  if (!e) return t;
+  static const struct { const char* name; Tiling t; } table[] = {
+      {"r2x2", {2, 8, 2, true}}, {"r2x4", {2, 8, 4, true}}, {"a2x4", {2, 8, 4, false}},
+      {"a2x3", {2, 8, 3, false}}, {"a4x3", {4, 8, 3, false}}, {"a4x2", {4, 8, 2, false}},
+      {"a1x4", {1, 8, 4, false}}, {"a2x3w8", {2, 8, 3, false, 8}}, {"a2x2w8", {2, 8, 2, false, 8}},
+      {"a2x4w8", {2, 8, 4, false, 8}}, {"a1x4w8", {1, 8, 4, false, 8}},
+      {"a1x4w16", {1, 8, 4, false, 16}}, {"a1x3w16", {1, 8, 3, false, 16}},
+      {"a1x3w8", {1, 8, 3, false, 8}}};
+  for (const auto& x : table)
+    if (!strcmp(e, x.name)) return x.t;
+  return t;
+}
+
+Tiling choose(int dtype, int mode, int64_t N) {
+  if (mode == SAGA_GEMM_GRU) return Tiling{1, (int)(N / 16), 4, false};
+  const int64_t nt = (N + 15) / 16;
+  if (nt <= 5) return Tiling{2, (int)nt, 4, false};
+  if (nt <= 8)  // measured best on the 2^21 x 602 x 128 transform
+    return cfg_override(dtype == SAGA_BF16 ? Tiling{1, 8, 4, false, 8} : Tiling{2, 8, 2, true});
+  return Tiling{2, 16, 3, false};
+}
+
+int kc_of(int dtype) { return dtype == SAGA_BF16 ? Mma<uint16_t>::KC : Mma<float>::KC; }
+
+struct Packed {
+  int64_t np, kp, kp2;
+  size_t off2, bytes;
+};
+
+Packed packed_layout(int dtype, int mode, int64_t N, int64_t K, int64_t K2) {
+  const Tiling t = choose(dtype, mode, N);
+  const int64_t bn = 16 * t.nt, kc = kc_of(dtype);
+  const size_t es = dtype == SAGA_BF16 ? 2 : 4;
+  Packed p;
+  p.np = (N + bn - 1) / bn * bn;
+  p.kp = (K + kc - 1) / kc * kc;
+  p.kp2 = mode == SAGA_GEMM_PLAIN ? 0 : (K2 + kc - 1) / kc * kc;
+  const size_t b1 = ((size_t)p.np * p.kp * es + 255) / 256 * 256;
+  p.off2 = b1;
+  p.bytes = b1 + ((size_t)p.np * p.kp2 * es + 255) / 256 * 256;
+  return p;
+}
+
+template <typename T, int MT, int NT, typename R>
 hipError_t launch_plain(const GemmArgs& g, hipStream_t st) {
-  const int64_t bm = 4 * MT * 16;
-  dim3 grid((unsigned)((g.M + bm - 1) / bm), (unsigned)((g.N + NT * 16 - 1) / (NT * 16)));
-  hipLaunchKernelGGL((k_gemm<T, MT, NT>), grid, dim3(kThreads), 0, st, g);
+  static_assert(R::LDS_BYTES <= 160 * 1024, "LDS ring too large");
+  dim3 grid((unsigned)((g.M + R::BM - 1) / R::BM), (unsigned)((g.N + R::BN - 1) / R::BN));
+  hipLaunchKernelGGL((k_gemm<T, MT, NT, R>), grid, dim3(R::THREADS), 0, st, g);
   return hipGetLastError();
 }
 
-// rows per wave for N <= 128 (2 x 16 = 32 rows by default); the
-// SAGA_GEMM_MT environment variable (1, 2 or 4) overrides it for tuning
-int gemm_mt() {
-  static int v = [] {
-    const char* e = getenv("SAGA_GEMM_MT");
-    int x = e ? atoi(e) : 2;
-    return (x == 1 || x == 2 || x == 4) ? x : 2;
-  }();
-  return v;
-}
-
 template <typename T, int NT>
-hipError_t launch_nt(const GemmArgs& g, hipStream_t st) {
-  switch (gemm_mt()) {
-    case 1: return launch_plain<T, 1, NT>(g, st);
-    case 2: return launch_plain<T, 2, NT>(g, st);
-    default: return launch_plain<T, 4, NT>(g, st);
+hipError_t launch_nt(const GemmArgs& g, const Tiling& t, hipStream_t st) {
+  if constexpr (NT == 8) {
+    if (t.ring_a) {
+      if (t.stages == 2) return launch_plain<T, 2, 8, Ring<T, 2, 8, 2>>(g, st);
+      return launch_plain<T, 2, 8, Ring<T, 2, 8, 4>>(g, st);
+    }
+    if (t.nw == 16) {
+      if (t.stages == 3) return launch_plain<T, 1, 8, RegA<T, 1, 8, 3, 16>>(g, st);
+      return launch_plain<T, 1, 8, RegA<T, 1, 8, 4, 16>>(g, st);
+    }
+    if (t.nw == 8) {
+      if (t.mt == 1 && t.stages == 3) return launch_plain<T, 1, 8, RegA<T, 1, 8, 3, 8>>(g, st);
+      if (t.mt == 1) return launch_plain<T, 1, 8, RegA<T, 1, 8, 4, 8>>(g, st);
+      if (t.stages == 2) return launch_plain<T, 2, 8, RegA<T, 2, 8, 2, 8>>(g, st);
+      if (t.stages == 4) return launch_plain<T, 2, 8, RegA<T, 2, 8, 4, 8>>(g, st);
+      return launch_plain<T, 2, 8, RegA<T, 2, 8, 3, 8>>(g, st);
+    }
+    if (t.mt == 1) return launch_plain<T, 1, 8, RegA<T, 1, 8, 4>>(g, st);
+    if (t.mt == 4 && t.stages == 2) return launch_plain<T, 4, 8, RegA<T, 4, 8, 2>>(g, st);
+    if (t.mt == 4) return launch_plain<T, 4, 8, RegA<T, 4, 8, 3>>(g, st);
+    if (t.stages == 3) return launch_plain<T, 2, 8, RegA<T, 2, 8, 3>>(g, st);
   }
+  if constexpr (NT == 16)
+    return launch_plain<T, 2, 16, RegA<T, 2, 16, 3>>(g, st);
+  else
+    return launch_plain<T, 2, NT, RegA<T, 2, NT, 4>>(g, st);
 }
 
 template <typename T>
 hipError_t dispatch(const GemmArgs& g, hipStream_t st) {
+  const Tiling t = choose(g.dtype, g.mode, g.N);
   if (g.mode == SAGA_GEMM_GRU) {
-    const int64_t F = g.N / 3;
     dim3 grid((unsigned)((g.M + 63) / 64));
-    switch (F) {
-      case 16: hipLaunchKernelGGL((k_gemm_gru<T, 1>), grid, dim3(kThreads), 0, st, g); break;
-      case 32: hipLaunchKernelGGL((k_gemm_gru<T, 2>), grid, dim3(kThreads), 0, st, g); break;
-      case 48: hipLaunchKernelGGL((k_gemm_gru<T, 3>), grid, dim3(kThreads), 0, st, g); break;
-      case 64: hipLaunchKernelGGL((k_gemm_gru<T, 4>), grid, dim3(kThreads), 0, st, g); break;
+    switch (t.nt) {
+      case 3: hipLaunchKernelGGL((k_gemm_gru<T, 1, 4>), grid, dim3(kThreads), 0, st, g); break;
+      case 6: hipLaunchKernelGGL((k_gemm_gru<T, 2, 4>), grid, dim3(kThreads), 0, st, g); break;
+      case 9: hipLaunchKernelGGL((k_gemm_gru<T, 3, 4>), grid, dim3(kThreads), 0, st, g); break;
+      case 12: hipLaunchKernelGGL((k_gemm_gru<T, 4, 4>), grid, dim3(kThreads), 0, st, g); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
   }
-  const int64_t nt = (g.N + 15) / 16;
-  if (nt <= 1) return launch_nt<T, 1>(g, st);
-  if (nt <= 2) return launch_nt<T, 2>(g, st);
-  if (nt <= 3) return launch_nt<T, 3>(g, st);
-  if (nt <= 4) return launch_nt<T, 4>(g, st);
-  if (nt <= 5) return launch_nt<T, 5>(g, st);
-  if (nt <= 8) return launch_nt<T, 8>(g, st);
-  return launch_plain<T, 2, 16>(g, st);
+  switch (t.nt) {
+    case 1: return launch_nt<T, 1>(g, t, st);
+    case 2: return launch_nt<T, 2>(g, t, st);
+    case 3: return launch_nt<T, 3>(g, t, st);
+    case 4: return launch_nt<T, 4>(g, t, st);
+    case 5: return launch_nt<T, 5>(g, t, st);
+    case 8: return launch_nt<T, 8>(g, t, st);
+    default: return launch_nt<T, 16>(g, t, st);
+  }
+}
+
+template <typename T>
+hipError_t pack(const void* w, int64_t ldw, int64_t K, int64_t N, void* wt, int64_t kp,
+                int64_t np, hipStream_t st) {
+  const int64_t total = np * kp;
+  const unsigned blocks = (unsigned)std::min<int64_t>((total + kThreads - 1) / kThreads, 2048);
+  hipLaunchKernelGGL((k_pack_wt<T>), dim3(blocks), dim3(kThreads), 0, st, static_cast<const T*>(w),
+                     ldw, K, N, static_cast<T*>(wt), kp, np);
+  return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_gemm(const GemmArgs& g, hipStream_t st) {
-  if (g.M == 0) return hipSuccess;
-  return g.dtype == SAGA_BF16 ? dispatch<uint16_t>(g, st) : dispatch<float>(g, st);
+size_t gemm_workspace_bytes(int dtype, int mode, int64_t N, int64_t K, int64_t K2) {
+  return packed_layout(dtype, mode, N, K, K2).bytes;
+}
+
+hipError_t launch_gemm(const GemmArgs& g0, hipStream_t st) {
+  if (g0.M == 0) return hipSuccess;
+  const Packed pk = packed_layout(g0.dtype, g0.mode, g0.N, g0.K, g0.K2);
+  if (!g0.ws || g0.ws_bytes < pk.bytes) return hipErrorInvalidValue;
+  GemmArgs g = g0;
+  char* ws = static_cast<char*>(g.ws);
+  g.wt = ws;
+  g.kp = pk.kp;
+  g.wt2 = pk.kp2 ? ws + pk.off2 : nullptr;
+  g.kp2 = pk.kp2;
+  const bool bf = g.dtype == SAGA_BF16;
+  hipError_t e = bf ? pack<uint16_t>(g.w, g.ldw, g.K, g.N, ws, pk.kp, pk.np, st)
+                    : pack<float>(g.w, g.ldw, g.K, g.N, ws, pk.kp, pk.np, st);
+  if (e == hipSuccess && pk.kp2)
+    e = bf ? pack<uint16_t>(g.w2, g.ldw2, g.K2, g.N, ws + pk.off2, pk.kp2, pk.np, st)
+           : pack<float>(g.w2, g.ldw2, g.K2, g.N, ws + pk.off2, pk.kp2, pk.np, st);
+  if (e != hipSuccess) return e;
+  return bf ? dispatch<uint16_t>(g, st) : dispatch<float>(g, st);
 }
 
 }  // namespace saga

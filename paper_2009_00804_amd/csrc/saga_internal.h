@@ -92,7 +92,14 @@ struct GemmArgs {
   const float* bias2;
   const int32_t* row_scale_deg;
   void* out; int64_t ldo;
+  // scratch for the packed transposed weights (gemm_workspace_bytes)
+  void* ws; size_t ws_bytes;
+  // set by launch_gemm: packed weights in the workspace, ld kp / kp2
+  const void* wt; int64_t kp;
+  const void* wt2; int64_t kp2;
 };
+// bytes of workspace launch_gemm needs for these shapes (packed weights)
+size_t gemm_workspace_bytes(int dtype, int mode, int64_t N, int64_t K, int64_t K2);
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t st);
 
 // ---- layer helpers (gather.hip) ----

@@ -32,7 +32,8 @@ ACT = {"none": 0, "relu": 1, "elu": 2, "sigmoid": 3, "tanh": 4}
 
 EXPORTS = [
     "saga_plan_workspace_size", "saga_plan_build", "saga_plan_check",
-    "saga_gather_workspace_size", "saga_scatter_apply_edge_gather", "saga_apply_vertex",
+    "saga_gather_workspace_size", "saga_scatter_apply_edge_gather",
+    "saga_apply_vertex_workspace_size", "saga_apply_vertex",
     "saga_layer_workspace_size", "saga_layer", "saga_status_str", "saga_last_error",
     "saga_version",
 ]
@@ -118,8 +119,10 @@ def lib():
         "saga_gather_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64, P(C.c_size_t)]),
         "saga_scatter_apply_edge_gather": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs), saga_mat,
                                                C.c_void_p, C.c_size_t, C.c_void_p]),
+        "saga_apply_vertex_workspace_size": (S, [P(saga_gemm_op), C.c_int64, C.c_int64, C.c_int64,
+                                                 P(C.c_size_t)]),
         "saga_apply_vertex": (S, [P(saga_gemm_op), saga_cmat, saga_cmat, saga_cmat, saga_cmat, C.c_void_p,
-                                  C.c_void_p, saga_mat, C.c_void_p]),
+                                  C.c_void_p, saga_mat, C.c_void_p, C.c_size_t, C.c_void_p]),
         "saga_layer_workspace_size": (S, [P(saga_plan), P(saga_layer_desc), P(C.c_size_t)]),
         "saga_layer": (S, [P(saga_plan), P(saga_layer_desc), saga_cmat, saga_cmat, saga_mat, C.c_void_p,
                            C.c_size_t, C.c_void_p]),
@@ -187,8 +190,16 @@ def saga_scatter_apply_edge_gather(plan, op, inputs, out, workspace, ws_bytes, s
                   "saga_scatter_apply_edge_gather")
 
 
-def saga_apply_vertex(op, a, w, a2, w2, bias, bias2, out, stream):
-    return _check(lib().saga_apply_vertex(C.byref(op), a, w, a2, w2, bias, bias2, out, stream),
+def saga_apply_vertex_workspace_size(op, k, k2, n):
+    out = C.c_size_t(0)
+    _check(lib().saga_apply_vertex_workspace_size(C.byref(op), k, k2, n, C.byref(out)),
+           "saga_apply_vertex_workspace_size")
+    return out.value
+
+
+def saga_apply_vertex(op, a, w, a2, w2, bias, bias2, out, workspace, ws_bytes, stream):
+    return _check(lib().saga_apply_vertex(C.byref(op), a, w, a2, w2, bias, bias2, out, workspace,
+                                          ws_bytes, stream),
                   "saga_apply_vertex")
 
 

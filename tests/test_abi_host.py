@@ -129,16 +129,16 @@ def test_gemm_rejects_bad_arguments(S):
     none = S.saga_cmat(None, 0, 0, 0)
     out = S.saga_mat(0x30000, 100, 16, 16)
     f = lambda *args: L.saga_apply_vertex(C.byref(args[0]), *args[1:])  # noqa: E731
-    assert f(op, a, S.saga_cmat(0x20000, 31, 16, 16), none, none, None, None, out, None) == S.SAGA_EINVAL
-    assert f(op, a, w, none, none, None, None, S.saga_mat(0x30000, 99, 16, 16), None) == S.SAGA_EINVAL
-    assert f(op, a, w, none, none, None, None, S.saga_mat(0x10000 + 128, 100, 16, 16), None) == S.SAGA_EINVAL
+    assert f(op, a, S.saga_cmat(0x20000, 31, 16, 16), none, none, None, None, out, 0x900000, 1 << 20, None) == S.SAGA_EINVAL
+    assert f(op, a, w, none, none, None, None, S.saga_mat(0x30000, 99, 16, 16), 0x900000, 1 << 20, None) == S.SAGA_EINVAL
+    assert f(op, a, w, none, none, None, None, S.saga_mat(0x10000 + 128, 100, 16, 16), 0x900000, 1 << 20, None) == S.SAGA_EINVAL
     gru = S.saga_gemm_op(S.SAGA_F32, S.SAGA_GEMM_GRU, 0, None)
     w3 = S.saga_cmat(0x20000, 32, 60, 60)
     a2 = S.saga_cmat(0x60000, 100, 20, 20)
     w23 = S.saga_cmat(0x70000, 20, 60, 60)
-    assert f(gru, a, w3, a2, w23, None, None, S.saga_mat(0x30000, 100, 20, 20), None) == S.SAGA_EUNSUPPORTED
+    assert f(gru, a, w3, a2, w23, None, None, S.saga_mat(0x30000, 100, 20, 20), 0x900000, 1 << 20, None) == S.SAGA_EUNSUPPORTED
     bad_mode = S.saga_gemm_op(S.SAGA_F32, 7, 0, None)
-    assert f(bad_mode, a, w, none, none, None, None, out, None) == S.SAGA_EINVAL
+    assert f(bad_mode, a, w, none, none, None, None, out, 0x900000, 1 << 20, None) == S.SAGA_EINVAL
 
 
 def test_layer_rejects_bad_descriptors(S):

@@ -222,9 +222,13 @@ def run_gemm(A, W, dtype, bias=None, act="none", deg=None, A2=None, W2=None, bia
     M = A.shape[0]
     N = out_cols or W.shape[1]
     out = dev_padded(np.zeros((M, N)), tdt, fill=3.0)
+    nws = S.saga_apply_vertex_workspace_size(op, A.shape[1], 0 if A2 is None else A2.shape[1],
+                                             W.shape[1])
+    ws = S.workspace(nws, dev)
     S.saga_apply_vertex(op, S.cmat(At), S.cmat(Wt), S.cmat(A2t), S.cmat(W2t),
                         None if bt is None else bt.data_ptr(),
-                        None if b2t is None else b2t.data_ptr(), S.mat(out), S.stream_handle())
+                        None if b2t is None else b2t.data_ptr(), S.mat(out),
+                        C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
     torch.cuda.synchronize()
     return out
 
