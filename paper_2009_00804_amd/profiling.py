@@ -28,12 +28,14 @@ import re
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 
-# stage -> (kernel-name pattern per dtype, source file, dispatches per call)
+# stage -> (kernel-name prefix per dtype, source file)
 STAGES = {
-    "gather1": ("k_gather_simple<{t}, 8, 1, 8, 4, false, false, true", "gather.hip"),
-    "gather2": ("k_gather_simple<{t}, {lpr2}, 1, 8, 4, false, false, false", "gather.hip"),
-    "gemm1": ("k_gemm<{t}, 2, 8>", "gemm.hip"),
-    "gemm2": ("k_gemm<{t}, 2, 3>", "gemm.hip"),
+    "gather1": ({"f32": "k_gather_simple<float, 8, 1, 8, 4, false, false, true",
+                 "bf16": "k_gather_simple<unsigned short, 8, 1, 8, 4, false, false, true"}, "gather.hip"),
+    "gather2": ({"f32": "k_gather_simple<float, 16, 1, 8, 4, false, false, false",
+                 "bf16": "k_gather_simple<unsigned short, 8, 1, 8, 4, false, false, false"}, "gather.hip"),
+    "gemm1": ({"f32": "k_gemm<float, 2, 8,", "bf16": "k_gemm<unsigned short, 1, 8,"}, "gemm.hip"),
+    "gemm2": ({"f32": "k_gemm<float, 2, 3,", "bf16": "k_gemm<unsigned short, 2, 3,"}, "gemm.hip"),
 }
 
 
@@ -99,8 +101,6 @@ def main():
     if a.slices <= 0:
         a.slices = 4 if a.dtype == "f32" else 2
     os.makedirs(a.out, exist_ok=True)
-    t = "float" if a.dtype == "f32" else "unsigned short"
-    lpr2 = "16" if a.dtype == "f32" else "8"
 
     st = kernel_stats(a.trace)
     tot = sum(v[2] for v in st.values())
@@ -133,8 +133,8 @@ def main():
 
     rec_path = os.path.join(a.out, "traffic.json")
     rec = json.load(open(rec_path)) if os.path.exists(rec_path) else {}
-    for stage, (pat, src) in STAGES.items():
-        pat = pat.format(t=t, lpr2=lpr2)
+    for stage, (pats, src) in STAGES.items():
+        pat = pats[a.dtype]
         keys = [k for k in set(fe) | set(wr) if k.startswith(pat)]
         if len(keys) != 1:
             continue
