@@ -90,7 +90,8 @@ class Step:
         al = 16 // es
         ld = lambda c: (c + al - 1) // al * al  # noqa: E731
         self.Z1 = torch.empty((self.V, S.gather_ld(hid, es)), dtype=tdt, device=dev)[:, :hid]
-        self.H1 = torch.empty((self.V, ld(hid)), dtype=tdt, device=dev)[:, :hid]
+        self.H1_base = torch.empty((self.V, ld(hid)), dtype=tdt, device=dev)
+        self.H1 = self.H1_base[:, :hid]
         self.Z2 = torch.empty((self.V, S.gather_ld(f_out, es)), dtype=tdt, device=dev)[:, :f_out]
         self.Y = torch.empty((self.V, ld(f_out)), dtype=tdt, device=dev)[:, :f_out]
         self.graph = S.Graph(self.rp, self.col)     # allocates + builds + checks once
@@ -120,6 +121,28 @@ class Step:
         self.sh = S.stream_handle(self.stream)
         self.names = ["plan", "gemm1", "gather1", "gemm2", "gather2"]
         self.ev = None
+        self.uws = None
+
+    def setup_unfused(self):
+        """Workspace (the E x F edge tensor) and output of the unfused layer-1
+        aggregation; allocated only when the fused/unfused comparison runs."""
+        S, torch = self.S, self.torch
+        hid = self.dims[1]
+        n = S.saga_unfused_workspace_size(self.graph.plan, self.op1, hid)
+        self.uws = S.workspace(n, self.H1.device)
+        self.Hu = torch.empty_like(self.H1_base)[:, :hid]
+
+    def run_unfused1(self):
+        """Layer-1 Scatter+ApplyEdge+Gather, unfused (Fig. 7a): index-select
+        into the edge tensor, then the segment reduction, on the same Z1."""
+        S = self.S
+        S.saga_scatter_gather_unfused(self.graph.plan, self.op1, self.in1, S.mat(self.Hu),
+                                      C.c_void_p(self.uws.data_ptr()), self.uws.numel(), self.sh)
+        return self.Hu
+
+    def free_unfused(self):
+        self.uws = None
+        self.Hu = None
 
     def run(self, events=None):
         S = self.S
@@ -205,6 +228,25 @@ def time_step(step, steps, warmup):
     return wall, per, tot
 
 
+def time_unfused(step, reps=3):
+    """Mean time of the unfused layer-1 aggregation next to the fused one."""
+    torch = step.torch
+    step.setup_unfused()
+    step.run_unfused1()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(step.stream)
+    for _ in range(reps):
+        step.run_unfused1()
+    e1.record(step.stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    step.free_unfused()
+    torch.cuda.empty_cache()
+    return ms
+
+
 def cpu_baseline(g, budget_s=12.0):
     """The oracle's layer-1 GCN (aggregate-first, float64) on a bounded random
     sample of destination rows of the same workload, one thread."""
@@ -251,6 +293,8 @@ def main():
     ap.add_argument("--scale", type=int, default=21)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--no-unfused", action="store_true",
+                    help="skip the fused-vs-unfused layer-1 aggregation comparison")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before timing, run one device-to-device copy of this many MiB "
                          "(a known-size kernel for calibrating memory counters)")
@@ -293,6 +337,10 @@ def main():
                            ev_ms=statistics.median(tot))
         log(f"{dt}: {ms:.3f} ms/step (events {statistics.median(tot):.3f}); "
             + ", ".join(f"{n} {med[n]:.3f}" for n in step.names))
+        if not args.no_unfused:
+            um = time_unfused(step)
+            results[dt]["unfused_ms"] = um
+            log(f"{dt}: layer-1 aggregation unfused {um:.3f} ms vs fused {mean['gather1']:.3f} ms")
         if dt != args.dtype:
             del step
             results[dt]["step"] = None
@@ -351,11 +399,20 @@ def main():
                  "split_rows": r["counts"].n_split, "max_in_degree": r["counts"].max_in_degree},
         "roofline": roof,
     }
+    if "unfused_ms" in r:
+        out["fusion"] = {
+            "stage": "layer-1 Scatter+ApplyEdge+Gather (Fig. 7a unfused vs Fig. 7b fused)",
+            "fused_ms": r["mean"]["gather1"], "unfused_ms": r["unfused_ms"],
+            "speedup": r["unfused_ms"] / r["mean"]["gather1"]}
     for dt in dtypes[1:]:
         rr = results[dt]
         out.setdefault("variants", {})[dt] = {
             "value": 2 * E / (rr["ms"] * 1e-3), "ms_per_step": rr["ms"],
             "stage_ms": {n: round(rr["mean"][n], 4) for n in rr["mean"]}}
+        if "unfused_ms" in rr:
+            out["variants"][dt]["fusion"] = {"fused_ms": rr["mean"]["gather1"],
+                                             "unfused_ms": rr["unfused_ms"],
+                                             "speedup": rr["unfused_ms"] / rr["mean"]["gather1"]}
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(g, args.cpu_budget)

@@ -16,6 +16,9 @@
  *                                   the in-CSR (the fused Gather is the
  *                                   sparse adjacency x embedding product,
  *                                   Sec. 3.2 "Gather", Fig. 7b)
+ *   saga_scatter_gather_unfused     the same, unfused: materialised edge
+ *                                   tensor, then a segment reduction (the
+ *                                   baseline of Fig. 7a)
  *   saga_apply_vertex               dense per-vertex transform on the matrix
  *                                   cores, with fused epilogues (Sec. 3.2
  *                                   "ApplyVertex", Table III)
@@ -248,6 +251,30 @@ saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edg
                                            const saga_edge_inputs* in, saga_mat out,
                                            void* workspace, size_t workspace_bytes,
                                            void* stream);
+
+/* ----------------------------------------------------------------------
+ * Unfused baseline (Sec. 3.2 "Gather", Fig. 7a): the same operation as
+ * saga_scatter_apply_edge_gather, computed the way a framework without a
+ * fused kernel does it.  Scatter + ApplyEdge first materialise the edge
+ * tensor msg[e] = w(u) * src[u] for every in-edge e = (u -> v) in CSR order
+ * (an index-select; w(u) = d_out(u)^-1/2 for SAGA_MSG_SRC_NORM, else 1),
+ * written into the workspace; Gather then reduces each destination's
+ * contiguous run of msg rows.  Supported: msg COPY or SRC_NORM, reduce SUM,
+ * MEAN or MAX, with the same dst_norm / bias / act epilogue; anything else
+ * is SAGA_EUNSUPPORTED.  The result matches the fused call up to the order
+ * of floating-point additions (MAX and float32 COPY are identical); for
+ * bfloat16 with SRC_NORM the message is rounded to bfloat16 before the sum.
+ * Workspace: saga_unfused_workspace_size() bytes, 256-byte aligned, not
+ * overlapping src or out -- num_edges x (feat padded to whole 16-byte or
+ * 64-byte units) elements of the op's dtype plus the split-row partials.
+ * ---------------------------------------------------------------------- */
+saga_status saga_unfused_workspace_size(const saga_plan* plan, const saga_edge_op* op,
+                                        int64_t feat, size_t* bytes);
+
+saga_status saga_scatter_gather_unfused(const saga_plan* plan, const saga_edge_op* op,
+                                        const saga_edge_inputs* in, saga_mat out,
+                                        void* workspace, size_t workspace_bytes,
+                                        void* stream);
 
 /* ======================================================================
  * ApplyVertex: dense transform on the matrix cores

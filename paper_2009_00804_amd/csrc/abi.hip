@@ -353,6 +353,68 @@ int64_t ld_for(int64_t cols, saga_dtype t) {
   return bytes / es;
 }
 
+// ---------------------------------------------------------------------------
+// unfused baseline: index-select into an E x ldm edge tensor, then reduce
+// ---------------------------------------------------------------------------
+size_t unfused_msg_bytes(const saga_plan& p, const saga_edge_op& op, int64_t feat, int64_t* ldm) {
+  const saga_dtype t = op.dtype == SAGA_BF16 ? SAGA_BF16 : SAGA_F32;
+  *ldm = ld_for(feat, t);
+  return align256((size_t)p.num_edges * (size_t)*ldm * esize(t));
+}
+
+saga_status unfused_ws_bytes(const saga_plan& p, const saga_edge_op& op, int64_t feat,
+                             size_t* bytes) {
+  int64_t ldm;
+  size_t pb;
+  gather_ws_bytes(p, op, feat, &pb);
+  *bytes = unfused_msg_bytes(p, op, feat, &ldm) + pb;
+  return SAGA_OK;
+}
+
+saga_status run_gather_unfused(const saga_plan& p, const saga_edge_op& op,
+                               const saga_edge_inputs& in, const saga_mat& out, void* ws,
+                               size_t ws_bytes, hipStream_t st) {
+  if (op.msg != SAGA_MSG_COPY && op.msg != SAGA_MSG_SRC_NORM)
+    return fail(SAGA_EUNSUPPORTED, "unfused path: msg must be COPY or SRC_NORM");
+  if (op.reduce != SAGA_RED_SUM && op.reduce != SAGA_RED_MEAN && op.reduce != SAGA_RED_MAX)
+    return fail(SAGA_EUNSUPPORTED, "unfused path: reduce must be SUM, MEAN or MAX");
+  saga_status s = validate_edge_op(p, op, in, out);
+  if (s) return s;
+  int64_t ldm;
+  const size_t mb = unfused_msg_bytes(p, op, in.src.cols, &ldm);
+  size_t need;
+  unfused_ws_bytes(p, op, in.src.cols, &need);
+  if (!ws || ws_bytes < need)
+    return fail(SAGA_EWORKSPACE, "unfused workspace: need %zu bytes, got %zu", need, ws_bytes);
+  if ((uintptr_t)ws % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
+  const size_t es = esize(op.dtype);
+  if (range_overlap(ws, need, out.ptr, mat_bytes(out.rows, out.cols, out.ld, es)) ||
+      range_overlap(ws, need, in.src.ptr, mat_bytes(in.src.rows, in.src.cols, in.src.ld, es)))
+    return fail(SAGA_EINVAL, "workspace overlaps an argument");
+  if (p.num_dst == 0) return ok();
+  saga::GatherArgs a = gather_args_from_plan(p);
+  a.msg = op.msg;
+  a.reduce = op.reduce;
+  a.dtype = op.dtype;
+  a.heads = 1;
+  a.dst_norm = op.dst_norm;
+  a.act = op.act;
+  a.feat = (int)in.src.cols;
+  a.out_cols = (int)out.cols;
+  a.src = in.src.ptr;
+  a.ld_src = in.src.ld;
+  a.bias = in.bias;
+  a.out = out.ptr;
+  a.ld_out = out.ld;
+  char* w = static_cast<char*>(ws);
+  a.partial = reinterpret_cast<float*>(w + mb);
+  a.pstride = (int64_t)saga::gather_partial_stride(op, in.src.cols);
+  a.pcols = saga::gather_partial_cols(in.src.cols);
+  hipError_t e = saga::launch_unfused(a, p.num_edges, w, ldm, st);
+  if (e != hipSuccess) return dev_fail(e, "unfused gather launch");
+  return ok();
+}
+
 saga_status layer_check_desc(const saga_plan& p, const saga_layer_desc& d) {
   if (p.num_dst != p.num_src) return fail(SAGA_EINVAL, "layers need num_src == num_dst");
   if (d.in_feat <= 0 || d.out_feat <= 0) return fail(SAGA_EINVAL, "layer feature sizes must be > 0");
@@ -756,6 +818,33 @@ saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edg
     if (!op || !in) return fail(SAGA_EINVAL, "null argument");
     return run_gather(*plan, *op, *in, out, workspace, workspace_bytes,
                       static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_unfused_workspace_size(const saga_plan* plan, const saga_edge_op* op,
+                                        int64_t feat, size_t* bytes) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!op || !bytes) return fail(SAGA_EINVAL, "null argument");
+    if (feat <= 0) return fail(SAGA_EINVAL, "feat must be > 0");
+    return unfused_ws_bytes(*plan, *op, feat, bytes) ? SAGA_EINTERNAL : ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_scatter_gather_unfused(const saga_plan* plan, const saga_edge_op* op,
+                                        const saga_edge_inputs* in, saga_mat out,
+                                        void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!op || !in) return fail(SAGA_EINVAL, "null argument");
+    return run_gather_unfused(*plan, *op, *in, out, workspace, workspace_bytes,
+                              static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(SAGA_EINTERNAL, "exception");
   }

@@ -18,6 +18,7 @@
 //     output row; segments of split rows (d_in > seg_len) write float32
 //     partials, merged in segment order by k_combine (deterministic: no
 //     floating-point atomics anywhere).
+#include <algorithm>
 #include <cstdlib>
 
 #include "saga_device.h"
@@ -62,7 +63,10 @@ __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int 
 // ------------------------------------------------------------------------
 // SLICED only distinguishes the sliced instance (rows wider than one slice)
 // in profiles.
-template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, bool SRCNORM, bool SLICED>
+// IDENT: the source row of edge e is row e itself (the segment reduction of
+// an edge tensor already laid out in CSR order; the unfused path).
+template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, bool SRCNORM, bool SLICED,
+          bool IDENT = false>
 __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int nslices, int slice0) {
   constexpr int EPV = Vec16<T>::N;
   constexpr int NG = kThreads / LPR;
@@ -99,7 +103,10 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         const int idx = e + j * LPR + gl;
-        c[j] = idx < end ? __builtin_nontemporal_load(col + idx) : 0;
+        if constexpr (IDENT)
+          c[j] = idx < end ? idx : 0;
+        else
+          c[j] = idx < end ? __builtin_nontemporal_load(col + idx) : 0;
       }
       const int n = (end - e) < LPR * CPL ? (end - e) : LPR * CPL;
 #pragma unroll
@@ -169,6 +176,50 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
         }
       }
     }
+  }
+}
+
+// ------------------------------------------------------------------------
+// Unfused Scatter + ApplyEdge (the baseline of Fig. 7a): materialise the
+// edge tensor msg[e] = w(u) * src[u] for every edge e = (u -> v) in CSR
+// order, w(u) = d_out(u)^-1/2 for the GCN source norm, else 1.  One thread
+// per 16-byte vector; the lanes of a row are consecutive, so both the row
+// read and the message write are contiguous.
+// ------------------------------------------------------------------------
+template <typename T, bool SRCNORM>
+__global__ __launch_bounds__(kThreads) void k_index_select(const int32_t* __restrict__ col,
+                                                           int64_t E, int nv,
+                                                           const uint4* __restrict__ src,
+                                                           int64_t ld16,
+                                                           const int32_t* __restrict__ d_out,
+                                                           uint4* __restrict__ msg, int64_t ldm16,
+                                                           const int32_t* __restrict__ counts) {
+  if (counts[kErrFlags]) return;
+  const int64_t total = E * nv;
+  for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kThreads) {
+    const int64_t e = i / nv;
+    const int v = (int)(i - e * nv);
+    const int32_t u = col[e];
+    uint4 r = src[(int64_t)u * ld16 + v];
+    if constexpr (SRCNORM) {
+      float x[Vec16<T>::N];
+      Vec16<T>::widen(r, x);
+      const float w = rsqrt_deg(d_out[u]);
+#pragma unroll
+      for (int k = 0; k < Vec16<T>::N; ++k) x[k] *= w;
+      if constexpr (sizeof(T) == 4) {
+        r = make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
+                       __float_as_uint(x[3]));
+      } else {
+        uint32_t w4[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          w4[k] = (uint32_t)f32_to_bf16(x[2 * k]) | ((uint32_t)f32_to_bf16(x[2 * k + 1]) << 16);
+        r = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+      }
+    }
+    msg[e * ldm16 + v] = r;
   }
 }
 
@@ -515,8 +566,14 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
 #define SAGA_LAUNCH(MX, SN, SL)                                                              \
   hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, SN, SL>), grid, dim3(kThreads), \
                      0, st, a, conc, s0)
+#define SAGA_LAUNCH_IDENT(MX)                                                                  \
+  hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, false, false, true>), grid,     \
+                     dim3(kThreads), 0, st, a, conc, s0)
     const bool sl = nslices > 1;
-    if (a.reduce == kMax) {
+    if (a.identity) {
+      if (a.reduce == kMax) SAGA_LAUNCH_IDENT(true);
+      else SAGA_LAUNCH_IDENT(false);
+    } else if (a.reduce == kMax) {
       if (srcnorm) SAGA_LAUNCH(true, true, false);
       else SAGA_LAUNCH(true, false, false);
     } else if (srcnorm) {
@@ -527,6 +584,7 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
       SAGA_LAUNCH(false, false, false);
     }
 #undef SAGA_LAUNCH
+#undef SAGA_LAUNCH_IDENT
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -606,6 +664,71 @@ hipError_t launch_gather(const GatherArgs& a, hipStream_t st) {
   } else {
     err = launch_simple<float>(a, nv, grid, st);
   }
+  if (err != hipSuccess) return err;
+  if (a.max_split > 0) {
+    const unsigned cg = (unsigned)(a.max_split < 4096 ? a.max_split : 4096);
+    if (a.dtype == SAGA_BF16)
+      hipLaunchKernelGGL(k_combine<uint16_t>, dim3(cg), dim3(kThreads), 0, st, a);
+    else
+      hipLaunchKernelGGL(k_combine<float>, dim3(cg), dim3(kThreads), 0, st, a);
+    err = hipGetLastError();
+  }
+  return err;
+}
+
+namespace {
+
+// segment reduction over a contiguous edge tensor: whole rows per lane group
+// (the tensor is streamed once, so no slicing for cache reuse)
+template <typename T>
+hipError_t launch_ident(const GatherArgs& a, int nv, unsigned blocks, hipStream_t st) {
+  if (nv > 64) return launch_simple_lpr<T, 64, 2>(a, blocks, 1, st);
+  switch (next_pow2(nv)) {
+    case 1: return launch_simple_lpr<T, 1, 1>(a, blocks, 1, st);
+    case 2: return launch_simple_lpr<T, 2, 1>(a, blocks, 1, st);
+    case 4: return launch_simple_lpr<T, 4, 1>(a, blocks, 1, st);
+    case 8: return launch_simple_lpr<T, 8, 1>(a, blocks, 1, st);
+    case 16: return launch_simple_lpr<T, 16, 1>(a, blocks, 1, st);
+    case 32: return launch_simple_lpr<T, 32, 1>(a, blocks, 1, st);
+    default: return launch_simple_lpr<T, 64, 1>(a, blocks, 1, st);
+  }
+}
+
+template <typename T>
+hipError_t launch_select(const GatherArgs& a, int nv, int64_t E, void* msg, int64_t ldm,
+                         hipStream_t st) {
+  const int64_t total = E * nv;
+  const unsigned grid = (unsigned)std::min<int64_t>((total + kThreads - 1) / kThreads, 1 << 16);
+  const int64_t ld16 = a.ld_src * (int64_t)sizeof(T) / 16, ldm16 = ldm * (int64_t)sizeof(T) / 16;
+  const uint4* src = static_cast<const uint4*>(a.src);
+  if (a.msg == SAGA_MSG_SRC_NORM)
+    hipLaunchKernelGGL((k_index_select<T, true>), dim3(grid), dim3(kThreads), 0, st, a.col_idx, E,
+                       nv, src, ld16, a.d_out, static_cast<uint4*>(msg), ldm16, a.counts);
+  else
+    hipLaunchKernelGGL((k_index_select<T, false>), dim3(grid), dim3(kThreads), 0, st, a.col_idx,
+                       E, nv, src, ld16, a.d_out, static_cast<uint4*>(msg), ldm16, a.counts);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_unfused(const GatherArgs& a0, int64_t E, void* msg, int64_t ldm,
+                          hipStream_t st) {
+  const int esz = a0.dtype == SAGA_BF16 ? 2 : 4;
+  const int nv = (int)((a0.feat * (int64_t)esz + 15) / 16);
+  hipError_t err = hipSuccess;
+  if (E > 0)
+    err = a0.dtype == SAGA_BF16 ? launch_select<uint16_t>(a0, nv, E, msg, ldm, st)
+                                : launch_select<float>(a0, nv, E, msg, ldm, st);
+  if (err != hipSuccess) return err;
+  GatherArgs a = a0;
+  a.msg = SAGA_MSG_COPY;
+  a.identity = 1;
+  a.src = msg;
+  a.ld_src = ldm;
+  const unsigned grid = (unsigned)(a.max_blocks > 0 ? a.max_blocks : 1);
+  err = a.dtype == SAGA_BF16 ? launch_ident<uint16_t>(a, nv, grid, st)
+                             : launch_ident<float>(a, nv, grid, st);
   if (err != hipSuccess) return err;
   if (a.max_split > 0) {
     const unsigned cg = (unsigned)(a.max_split < 4096 ? a.max_split : 4096);

@@ -74,11 +74,14 @@ struct GatherArgs {
   // split-row partials (float32), stride pstride floats per segment
   float* partial; int64_t pstride;
   int pcols;       // partial accumulator columns; softmax m/l follow at pcols
+  int identity;    // source row of edge e is row e (unfused segment reduction)
 };
 
 int gather_partial_cols(int64_t feat);
 size_t gather_partial_stride(const saga_edge_op& op, int64_t feat);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t st);
+// unfused baseline: materialise msg (E x ldm, CSR order), then reduce it
+hipError_t launch_unfused(const GatherArgs& a, int64_t E, void* msg, int64_t ldm, hipStream_t st);
 
 // ---- gemm.hip ----
 struct GemmArgs {

@@ -33,6 +33,7 @@ ACT = {"none": 0, "relu": 1, "elu": 2, "sigmoid": 3, "tanh": 4}
 EXPORTS = [
     "saga_plan_workspace_size", "saga_plan_build", "saga_plan_check",
     "saga_gather_workspace_size", "saga_scatter_apply_edge_gather",
+    "saga_unfused_workspace_size", "saga_scatter_gather_unfused",
     "saga_apply_vertex_workspace_size", "saga_apply_vertex",
     "saga_layer_workspace_size", "saga_layer", "saga_status_str", "saga_last_error",
     "saga_version",
@@ -119,6 +120,9 @@ def lib():
         "saga_gather_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64, P(C.c_size_t)]),
         "saga_scatter_apply_edge_gather": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs), saga_mat,
                                                C.c_void_p, C.c_size_t, C.c_void_p]),
+        "saga_unfused_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64, P(C.c_size_t)]),
+        "saga_scatter_gather_unfused": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs), saga_mat,
+                                            C.c_void_p, C.c_size_t, C.c_void_p]),
         "saga_apply_vertex_workspace_size": (S, [P(saga_gemm_op), C.c_int64, C.c_int64, C.c_int64,
                                                  P(C.c_size_t)]),
         "saga_apply_vertex": (S, [P(saga_gemm_op), saga_cmat, saga_cmat, saga_cmat, saga_cmat, C.c_void_p,
@@ -188,6 +192,19 @@ def saga_scatter_apply_edge_gather(plan, op, inputs, out, workspace, ws_bytes, s
     return _check(lib().saga_scatter_apply_edge_gather(C.byref(plan), C.byref(op), C.byref(inputs), out,
                                                        workspace, ws_bytes, stream),
                   "saga_scatter_apply_edge_gather")
+
+
+def saga_unfused_workspace_size(plan, op, feat):
+    out = C.c_size_t(0)
+    _check(lib().saga_unfused_workspace_size(C.byref(plan), C.byref(op), feat, C.byref(out)),
+           "saga_unfused_workspace_size")
+    return out.value
+
+
+def saga_scatter_gather_unfused(plan, op, inputs, out, workspace, ws_bytes, stream):
+    return _check(lib().saga_scatter_gather_unfused(C.byref(plan), C.byref(op), C.byref(inputs), out,
+                                                    workspace, ws_bytes, stream),
+                  "saga_scatter_gather_unfused")
 
 
 def saga_apply_vertex_workspace_size(op, k, k2, n):

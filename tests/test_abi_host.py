@@ -121,6 +121,35 @@ def test_gather_rejects_bad_arguments(S):
     assert b"F == 64" in L.saga_last_error()
 
 
+def test_unfused_rejects_bad_arguments(S):
+    """The unfused baseline: unsupported ops, workspace size, alignment and
+    overlap are all rejected on the host before any launch."""
+    p = _fake_plan(S)
+    op = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 0, 0.2, 0)
+    inp = S.saga_edge_inputs()
+    inp.src = S.saga_cmat(0x50000, 16, 8, 8)
+    out = S.saga_mat(0x40000, 16, 8, 8)
+    L = S.lib()
+
+    def call(o=op, ws=0x900000, nb=1 << 20):
+        return L.saga_scatter_gather_unfused(C.byref(p), C.byref(o), C.byref(inp), out, ws, nb, None)
+
+    need = S.saga_unfused_workspace_size(p, op, 8)
+    assert need >= 40 * 8 * 4      # the E x F edge tensor
+    big = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 0, 0.2, 0)
+    assert S.saga_unfused_workspace_size(p, big, 64) > need
+    assert call(nb=need - 1) == S.SAGA_EWORKSPACE
+    assert call(ws=None, nb=0) == S.SAGA_EWORKSPACE
+    assert call(ws=0x900000 + 16, nb=need) == S.SAGA_EINVAL        # not 256-byte aligned
+    assert call(ws=0x40000, nb=need) == S.SAGA_EINVAL              # overlaps the output
+    gat = S.saga_edge_op(S.SAGA_MSG_GAT, S.SAGA_RED_SOFTMAX, S.SAGA_F32, 2, 0, 0, 0.2, 0)
+    assert call(o=gat) == S.SAGA_EUNSUPPORTED
+    soft = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SOFTMAX, S.SAGA_F32, 1, 0, 0, 0.2, 0)
+    assert call(o=soft) == S.SAGA_EUNSUPPORTED
+    gated = S.saga_edge_op(S.SAGA_MSG_GATED, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 0, 0.2, 0)
+    assert call(o=gated) == S.SAGA_EUNSUPPORTED
+
+
 def test_gemm_rejects_bad_arguments(S):
     L = S.lib()
     op = S.saga_gemm_op(S.SAGA_F32, S.SAGA_GEMM_PLAIN, 0, None)

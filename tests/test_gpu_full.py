@@ -117,3 +117,52 @@ def test_full_gcn_sampled(big, dev_graph, dtype):
     print(f"{dtype}: layer-1 sampled err {e1:.3e}, two-layer sampled err {e2:.3e}", flush=True)
     assert e1 <= tol
     assert e2 <= (tol if dtype == "f32" else 2 * tol)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_full_bench_step_sampled(big, dtype):
+    """The op-level call sequence the benchmark times (plan, GEMM, fused
+    gather, GEMM, fused gather, with its buffers and leading dimensions) and
+    the unfused layer-1 aggregation it is compared with, on sampled rows."""
+    import bench
+
+    g = big
+    if dtype == "bf16":
+        C.add_bf16_variant(g)
+        Xo = T.bf16_to_f32(g["X_bf16"][:, :g["dims"][0]])
+        W1, W2, tol = g["W1_bf"], g["W2_bf"], BF16_TOL
+    else:
+        Xo = g["X"][:, :g["dims"][0]]
+        W1, W2, tol = g["W1"], g["W2"], FP32_TOL
+    step = bench.Step(g, dtype, torch.device("cuda:0"))
+    print(f"bench step ({dtype}) on the GPU", flush=True)
+    step.run()
+    torch.cuda.synchronize()
+    y = step.Y.clone()
+    step.run()
+    torch.cuda.synchronize()
+    assert torch.equal(y, step.Y)                  # deterministic bytes
+    assert torch.isfinite(y.float()).all()
+    rp, col = g["row_ptr"], g["col_idx"]
+    rows = _samples(g, seed=3)
+    rsel = torch.from_numpy(rows).cuda()
+    print(f"oracle layer 1 on {len(rows)} sampled rows", flush=True)
+    ref1 = O.gcn_layer(rp, col, Xo, W1, g["b1"], "relu", rows=rows)
+    e1 = rel_err(to_np(step.H1[rsel]), ref1)
+    print("unfused layer-1 aggregation on the GPU", flush=True)
+    step.setup_unfused()
+    hu = step.run_unfused1()
+    torch.cuda.synchronize()
+    eu = rel_err(to_np(hu[rsel]), ref1)
+    step.free_unfused()
+    rows2 = _small_two_hop(g, seed=4)
+    print(f"oracle two layers on {len(rows2)} sampled rows", flush=True)
+    ref2 = O.gcn_2layer(dict(g, X=Xo), X=Xo, W1=W1, W2=W2, rows=rows2)
+    e2 = rel_err(to_np(y[torch.from_numpy(rows2).cuda()]), ref2)
+    print(f"{dtype}: layer-1 err {e1:.3e}, unfused layer-1 err {eu:.3e}, two-layer err {e2:.3e}",
+          flush=True)
+    assert e1 <= tol
+    assert eu <= tol
+    assert e2 <= (tol if dtype == "f32" else 2 * tol)
+    del step
+    torch.cuda.empty_cache()
