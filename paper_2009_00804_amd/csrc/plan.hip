@@ -139,30 +139,37 @@ __global__ __launch_bounds__(kThreads) void k_degrees(const int32_t* __restrict_
       maxd = s_max[k] > maxd ? s_max[k] : maxd;
     }
     if (err) atomicOr(&counts[kErrFlags], err);
-    if (maxd) atomicMax(&counts[kMaxDegree], maxd);
+    // most workgroups already see a larger maximum: skip their atomic
+    if (maxd > __hip_atomic_load(&counts[kMaxDegree], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+      atomicMax(&counts[kMaxDegree], maxd);
   }
 }
 
 // ------------------------------------------------------------------------
 // Out-degrees without global atomics.  A power-law graph sends a large share
 // of all edges to a few hub sources, and same-address atomics serialize, so
-// instead: (1) histogram the CSR source ids by bucket (32768 ids per bucket)
-// per tile, (2) scan, (3) scatter the ids into bucket order, (4) count each
-// bucket in a 128 KB LDS histogram and store the counts.
+// instead: (1) histogram the CSR source ids by bucket (8192 ids per bucket)
+// per tile, (2) scan, (3) scatter the ids into bucket order as 16-bit
+// offsets within their bucket, (4) count each bucket in a 32 KB LDS
+// histogram and store the counts.
 // ------------------------------------------------------------------------
-constexpr int kBucketBits = 15;
+constexpr int kBucketBits = 13;
 constexpr int kBucketSize = 1 << kBucketBits;
-constexpr int kMaxBuckets = 4096;
+constexpr int kMaxBuckets = 2048;  // keeps the scatter's LDS within 64 KB
 constexpr int kEdgeItems = 32;
 constexpr int kEdgeTile = kThreads * kEdgeItems;  // 8192 edges per tile
 
+// per-tile bucket histogram; each wave counts into its own copy (fewer
+// same-address LDS atomics), the copies are summed at the end
 __global__ __launch_bounds__(kThreads) void k_outdeg_hist(const int32_t* __restrict__ col,
                                                           int64_t E, int32_t Vs, int nb,
                                                           int32_t* __restrict__ hist,
                                                           int64_t ntiles, int32_t* counts) {
-  __shared__ int32_t h[kMaxBuckets];
-  for (int b = threadIdx.x; b < nb; b += kThreads) h[b] = 0;
+  extern __shared__ int32_t h[];  // [kThreads / 64][nb]
+  constexpr int NW = kThreads / 64;
+  for (int b = threadIdx.x; b < NW * nb; b += kThreads) h[b] = 0;
   __syncthreads();
+  int32_t* hw = h + (threadIdx.x >> 6) * nb;
   int err = 0;
   const int64_t base = blockIdx.x * (int64_t)kEdgeTile;
   int32_t c[kEdgeItems];
@@ -178,27 +185,86 @@ __global__ __launch_bounds__(kThreads) void k_outdeg_hist(const int32_t* __restr
       if (c[j] < 0 || c[j] >= Vs)
         err |= 8;
       else
-        atomicAdd(&h[c[j] >> kBucketBits], 1);
+        atomicAdd(&hw[c[j] >> kBucketBits], 1);
     }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) err |= __shfl_xor(err, off, 64);
   if ((threadIdx.x & 63) == 0 && err) atomicOr(&counts[kErrFlags], err);
   __syncthreads();
-  for (int b = threadIdx.x; b < nb; b += kThreads) hist[(int64_t)b * ntiles + blockIdx.x] = h[b];
+  for (int b = threadIdx.x; b < nb; b += kThreads) {
+    int32_t t = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) t += h[w * nb + b];
+    hist[(int64_t)b * ntiles + blockIdx.x] = t;
+  }
 }
 
+// Scatter one tile into bucket order.  The tile is first ranked by bucket in
+// LDS, then written out so that consecutive threads store consecutive
+// positions of one bucket (coalesced 16-bit stores).  `offs` is the
+// exclusive scan of hist in bucket-major order, so the tile's count in
+// bucket b is offs[b * ntiles + tile + 1] - offs[b * ntiles + tile].
 __global__ __launch_bounds__(kThreads) void k_outdeg_scatter(const int32_t* __restrict__ col,
                                                              int64_t E, int nb,
                                                              const int32_t* __restrict__ offs,
                                                              int64_t ntiles,
-                                                             int32_t* __restrict__ out,
+                                                             uint16_t* __restrict__ out,
                                                              int32_t* counts) {
   if (counts[kErrFlags]) return;
-  __shared__ int32_t cur[kMaxBuckets];
-  for (int b = threadIdx.x; b < nb; b += kThreads) cur[b] = offs[(int64_t)b * ntiles + blockIdx.x];
+  extern __shared__ int32_t sm[];
+  __shared__ int s_bad;
+  int32_t* gbase = sm;            // [nb] global start of this tile's run in bucket b
+  int32_t* lbase = sm + nb;       // [nb] local start of bucket b within the tile
+  int32_t* cur = sm + 2 * nb;     // [nb] local cursor
+  uint16_t* sval = reinterpret_cast<uint16_t*>(sm + 3 * nb);  // [kEdgeTile]
+  uint16_t* sbkt = sval + kEdgeTile;                           // [kEdgeTile]
+  const int64_t tile = blockIdx.x;
+  const int64_t base = tile * (int64_t)kEdgeTile;
+  const int n = (int)(E - base < kEdgeTile ? E - base : kEdgeTile);
+  for (int b = threadIdx.x; b < nb; b += kThreads) {
+    const int64_t f = (int64_t)b * ntiles + tile;
+    const int32_t g0 = offs[f];
+    const int32_t g1 = f + 1 < (int64_t)nb * ntiles ? offs[f + 1] : (int32_t)E;
+    gbase[b] = g0;
+    cur[b] = g1 - g0;  // count, scanned below
+  }
   __syncthreads();
-  const int64_t base = blockIdx.x * (int64_t)kEdgeTile;
+  {  // exclusive scan of the tile's bucket counts: thread t owns buckets
+     // [t * per, (t + 1) * per), then a wave scan and a cross-wave pass
+    __shared__ int32_t wsum[kThreads / 64];
+    const int per = (nb + kThreads - 1) / kThreads;
+    const int b0 = threadIdx.x * per;
+    int32_t own = 0;
+    for (int k = 0; k < per; ++k)
+      if (b0 + k < nb) own += cur[b0 + k];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int32_t inc = own;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t y = __shfl_up(inc, off, 64);
+      if (lane >= off) inc += y;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int32_t run = inc - own;
+    for (int w = 0; w < wave; ++w) run += wsum[w];
+    int32_t total = 0;
+    for (int w = 0; w < kThreads / 64; ++w) total += wsum[w];
+    for (int k = 0; k < per; ++k)
+      if (b0 + k < nb) {
+        const int32_t c = cur[b0 + k];
+        lbase[b0 + k] = run;
+        cur[b0 + k] = run;
+        run += c;
+      }
+    if (threadIdx.x == 0) {
+      s_bad = total != n;
+      if (s_bad) atomicOr(&counts[kErrFlags], kErrInternal);
+    }
+  }
+  __syncthreads();
+  if (s_bad) return;
   int32_t c[kEdgeItems];
 #pragma unroll
   for (int j = 0; j < kEdgeItems; ++j) {
@@ -207,23 +273,32 @@ __global__ __launch_bounds__(kThreads) void k_outdeg_scatter(const int32_t* __re
   }
 #pragma unroll
   for (int j = 0; j < kEdgeItems; ++j) {
-    const int64_t i = base + j * kThreads + threadIdx.x;
-    if (i < E) {
-      const int32_t p = atomicAdd(&cur[c[j] >> kBucketBits], 1);
-      if (p >= 0 && p < E)
-        out[p] = c[j];
-      else
-        atomicOr(&counts[kErrFlags], kErrInternal);
+    if (j * kThreads + threadIdx.x < n) {
+      const int b = c[j] >> kBucketBits;
+      const int32_t p = atomicAdd(&cur[b], 1);
+      if (p >= 0 && p < n) {
+        sval[p] = (uint16_t)(c[j] & (kBucketSize - 1));
+        sbkt[p] = (uint16_t)b;
+      }
     }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < n; i += kThreads) {
+    const int b = sbkt[i];
+    const int64_t g = (int64_t)gbase[b] + (i - lbase[b]);
+    if (g >= 0 && g < E)
+      out[g] = sval[i];
+    else
+      atomicOr(&counts[kErrFlags], kErrInternal);
   }
 }
 
 // kOutdegSplit workgroups per bucket, each counting one slice of the
 // bucket into LDS and storing its partial histogram (a hub's occurrences are
 // split over the workgroups, so same-address LDS atomics stay few per CU)
-constexpr int kOutdegSplit = 16;
+constexpr int kOutdegSplit = 8;
 
-__global__ __launch_bounds__(1024) void k_outdeg_count(const int32_t* __restrict__ bucketed,
+__global__ __launch_bounds__(1024) void k_outdeg_count(const uint16_t* __restrict__ bucketed,
                                                        const int32_t* __restrict__ offs,
                                                        int64_t ntiles, int nb, int64_t E,
                                                        int32_t Vs, int32_t* __restrict__ part,
@@ -245,7 +320,7 @@ __global__ __launch_bounds__(1024) void k_outdeg_count(const int32_t* __restrict
 #pragma unroll
     for (int j = 0; j < kB; ++j) {
       const int64_t i = i0 + j * 1024 + threadIdx.x;
-      v[j] = i < s1 ? __builtin_nontemporal_load(bucketed + i) : -1;
+      v[j] = i < s1 ? (int32_t)__builtin_nontemporal_load(bucketed + i) : -1;
     }
 #pragma unroll
     for (int j = 0; j < kB; ++j)
@@ -552,7 +627,7 @@ bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t
   take(hist_n);
   take(scan_tiles + 1);
   take(L->max_segments);
-  take(L->outdeg_bucketed ? E : 0);
+  take(L->outdeg_bucketed ? cdiv(E, 2) : 0);
   take(L->outdeg_bucketed ? L->outdeg_nb * L->edge_tiles : 0);
   take(L->outdeg_bucketed ? (int64_t)kOutdegSplit * L->outdeg_nb * kBucketSize : 0);
   L->scratch_bytes = o - L->off_scratch;
@@ -583,7 +658,7 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
     scan_tiles = cdiv(L.outdeg_nb * L.edge_tiles, kTile);
   int32_t* tile_sums = reinterpret_cast<int32_t*>(take(scan_tiles + 1));
   int32_t* P = reinterpret_cast<int32_t*>(take(L.max_segments));
-  int32_t* bucketed = reinterpret_cast<int32_t*>(take(L.outdeg_bucketed ? E : 0));
+  uint16_t* bucketed = reinterpret_cast<uint16_t*>(take(L.outdeg_bucketed ? cdiv(E, 2) : 0));
   int32_t* ohist = reinterpret_cast<int32_t*>(take(L.outdeg_bucketed ? L.outdeg_nb * L.edge_tiles : 0));
   int32_t* opart = reinterpret_cast<int32_t*>(
       take(L.outdeg_bucketed ? (int64_t)kOutdegSplit * L.outdeg_nb * kBucketSize : 0));
@@ -593,16 +668,17 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
     hipLaunchKernelGGL(k_zero, dim3(grid_for(Vs)), dim3(kThreads), 0, st, p.d_out, (int64_t)Vs);
   if (V == 0) return hipGetLastError();
   const int edges_too = L.outdeg_bucketed ? 0 : 1;
-  hipLaunchKernelGGL(k_degrees, dim3(grid_for(edges_too && E > V ? E : V)), dim3(kThreads), 0, st,
+  hipLaunchKernelGGL(k_degrees, dim3(grid_for(edges_too && E > V ? E : V, 2048)), dim3(kThreads), 0, st,
                      p.row_ptr, p.col_idx, V, Vs, E, edges_too, p.d_in, p.d_out, p.counts);
   if (L.outdeg_bucketed) {
     const int nb = (int)L.outdeg_nb;
     const int64_t et = L.edge_tiles;
-    hipLaunchKernelGGL(k_outdeg_hist, dim3(et), dim3(kThreads), 0, st, p.col_idx, E, Vs, nb,
-                       ohist, et, p.counts);
+    hipLaunchKernelGGL(k_outdeg_hist, dim3(et), dim3(kThreads), (kThreads / 64) * nb * 4, st,
+                       p.col_idx, E, Vs, nb, ohist, et, p.counts);
     scan(ArrF{ohist}, (int64_t)nb * et, nullptr, ohist, nullptr, tile_sums, p.counts, st);
-    hipLaunchKernelGGL(k_outdeg_scatter, dim3(et), dim3(kThreads), 0, st, p.col_idx, E, nb, ohist,
-                       et, bucketed, p.counts);
+    hipLaunchKernelGGL(k_outdeg_scatter, dim3(et), dim3(kThreads),
+                       3 * nb * 4 + 2 * kEdgeTile * 2, st, p.col_idx, E, nb, ohist, et, bucketed,
+                       p.counts);
     hipLaunchKernelGGL(k_outdeg_count, dim3(kOutdegSplit, nb), dim3(1024), 0, st, bucketed, ohist,
                        et, nb, E, Vs, opart, p.counts);
     hipLaunchKernelGGL(k_outdeg_reduce, dim3(grid_for(Vs)), dim3(kThreads), 0, st, opart, nb, Vs,
