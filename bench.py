@@ -247,6 +247,88 @@ def time_unfused(step, reps=3):
     return ms
 
 
+SUITE = [  # the other workloads, one model each (Table I models at their configured sizes)
+    ("gcn_er", "2-layer GCN, directed ER G(2000, 10000) + self-loops, 128->16->8"),
+    ("gat_ba", "2-layer GAT, BA(20000, m=5) symmetrised + self-loops, 512->8x8->8x8 (mean)"),
+    ("sage_rmat", "GraphSAGE-pool, R-MAT scale 17, 16 edges/vertex, 256->256"),
+    ("gated_rgg", "gated edge MPNN + GRU, torus RGG(100000, expected degree 12), 64 (+16 edge)"),
+]
+
+
+def _padded(a, torch, dev):
+    """Device copy of a float32 matrix with 16-byte-aligned rows."""
+    a = torch.from_numpy(a)
+    n, f = a.shape
+    ld = (f + 3) // 4 * 4
+    t = torch.zeros((n, ld), dtype=torch.float32, device=dev)
+    t[:, :f] = a.to(dev)
+    return t[:, :f]
+
+
+def suite(dev, reps=10):
+    """Per-workload, per-layer timing of the other four workloads through
+    saga_layer (plan built once per graph and timed separately)."""
+    import torch
+
+    import paper_2009_00804_amd.layers as LY
+    import paper_2009_00804_amd.saga as S
+    from synth import configs as Cfg
+
+    out = {}
+    for name, desc in SUITE:
+        g = Cfg.build(name)
+        rp = torch.from_numpy(g["row_ptr"]).to(dev)
+        col = torch.from_numpy(g["col_idx"]).to(dev)
+        graph = S.Graph(rp, col)
+        V, E = g["num_vertices"], g["num_edges"]
+        if name == "gcn_er":
+            model = LY.gcn2(graph, torch.from_numpy(g["W1"]), torch.from_numpy(g["b1"]),
+                            torch.from_numpy(g["W2"]), torch.from_numpy(g["b2"]))
+            x, ef = _padded(g["X"][:, :g["dims"][0]], torch, dev), None
+        elif name == "gat_ba":
+            model, x, ef = LY.gat2(graph, g), _padded(g["X"], torch, dev), None
+        elif name == "sage_rmat":
+            model, x, ef = LY.sage_pool(graph, g), _padded(g["X"], torch, dev), None
+        else:
+            model = LY.gated_gru(graph, g)
+            x, ef = _padded(g["H"], torch, dev), _padded(g["E_feat"], torch, dev)
+        st = torch.cuda.current_stream()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(model) + 1)]
+        for _ in range(3):
+            LY.run(model, x, edge_feat=ef)
+        torch.cuda.synchronize()
+        per = [0.0] * len(model)
+        for _ in range(reps):
+            h = x
+            ev[0].record(st)
+            for i, layer in enumerate(model):
+                h = layer(h, edge_feat=ef)
+                ev[i + 1].record(st)
+            torch.cuda.synchronize()
+            for i in range(len(model)):
+                per[i] += ev[i].elapsed_time(ev[i + 1]) / reps
+        # plan build alone
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(reps):
+            S.saga_plan_build(graph.num_dst, graph.num_src, graph.num_edges,
+                              C.c_void_p(rp.data_ptr()), C.c_void_p(col.data_ptr()), graph.opts,
+                              C.c_void_p(graph.ws.data_ptr()), graph.ws.numel(),
+                              S.stream_handle(st))
+        e1.record(st)
+        torch.cuda.synchronize()
+        out[name] = {
+            "workload": desc, "vertices": V, "edges": E,
+            "plan_ms": e0.elapsed_time(e1) / reps,
+            "layers": [{"ms": round(ms, 5), "gteps": E / (ms * 1e-3) / 1e9,
+                        "vertices_per_s": V / (ms * 1e-3)} for ms in per]}
+        log(f"suite {name}: V={V} E={E} plan {out[name]['plan_ms']:.3f} ms, layers "
+            + ", ".join(f"{ms:.3f} ms" for ms in per))
+        del model, graph
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(g, budget_s=12.0):
     """The oracle's layer-1 GCN (aggregate-first, float64) on a bounded random
     sample of destination rows of the same workload, one thread."""
@@ -293,6 +375,8 @@ def main():
     ap.add_argument("--scale", type=int, default=21)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--no-suite", action="store_true",
+                    help="skip the per-layer timing of the four smaller workloads")
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip the fused-vs-unfused layer-1 aggregation comparison")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -413,6 +497,8 @@ def main():
             out["variants"][dt]["fusion"] = {"fused_ms": rr["mean"]["gather1"],
                                              "unfused_ms": rr["unfused_ms"],
                                              "speedup": rr["unfused_ms"] / rr["mean"]["gather1"]}
+    if not args.no_suite:
+        out["suite"] = suite(dev)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(g, args.cpu_budget)
