@@ -131,8 +131,11 @@ typedef struct saga_mat { void* ptr; int64_t rows, cols, ld; } saga_mat;
  * All of it is integer and reproducible bit for bit.
  */
 typedef struct saga_plan_opts {
-  int32_t seg_len;     /* > 0; default 512 */
-  int32_t block_cost;  /* >= seg_len + row_cost; default 4096 */
+  int32_t seg_len;     /* > 0; default (0): min(512, block_cost / 2) */
+  int32_t block_cost;  /* >= seg_len + row_cost; default (0): the power of two at
+                          or below (num_edges + row_cost * num_dst) / 2048, clamped
+                          to [256, 4096] (about 2048 row blocks on small graphs;
+                          4096 and seg_len 512 on large ones) */
   int32_t row_cost;    /* >= 1; default 4 */
 } saga_plan_opts;
 

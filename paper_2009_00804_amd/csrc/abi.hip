@@ -65,10 +65,25 @@ saga_status check_mat(const void* ptr, int64_t rows, int64_t cols, int64_t ld, i
   return SAGA_OK;
 }
 
-saga_status resolve_opts(const saga_plan_opts* o, int32_t* T, int32_t* B, int32_t* c) {
-  *T = o && o->seg_len ? o->seg_len : 512;
+// Defaults sized to the graph: enough row blocks (about 2048) to fill the
+// GPU on small graphs.  block_cost = the power of two at or below
+// (E + row_cost * V) / 2048, clamped to [256, 4096]; seg_len = min(512,
+// block_cost / 2).  The 2^21-vertex graph gets 4096 and 512.
+int32_t default_block_cost(int64_t V, int64_t E, int32_t c) {
+  const int64_t total = E + (int64_t)c * V;
+  int64_t b = 256;
+  while (b < 4096 && b * 2 <= total / 2048) b *= 2;
+  return (int32_t)b;
+}
+
+saga_status resolve_opts(const saga_plan_opts* o, int64_t V, int64_t E, int32_t* T, int32_t* B,
+                         int32_t* c) {
+  const bool auto_t = !(o && o->seg_len), auto_b = !(o && o->block_cost);
   *c = o && o->row_cost ? o->row_cost : 4;
-  *B = o && o->block_cost ? o->block_cost : 4096;
+  *B = auto_b ? default_block_cost(V, E, *c) : o->block_cost;
+  *T = auto_t ? (*B / 2 < 512 ? *B / 2 : 512) : o->seg_len;
+  if (auto_b && *c > 0 && *T > 0)
+    while (*B < *T + *c && *B < (1 << 30)) *B *= 2;
   if (*T <= 0 || *c <= 0) return fail(SAGA_EINVAL, "plan options: seg_len and row_cost must be > 0");
   if (*B < *T + *c) return fail(SAGA_EINVAL, "plan options: block_cost must be >= seg_len + row_cost");
   return SAGA_OK;
@@ -702,7 +717,7 @@ saga_status saga_plan_workspace_size(int32_t num_dst, int32_t num_src, int64_t n
   try {
     if (!bytes) return fail(SAGA_EINVAL, "bytes is null");
     int32_t T, B, c;
-    saga_status s = resolve_opts(opts, &T, &B, &c);
+    saga_status s = resolve_opts(opts, num_dst, num_edges, &T, &B, &c);
     if (s) return s;
     saga::PlanLayout L;
     if (!saga::plan_layout(num_dst, num_src, num_edges, T, B, c, &L))
@@ -721,7 +736,7 @@ saga_status saga_plan_build(int32_t num_dst, int32_t num_src, int64_t num_edges,
   try {
     if (!plan) return fail(SAGA_EINVAL, "plan is null");
     int32_t T, B, c;
-    saga_status s = resolve_opts(opts, &T, &B, &c);
+    saga_status s = resolve_opts(opts, num_dst, num_edges, &T, &B, &c);
     if (s) return s;
     saga::PlanLayout L;
     if (!saga::plan_layout(num_dst, num_src, num_edges, T, B, c, &L))

@@ -321,7 +321,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_gat(GatherArgs a) {
 // Gated messages: sigmoid(gs[u] + gd[v] + b_e + e_uv W_ee) * h[u], SUM
 // (float32, F = 64, one 16-byte slice of 4 features per lane)
 // ------------------------------------------------------------------------
-template <int LPR>
+template <int LPR, int U>
 __global__ __launch_bounds__(kThreads) void k_gather_gated(GatherArgs a) {
   constexpr int NG = kThreads / LPR;
   constexpr int FE_MAX = 16;
@@ -363,30 +363,42 @@ __global__ __launch_bounds__(kThreads) void k_gather_gated(GatherArgs a) {
         const int my = e + gl;
         const int c = my < end ? col[my] : 0;
         const int n = (end - e) < LPR ? (end - e) : LPR;
-        for (int t = 0; t < n; ++t) {
-          const int u = __shfl(c, gbase + t, 64);
-          if (!active) continue;
-          const int64_t eid = (int64_t)(e + t);
-          float hs[4], gs[4];
-          Vec16<float>::load(h + (int64_t)u * a.ld_src + gl * 4, hs);
-          Vec16<float>::load(a.gsrc + (int64_t)u * a.ld_gsrc + gl * 4, gs);
-          float pre[4];
+        // U edges' loads (h_u, S_src[u], e_uv) in flight before the math;
+        // a short last batch repeats its first edge and skips it
+        for (int t = 0; t < n; t += U) {
+          float hs[U][4], gs[U][4], ev[U][FE_MAX];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) pre[q] = gs[q] + gd[q];
-          const float* ef = a.efeat + eid * a.ld_efeat;
+          for (int k = 0; k < U; ++k) {
+            const int tk = t + k < n ? t + k : t;
+            const int u = __shfl(c, gbase + tk, 64);
+            if (active) {
+              Vec16<float>::load(h + (int64_t)u * a.ld_src + gl * 4, hs[k]);
+              Vec16<float>::load(a.gsrc + (int64_t)u * a.ld_gsrc + gl * 4, gs[k]);
+              const float* ef = a.efeat + (int64_t)(e + tk) * a.ld_efeat;
 #pragma unroll
-          for (int i4 = 0; i4 < FE_MAX / 4; ++i4) {
-            if (i4 * 4 < Fe) {
-              float ev[4];
-              Vec16<float>::load(ef + i4 * 4, ev);
+              for (int i4 = 0; i4 < FE_MAX / 4; ++i4) {
+                float v4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                if (i4 * 4 < Fe) Vec16<float>::load(ef + i4 * 4, v4);
 #pragma unroll
-              for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) pre[q] += ev[j] * wr[i4 * 4 + j][q];
+                for (int j = 0; j < 4; ++j) ev[k][i4 * 4 + j] = v4[j];
+              }
             }
           }
+          if (!active) continue;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) acc[q] += sigmoidf_(pre[q]) * hs[q];
+          for (int k = 0; k < U; ++k) {
+            if (t + k < n) {
+              float pre[4];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) pre[q] = gs[k][q] + gd[q];
+#pragma unroll
+              for (int j = 0; j < FE_MAX; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) pre[q] += ev[k][j] * wr[j][q];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) acc[q] += sigmoidf_(pre[q]) * hs[k][q];
+            }
+          }
         }
       }
       if (!active) continue;
@@ -657,7 +669,7 @@ hipError_t launch_gather(const GatherArgs& a, hipStream_t st) {
     }
     err = hipGetLastError();
   } else if (a.msg == SAGA_MSG_GATED) {
-    hipLaunchKernelGGL((k_gather_gated<16>), dim3(grid), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((k_gather_gated<16, 4>), dim3(grid), dim3(kThreads), 0, st, a);
     err = hipGetLastError();
   } else if (a.dtype == SAGA_BF16) {
     err = launch_simple<uint16_t>(a, nv, grid, st);

@@ -571,9 +571,9 @@ Tiling choose(int dtype, int mode, int64_t N) {
   if (mode == SAGA_GEMM_GRU) return Tiling{1, (int)(N / 16), 4, false};
   const int64_t nt = (N + 15) / 16;
   if (nt <= 5) return Tiling{2, (int)nt, 4, false};
-  if (nt <= 8)  // measured best on the 2^21 x 602 x 128 transform
-    return cfg_override(dtype == SAGA_BF16 ? Tiling{1, 8, 4, false, 8} : Tiling{2, 8, 2, true});
-  return Tiling{2, 16, 3, false};
+  // 128-column tiles (more columns: several tiles along N), measured best
+  // on the 2^21 x 602 x 128 transform and on 131072 x 512 x 256
+  return cfg_override(dtype == SAGA_BF16 ? Tiling{1, 8, 4, false, 8} : Tiling{2, 8, 2, true});
 }
 
 int kc_of(int dtype) { return dtype == SAGA_BF16 ? Mma<uint16_t>::KC : Mma<float>::KC; }
@@ -628,10 +628,7 @@ hipError_t launch_nt(const GemmArgs& g, const Tiling& t, hipStream_t st) {
     if (t.mt == 4) return launch_plain<T, 4, 8, RegA<T, 4, 8, 3>>(g, st);
     if (t.stages == 3) return launch_plain<T, 2, 8, RegA<T, 2, 8, 3>>(g, st);
   }
-  if constexpr (NT == 16)
-    return launch_plain<T, 2, 16, RegA<T, 2, 16, 3>>(g, st);
-  else
-    return launch_plain<T, 2, NT, RegA<T, 2, NT, 4>>(g, st);
+  return launch_plain<T, 2, NT, RegA<T, 2, NT, 4>>(g, st);
 }
 
 template <typename T>
@@ -654,8 +651,7 @@ hipError_t dispatch(const GemmArgs& g, hipStream_t st) {
     case 3: return launch_nt<T, 3>(g, t, st);
     case 4: return launch_nt<T, 4>(g, t, st);
     case 5: return launch_nt<T, 5>(g, t, st);
-    case 8: return launch_nt<T, 8>(g, t, st);
-    default: return launch_nt<T, 16>(g, t, st);
+    default: return launch_nt<T, 8>(g, t, st);
   }
 }
 
