@@ -265,9 +265,22 @@ def _padded(a, torch, dev):
     return t[:, :f]
 
 
-def suite(dev, reps=10):
+def _oracle_model(name, g):
+    from oracle import saga_oracle as O
+
+    if name == "gcn_er":
+        return O.gcn_2layer(g, X=g["X"][:, :g["dims"][0]])
+    if name == "gat_ba":
+        return O.gat_2layer(g)
+    if name == "sage_rmat":
+        return O.sage_layer_of(g)
+    return O.gated_layer_of(g)
+
+
+def suite(dev, reps=10, oracle=True):
     """Per-workload, per-layer timing of the other four workloads through
-    saga_layer (plan built once per graph and timed separately)."""
+    saga_layer (plan built once per graph and timed separately); with
+    `oracle`, the oracle's whole model on the same inputs, one thread."""
     import torch
 
     import paper_2009_00804_amd.layers as LY
@@ -324,6 +337,16 @@ def suite(dev, reps=10):
                         "vertices_per_s": V / (ms * 1e-3)} for ms in per]}
         log(f"suite {name}: V={V} E={E} plan {out[name]['plan_ms']:.3f} ms, layers "
             + ", ".join(f"{ms:.3f} ms" for ms in per))
+        if oracle:
+            from threadpoolctl import threadpool_limits
+
+            with threadpool_limits(1):
+                t0 = time.perf_counter()
+                _oracle_model(name, g)
+                t = time.perf_counter() - t0
+            out[name]["cpu_oracle"] = {"ms": t * 1e3, "edges_per_s": len(per) * E / t, "cores": 1,
+                                       "kind": "oracle", "sample": "whole model, float64"}
+            log(f"suite {name}: oracle {t:.2f} s")
         del model, graph
         torch.cuda.empty_cache()
     return out
@@ -498,7 +521,7 @@ def main():
                                              "unfused_ms": rr["unfused_ms"],
                                              "speedup": rr["unfused_ms"] / rr["mean"]["gather1"]}
     if not args.no_suite:
-        out["suite"] = suite(dev)
+        out["suite"] = suite(dev, oracle=not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(g, args.cpu_budget)
