@@ -42,6 +42,13 @@ notes of the repository):
   R6 SAGE-pool: p_u = ReLU(h_u W_pool + b_pool), elementwise max over
      in-edges, y = [h_v | a_v] W + b, no activation.
   R7 ReLU(x) = x if x > 0 else +0.
+  R8 GraphSAGE with the LSTM reduction (Table I, GraphSAGE row; Sec. 3.2
+     "Gather"): the in-edges of v, in CSR order, are the input sequence of
+     an LSTM that starts from h = c = 0; a_v is its final hidden state (0
+     for an empty row).  Gate blocks in the order (i, f, g, o) of width H:
+     [i|f|g|o] = x_t W_ih + b_ih + h W_hh + b_hh, c = f*c + i*g,
+     h = o*tanh(c), with i, f, o sigmoids and g a tanh.  Then
+     y_v = [x_v | a_v] W + b, no activation.
 """
 from __future__ import annotations
 
@@ -425,3 +432,62 @@ def gated_layer_of(g, rows=None):
 def sage_layer_of(g, rows=None):
     return sage_pool_layer(g["row_ptr"], g["col_idx"], g["X"], g["W_pool"], g["b_pool"],
                            g["W"], g["b"], rows=rows)
+
+
+def lstm_gather(row_ptr, col_idx, X, W_ih, b_ih, W_hh, b_hh, rows=None):
+    """LSTM reduction over each destination's in-edges (reading R8).
+
+    The paper names this Gather as the one that cannot be fused: it treats
+    the in-edges of a vertex as a sequence (Sec. 3.2, Gather paragraph).
+    For row v with sources u_1 .. u_d in CSR order, starting from h = c = 0:
+        [i | f | g | o] = x_{u_t} W_ih + b_ih + h W_hh + b_hh
+        i, f, o = sigmoid(.), g = tanh(.)
+        c = f * c + i * g;  h = o * tanh(c)
+    and a_v = h after the last step (0 for an empty row).
+    """
+    rp = np.asarray(row_ptr, dtype=np.int64)
+    col = np.asarray(col_idx, dtype=np.int64)
+    rows = _rows_arg(rows, rp.shape[0] - 1)
+    Wi, Wh = _f64(W_ih), _f64(W_hh)
+    b = _f64(b_ih) + _f64(b_hh)
+    H = Wh.shape[0]
+    A = np.zeros((rows.shape[0], H), dtype=np.float64)
+    for n, v in enumerate(rows):
+        nb = col[rp[v]:rp[v + 1]]
+        if nb.shape[0] == 0:
+            continue
+        # input contributions of the whole sequence at once (a matrix
+        # product over the sequence); the recurrence itself is step by step
+        gx = _f64(X[nb]) @ Wi + b[None, :]
+        h = np.zeros(H)
+        c = np.zeros(H)
+        for t in range(nb.shape[0]):
+            h, c = lstm_cell(gx[t] + h @ Wh, c)
+        A[n] = h
+    return A
+
+
+def lstm_cell(z, c):
+    """One LSTM step from the gate pre-activations z = [i | f | g | o]."""
+    H = c.shape[0]
+    i = sigmoid(z[:H])
+    f = sigmoid(z[H:2 * H])
+    g = np.tanh(z[2 * H:3 * H])
+    o = sigmoid(z[3 * H:])
+    c = f * c + i * g
+    return o * np.tanh(c), c
+
+
+def sage_lstm_layer(row_ptr, col_idx, X, W_ih, b_ih, W_hh, b_hh, W, b, rows=None):
+    """GraphSAGE layer with the LSTM reduction (Table I, GraphSAGE row:
+    LSTM(in_edges) Gather, MLP ApplyVertex; reading R8):
+    y_v = [x_v | a_v] W + b with a_v = lstm_gather(...)."""
+    rows = _rows_arg(rows, len(row_ptr) - 1)
+    A = lstm_gather(row_ptr, col_idx, X, W_ih, b_ih, W_hh, b_hh, rows=rows)
+    cat = np.concatenate([_f64(X[rows]), A], axis=1)
+    return dense(cat, W, bias=b)
+
+
+def sage_lstm_layer_of(g, rows=None):
+    return sage_lstm_layer(g["row_ptr"], g["col_idx"], g["X"], g["W_ih"], g["b_ih"], g["W_hh"],
+                           g["b_hh"], g["W"], g["b"], rows=rows)

@@ -96,6 +96,29 @@ def sage_rmat(scale=17, avg_deg=16, f=256, key=3):
     return d
 
 
+def sage_lstm(scale=17, avg_deg=16, f=256, hidden=128, f_out=256, key=6, graph_key=3):
+    """GraphSAGE with the LSTM Gather on the GraphSAGE-pool workload's R-MAT
+    graph and features (same graph_key); LSTM weights U(+-1/sqrt(hidden))."""
+    n = 1 << scale
+    E = avg_deg * n
+    src, dst = G.rmat(scale, E, *RMAT_ABC, key=(graph_key, 0))
+    perm = G.rng_for(graph_key, 4).permutation(n).astype(np.int32)
+    src, dst = G.relabel(src, dst, perm)
+    d = _csr_dict("sage_lstm", n, src, dst)
+    d["model"] = "sage_lstm"
+    d["X"] = T.normal_matrix(n, f, (graph_key, 1))
+    rw = G.rng_for(key, 3)
+    a = 1.0 / np.sqrt(hidden)
+    d["W_ih"] = rw.uniform(-a, a, (f, 4 * hidden)).astype(np.float32)
+    d["W_hh"] = rw.uniform(-a, a, (hidden, 4 * hidden)).astype(np.float32)
+    d["b_ih"] = rw.uniform(-a, a, 4 * hidden).astype(np.float32)
+    d["b_hh"] = rw.uniform(-a, a, 4 * hidden).astype(np.float32)
+    d["W"] = T.glorot(f + hidden, f_out, rw)
+    d["b"] = T.bias(f + hidden, f_out, rw)
+    d["dims"] = (f, hidden, f_out)
+    return d
+
+
 def gated_rgg(n=100000, avg_deg=12, f=64, fe=16, key=4):
     r = math.sqrt(avg_deg / (math.pi * (n - 1)))
     src, dst = G.torus_rgg(n, r, G.rng_for(key, 0))
@@ -159,6 +182,7 @@ BUILDERS = {
     "sage_rmat": sage_rmat,
     "gated_rgg": gated_rgg,
     "gcn_rmat": gcn_rmat,
+    "sage_lstm": sage_lstm,
 }
 
 # scaled variants used by parity tests (K + 100 seeds)
@@ -168,6 +192,7 @@ SMALL = {
     "sage_rmat": dict(scale=12, key=103),
     "gated_rgg": dict(n=8000, key=104),
     "gcn_rmat": dict(scale=13, avg_deg=50, key=105),
+    "sage_lstm": dict(scale=10, key=106, graph_key=106),
 }
 
 
