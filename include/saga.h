@@ -19,6 +19,8 @@
  *   saga_scatter_gather_unfused     the same, unfused: materialised edge
  *                                   tensor, then a segment reduction (the
  *                                   baseline of Fig. 7a)
+ *   saga_lstm_gather                GraphSAGE's LSTM Gather: a recurrence
+ *                                   along each row's in-edges
  *   saga_apply_vertex               dense per-vertex transform on the matrix
  *                                   cores, with fused epilogues (Sec. 3.2
  *                                   "ApplyVertex", Table III)
@@ -279,12 +281,37 @@ saga_status saga_scatter_gather_unfused(const saga_plan* plan, const saga_edge_o
                                         void* workspace, size_t workspace_bytes,
                                         void* stream);
 
+/* ----------------------------------------------------------------------
+ * LSTM Gather (GraphSAGE row of Table I; Sec. 3.2 "Gather": the reduction
+ * that treats a vertex's in-edges as a sequence and cannot be fused).  For
+ * destination v with sources u_1 .. u_d in CSR order, from h = c = 0:
+ *     z = gates_x[u_t] + h w_hh        (gate blocks i | f | g | o, width H)
+ *     i, f, o = sigmoid(z_i, z_f, z_o);  g = tanh(z_g)
+ *     c = f * c + i * g;  h = o * tanh(c)
+ * out[v] = h after step d (0 for an empty row).  gates_x is the input part
+ * of the gates, computed once per source vertex: x_u W_ih + b_ih + b_hh
+ * (saga_apply_vertex with bias and bias2), num_src x 4H.  w_hh: H x 4H.
+ * out: num_dst x H.  All float32; H = 32, 64 or 128 (SAGA_EUNSUPPORTED
+ * otherwise).  Rows run longest first on a persistent grid; the time is
+ * bounded below by the longest row's d sequential steps.
+ * Workspace: saga_lstm_gather_workspace_size() bytes (a work-queue counter,
+ * cleared by the call itself), 256-byte aligned.
+ * ---------------------------------------------------------------------- */
+saga_status saga_lstm_gather_workspace_size(const saga_plan* plan, int64_t hidden,
+                                            size_t* bytes);
+
+saga_status saga_lstm_gather(const saga_plan* plan, saga_cmat gates_x, saga_cmat w_hh,
+                             saga_mat out, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
 /* ======================================================================
  * ApplyVertex: dense transform on the matrix cores
  * ======================================================================
  * Sec. 3.2 "ApplyVertex" (all vertices batched into one GEMM), Table III.
- * mode PLAIN:  out = act(rs * (a w) + bias)
- * mode CONCAT: out = act(rs * (a w + a2 w2) + bias)   ([a | a2] [w ; w2])
+ * mode PLAIN:  out = act(rs * (a w) + bias + bias2)
+ * mode CONCAT: out = act(rs * (a w + a2 w2) + bias + bias2)   ([a | a2] [w ; w2])
+ *              (bias, bias2 nullable; two vectors so that e.g. an LSTM's
+ *              b_ih + b_hh need not be summed by the caller)
  * mode GRU:    GRU cell with input a and hidden state a2 (Fig. 2, GGNN):
  *              gi = a w + bias, gh = a2 w2 + bias2 (column blocks r, z, n of
  *              width F = a2.cols), r = s(gi_r + gh_r), z = s(gi_z + gh_z),
@@ -329,6 +356,9 @@ saga_status saga_apply_vertex(const saga_gemm_op* op, saga_cmat a, saga_cmat w,
  *           act(concat + b) or mean over heads + b.
  * SAGE_POOL P = ReLU(X W_pool + b_pool); A = max-Gather of P;
  *           out = [X | A] W + b   (W is 2 F_in x F_out).
+ * SAGE_LSTM P = X W_ih + b_ih + b_hh; A = LSTM Gather of P with W_hh
+ *           (saga_lstm_gather); out = [X | A] W + b (W is (F_in + H) x
+ *           F_out).  float32 only.
  * GATED_GRU [S_src, S_dst] = X [W_e,src, W_e,dst]; gated sum-Gather with
  *           W_e,edge and b_e; out = GRU(a, X) with W_ih, W_hh, b_ih, b_hh.
  *           (W_e rows: [0,F) src part, [F,2F) dst part, [2F,2F+Fe) edge.)
@@ -339,7 +369,8 @@ typedef enum saga_layer_kind {
   SAGA_LAYER_GCN = 0,
   SAGA_LAYER_GAT = 1,
   SAGA_LAYER_SAGE_POOL = 2,
-  SAGA_LAYER_GATED_GRU = 3
+  SAGA_LAYER_GATED_GRU = 3,
+  SAGA_LAYER_SAGE_LSTM = 4
 } saga_layer_kind;
 
 typedef struct saga_layer_desc {
@@ -354,8 +385,9 @@ typedef struct saga_layer_desc {
   const void* w_pool; const float* b_pool;    /* SAGE_POOL */
   const float* attn_l; const float* attn_r;   /* GAT: heads x (F/heads) */
   const float* w_e; const float* b_e;         /* GATED_GRU: (2F + Fe) x F, F */
-  const float* w_ih; const float* b_ih;       /* GATED_GRU: F x 3F, 3F */
-  const float* w_hh; const float* b_hh;
+  const float* w_ih; const float* b_ih;       /* GATED_GRU: F x 3F, 3F; SAGE_LSTM: F x 4H, 4H */
+  const float* w_hh; const float* b_hh;       /* GATED_GRU: F x 3F;  SAGE_LSTM: H x 4H, 4H */
+  int32_t hidden;                             /* SAGE_LSTM: H (32, 64 or 128) */
 } saga_layer_desc;
 
 saga_status saga_layer_workspace_size(const saga_plan* plan, const saga_layer_desc* desc,

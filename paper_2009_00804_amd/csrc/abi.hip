@@ -430,6 +430,51 @@ saga_status run_gather_unfused(const saga_plan& p, const saga_edge_op& op,
   return ok();
 }
 
+// ---------------------------------------------------------------------------
+// LSTM Gather
+// ---------------------------------------------------------------------------
+constexpr size_t kLstmWs = 256;
+
+saga_status run_lstm(const saga_plan& p, const saga_cmat& gx, const saga_cmat& whh,
+                     const saga_mat& out, void* ws, size_t ws_bytes, hipStream_t st) {
+  const int64_t H = whh.rows;
+  if (H != 32 && H != 64 && H != 128)
+    return fail(SAGA_EUNSUPPORTED, "lstm gather: hidden size must be 32, 64 or 128 (got %lld)",
+                (long long)H);
+  saga_status s = check_mat(gx.ptr, gx.rows, gx.cols, gx.ld, p.num_src, 4 * H, 4, true, "gates_x");
+  if (s) return s;
+  s = check_mat(whh.ptr, whh.rows, whh.cols, whh.ld, H, 4 * H, 4, false, "w_hh");
+  if (s) return s;
+  s = check_mat(out.ptr, out.rows, out.cols, out.ld, p.num_dst, H, 4, false, "out");
+  if (s) return s;
+  if (!ws || ws_bytes < kLstmWs)
+    return fail(SAGA_EWORKSPACE, "lstm workspace: need %zu bytes, got %zu", kLstmWs, ws_bytes);
+  if ((uintptr_t)ws % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
+  const size_t ob = mat_bytes(out.rows, out.cols, out.ld, 4);
+  if (range_overlap(out.ptr, ob, gx.ptr, mat_bytes(gx.rows, gx.cols, gx.ld, 4)) ||
+      range_overlap(out.ptr, ob, whh.ptr, mat_bytes(whh.rows, whh.cols, whh.ld, 4)) ||
+      range_overlap(out.ptr, ob, ws, kLstmWs))
+    return fail(SAGA_EINVAL, "output overlaps an input or the workspace");
+  saga::LstmArgs a;
+  memset(&a, 0, sizeof(a));
+  a.row_ptr = p.row_ptr;
+  a.col_idx = p.col_idx;
+  a.perm = p.perm;
+  a.counts = p.counts;
+  a.num_dst = p.num_dst;
+  a.hidden = (int)H;
+  a.gates_x = static_cast<const float*>(gx.ptr);
+  a.ld_gx = gx.ld;
+  a.w_hh = static_cast<const float*>(whh.ptr);
+  a.ld_whh = whh.ld;
+  a.out = static_cast<float*>(out.ptr);
+  a.ld_out = out.ld;
+  a.queue = static_cast<int32_t*>(ws);
+  hipError_t e = saga::launch_lstm_gather(a, st);
+  if (e != hipSuccess) return dev_fail(e, "lstm gather launch");
+  return ok();
+}
+
 saga_status layer_check_desc(const saga_plan& p, const saga_layer_desc& d) {
   if (p.num_dst != p.num_src) return fail(SAGA_EINVAL, "layers need num_src == num_dst");
   if (d.in_feat <= 0 || d.out_feat <= 0) return fail(SAGA_EINVAL, "layer feature sizes must be > 0");
@@ -446,6 +491,12 @@ saga_status layer_check_desc(const saga_plan& p, const saga_layer_desc& d) {
     case SAGA_LAYER_SAGE_POOL:
       if (d.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "SAGE layer is float32 only");
       if (!d.w || !d.w_pool) return fail(SAGA_EINVAL, "SAGE: null weights");
+      break;
+    case SAGA_LAYER_SAGE_LSTM:
+      if (d.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "SAGE-LSTM layer is float32 only");
+      if (!d.w || !d.w_ih || !d.w_hh) return fail(SAGA_EINVAL, "SAGE-LSTM: null weights");
+      if (d.hidden != 32 && d.hidden != 64 && d.hidden != 128)
+        return fail(SAGA_EUNSUPPORTED, "SAGE-LSTM: hidden must be 32, 64 or 128");
       break;
     case SAGA_LAYER_GATED_GRU:
       if (d.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "gated layer is float32 only");
@@ -468,6 +519,7 @@ struct LayerBufs {
   size_t part_bytes = 0;
   void* gws = nullptr;                     // packed weights of the layer's GEMMs
   size_t gws_bytes = 0;
+  void* lstm_q = nullptr;                  // LSTM Gather work-queue counter
 };
 
 bool gcn_transform_first(const saga_layer_desc& d) { return d.out_feat <= d.in_feat; }
@@ -513,6 +565,15 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
       op.reduce = SAGA_RED_MAX;
       gfeat = d.in_feat;
       break;
+    case SAGA_LAYER_SAGE_LSTM:
+      b->ldz = 4 * (int64_t)d.hidden;  // P rows of 512 B (H = 32) to 2 KB, whole lines
+      b->z = c.take((size_t)V * b->ldz * 4);
+      b->ldz2 = ld_for(d.hidden, SAGA_F32);
+      b->z2 = c.take((size_t)V * b->ldz2 * 4);
+      b->lstm_q = c.take(kLstmWs);
+      op.reduce = SAGA_RED_SUM;
+      gfeat = 0;
+      break;
     case SAGA_LAYER_GATED_GRU:
       b->ldz = ld_for(d.in_feat, t);
       b->z = c.take((size_t)V * b->ldz * es);
@@ -524,8 +585,8 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
       gfeat = d.in_feat;
       break;
   }
-  size_t pb;
-  gather_ws_bytes(p, op, gfeat, &pb);
+  size_t pb = 0;
+  if (gfeat > 0) gather_ws_bytes(p, op, gfeat, &pb);
   b->part_bytes = pb;
   b->part = c.take(pb);
   // one region for the packed weights, sized for the largest GEMM of the layer
@@ -554,6 +615,12 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
       gb = gemm_ws_bytes(g, Fi, 0, Fi);
       g.mode = SAGA_GEMM_GRU;
       gb = std::max(gb, gemm_ws_bytes(g, Fi, Fi, 3 * Fi));
+      break;
+    }
+    case SAGA_LAYER_SAGE_LSTM: {
+      gb = gemm_ws_bytes(g, Fi, 0, 4 * (int64_t)d.hidden);
+      g.mode = SAGA_GEMM_CONCAT;
+      gb = std::max(gb, gemm_ws_bytes(g, Fi, d.hidden, Fo));
       break;
     }
   }
@@ -662,6 +729,22 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       g.act = SAGA_ACT_NONE;
       return run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, Fi, b.ldz2},
                       saga_cmat{w + (size_t)Fi * Fo * es, Fi, Fo, Fo}, d.b, nullptr, out, b.gws, b.gws_bytes, st);
+    }
+    case SAGA_LAYER_SAGE_LSTM: {
+      // P = X W_ih + b_ih + b_hh; A = LSTM Gather; out = [X | A] W + b
+      const int64_t H = d.hidden;
+      g.mode = SAGA_GEMM_PLAIN;
+      s = run_gemm(g, x, saga_cmat{d.w_ih, Fi, 4 * H, 4 * H}, none, none, d.b_ih, d.b_hh,
+                   saga_mat{b.z, V, 4 * H, b.ldz}, b.gws, b.gws_bytes, st);
+      if (s) return s;
+      s = run_lstm(p, saga_cmat{b.z, V, 4 * H, b.ldz}, saga_cmat{d.w_hh, H, 4 * H, 4 * H},
+                   saga_mat{b.z2, V, H, b.ldz2}, b.lstm_q, kLstmWs, st);
+      if (s) return s;
+      const char* w = static_cast<const char*>(d.w);
+      g.mode = SAGA_GEMM_CONCAT;
+      return run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, H, b.ldz2},
+                      saga_cmat{w + (size_t)Fi * Fo * 4, H, Fo, Fo}, d.b, nullptr, out, b.gws,
+                      b.gws_bytes, st);
     }
     case SAGA_LAYER_GATED_GRU: {
       const int64_t F = Fi, Fe = d.edge_feat;
@@ -860,6 +943,35 @@ saga_status saga_scatter_gather_unfused(const saga_plan* plan, const saga_edge_o
     if (!op || !in) return fail(SAGA_EINVAL, "null argument");
     return run_gather_unfused(*plan, *op, *in, out, workspace, workspace_bytes,
                               static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_lstm_gather_workspace_size(const saga_plan* plan, int64_t hidden,
+                                            size_t* bytes) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!bytes) return fail(SAGA_EINVAL, "bytes is null");
+    if (hidden != 32 && hidden != 64 && hidden != 128)
+      return fail(SAGA_EUNSUPPORTED, "lstm gather: hidden size must be 32, 64 or 128");
+    *bytes = kLstmWs;
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_lstm_gather(const saga_plan* plan, saga_cmat gates_x, saga_cmat w_hh,
+                             saga_mat out, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (plan->num_dst == 0) return ok();
+    return run_lstm(*plan, gates_x, w_hh, out, workspace, workspace_bytes,
+                    static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(SAGA_EINTERNAL, "exception");
   }

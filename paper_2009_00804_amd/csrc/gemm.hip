@@ -493,6 +493,7 @@ __global__ __launch_bounds__(R::THREADS) void k_gemm(GemmArgs g) {
         if (c >= g.N) continue;
         float v = acc[mt][nt][r] * rs;
         if (g.bias) v += g.bias[c];
+        if (g.bias2) v += g.bias2[c];
         out[row * g.ldo + c] = Mma<T>::from_f(apply_act(g.act, v));
       }
     }

@@ -101,6 +101,21 @@ struct GemmArgs {
   const void* wt; int64_t kp;
   const void* wt2; int64_t kp2;
 };
+// LSTM Gather (GraphSAGE): recurrence over each row's in-edges
+struct LstmArgs {
+  const int32_t* row_ptr;
+  const int32_t* col_idx;
+  const int32_t* perm;
+  const int32_t* counts;
+  int32_t num_dst;
+  int hidden;                          // H: 32, 64 or 128
+  const float* gates_x; int64_t ld_gx; // num_src x 4H: x W_ih + b_ih + b_hh
+  const float* w_hh; int64_t ld_whh;   // H x 4H
+  float* out; int64_t ld_out;          // num_dst x H
+  int32_t* queue;                      // work-queue counter (workspace)
+};
+hipError_t launch_lstm_gather(const LstmArgs& a, hipStream_t st);
+
 // bytes of workspace launch_gemm needs for these shapes (packed weights)
 size_t gemm_workspace_bytes(int dtype, int mode, int64_t N, int64_t K, int64_t K2);
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t st);

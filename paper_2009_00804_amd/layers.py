@@ -26,13 +26,13 @@ class Layer:
 
     def __init__(self, graph: S.Graph, kind: str, in_feat: int, out_feat: int, weights: dict,
                  dtype=torch.float32, act="none", heads=1, head_mean=False, neg_slope=0.2,
-                 edge_feat=0, out_ld=None):
+                 edge_feat=0, out_ld=None, hidden=0):
         dev = graph.row_ptr.device
         self.graph = graph
         self.dtype = dtype
         wdt = dtype
         kinds = {"gcn": S.SAGA_LAYER_GCN, "gat": S.SAGA_LAYER_GAT, "sage_pool": S.SAGA_LAYER_SAGE_POOL,
-                 "gated_gru": S.SAGA_LAYER_GATED_GRU}
+                 "gated_gru": S.SAGA_LAYER_GATED_GRU, "sage_lstm": S.SAGA_LAYER_SAGE_LSTM}
         self.w = {k: (_dev(v, dev, wdt if k in ("w", "w_pool") else torch.float32))
                   for k, v in weights.items()}
         d = S.saga_layer_desc()
@@ -45,6 +45,7 @@ class Layer:
         d.neg_slope = neg_slope
         d.act = S.ACT[act]
         d.edge_feat = edge_feat
+        d.hidden = hidden
         for k in ("w", "b", "w_pool", "b_pool", "attn_l", "attn_r", "w_e", "b_e", "w_ih", "b_ih",
                   "w_hh", "b_hh"):
             t = self.w.get(k)
@@ -95,6 +96,14 @@ def gated_gru(graph, g):
     return [Layer(graph, "gated_gru", F, F,
                   {"w_e": g["W_e"], "b_e": g["b_e"], "w_ih": g["W_ih"], "b_ih": g["b_ih"],
                    "w_hh": g["W_hh"], "b_hh": g["b_hh"]}, edge_feat=g["E_feat"].shape[1])]
+
+
+def sage_lstm(graph, g):
+    """GraphSAGE layer with the LSTM Gather: out = [x | LSTM(in-edges)] W + b."""
+    F, G4 = g["W_ih"].shape
+    return [Layer(graph, "sage_lstm", F, g["W"].shape[1],
+                  {"w": g["W"], "b": g["b"], "w_ih": g["W_ih"], "b_ih": g["b_ih"],
+                   "w_hh": g["W_hh"], "b_hh": g["b_hh"]}, hidden=G4 // 4)]
 
 
 def run(layers, x, edge_feat=None, stream=None):

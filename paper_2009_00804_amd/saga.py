@@ -26,7 +26,7 @@ SAGA_RED_SUM, SAGA_RED_MEAN, SAGA_RED_MAX, SAGA_RED_SOFTMAX = range(4)
 SAGA_MSG_COPY, SAGA_MSG_SRC_NORM, SAGA_MSG_GAT, SAGA_MSG_GATED = range(4)
 SAGA_ACT_NONE, SAGA_ACT_RELU, SAGA_ACT_ELU, SAGA_ACT_SIGMOID, SAGA_ACT_TANH = range(5)
 SAGA_GEMM_PLAIN, SAGA_GEMM_CONCAT, SAGA_GEMM_GRU = range(3)
-SAGA_LAYER_GCN, SAGA_LAYER_GAT, SAGA_LAYER_SAGE_POOL, SAGA_LAYER_GATED_GRU = range(4)
+SAGA_LAYER_GCN, SAGA_LAYER_GAT, SAGA_LAYER_SAGE_POOL, SAGA_LAYER_GATED_GRU, SAGA_LAYER_SAGE_LSTM = range(5)
 
 ACT = {"none": 0, "relu": 1, "elu": 2, "sigmoid": 3, "tanh": 4}
 
@@ -34,6 +34,7 @@ EXPORTS = [
     "saga_plan_workspace_size", "saga_plan_build", "saga_plan_check",
     "saga_gather_workspace_size", "saga_scatter_apply_edge_gather",
     "saga_unfused_workspace_size", "saga_scatter_gather_unfused",
+    "saga_lstm_gather_workspace_size", "saga_lstm_gather",
     "saga_apply_vertex_workspace_size", "saga_apply_vertex",
     "saga_layer_workspace_size", "saga_layer", "saga_status_str", "saga_last_error",
     "saga_version",
@@ -96,6 +97,7 @@ class saga_layer_desc(C.Structure):
         ("w", C.c_void_p), ("b", C.c_void_p), ("w_pool", C.c_void_p), ("b_pool", C.c_void_p),
         ("attn_l", C.c_void_p), ("attn_r", C.c_void_p), ("w_e", C.c_void_p), ("b_e", C.c_void_p),
         ("w_ih", C.c_void_p), ("b_ih", C.c_void_p), ("w_hh", C.c_void_p), ("b_hh", C.c_void_p),
+        ("hidden", C.c_int32),
     ]
 
 
@@ -123,6 +125,9 @@ def lib():
         "saga_unfused_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64, P(C.c_size_t)]),
         "saga_scatter_gather_unfused": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs), saga_mat,
                                             C.c_void_p, C.c_size_t, C.c_void_p]),
+        "saga_lstm_gather_workspace_size": (S, [P(saga_plan), C.c_int64, P(C.c_size_t)]),
+        "saga_lstm_gather": (S, [P(saga_plan), saga_cmat, saga_cmat, saga_mat, C.c_void_p, C.c_size_t,
+                                 C.c_void_p]),
         "saga_apply_vertex_workspace_size": (S, [P(saga_gemm_op), C.c_int64, C.c_int64, C.c_int64,
                                                  P(C.c_size_t)]),
         "saga_apply_vertex": (S, [P(saga_gemm_op), saga_cmat, saga_cmat, saga_cmat, saga_cmat, C.c_void_p,
@@ -205,6 +210,18 @@ def saga_scatter_gather_unfused(plan, op, inputs, out, workspace, ws_bytes, stre
     return _check(lib().saga_scatter_gather_unfused(C.byref(plan), C.byref(op), C.byref(inputs), out,
                                                     workspace, ws_bytes, stream),
                   "saga_scatter_gather_unfused")
+
+
+def saga_lstm_gather_workspace_size(plan, hidden):
+    out = C.c_size_t(0)
+    _check(lib().saga_lstm_gather_workspace_size(C.byref(plan), hidden, C.byref(out)),
+           "saga_lstm_gather_workspace_size")
+    return out.value
+
+
+def saga_lstm_gather(plan, gates_x, w_hh, out, workspace, ws_bytes, stream):
+    return _check(lib().saga_lstm_gather(C.byref(plan), gates_x, w_hh, out, workspace, ws_bytes, stream),
+                  "saga_lstm_gather")
 
 
 def saga_apply_vertex_workspace_size(op, k, k2, n):

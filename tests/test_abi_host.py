@@ -150,6 +150,27 @@ def test_unfused_rejects_bad_arguments(S):
     assert call(o=gated) == S.SAGA_EUNSUPPORTED
 
 
+def test_lstm_gather_rejects_bad_arguments(S):
+    p = _fake_plan(S)
+    L = S.lib()
+    gx = S.saga_cmat(0x50000, 16, 512, 512)
+    whh = S.saga_cmat(0x90000, 128, 512, 512)
+    out = S.saga_mat(0x100000, 16, 128, 128)
+
+    def call(g=gx, w=whh, o=out, ws=0x900000, nb=256):
+        return L.saga_lstm_gather(C.byref(p), g, w, o, ws, nb, None)
+
+    assert S.saga_lstm_gather_workspace_size(p, 128) == 256
+    assert L.saga_lstm_gather_workspace_size(C.byref(p), 100, C.byref(C.c_size_t())) == S.SAGA_EUNSUPPORTED
+    assert call(w=S.saga_cmat(0x90000, 100, 400, 400)) == S.SAGA_EUNSUPPORTED    # H = 100
+    assert call(g=S.saga_cmat(0x50000, 15, 512, 512)) == S.SAGA_EINVAL           # rows != num_src
+    assert call(g=S.saga_cmat(0x50000, 16, 256, 256)) == S.SAGA_EINVAL           # not 4H columns
+    assert call(o=S.saga_mat(0x100000, 16, 64, 64)) == S.SAGA_EINVAL             # not H columns
+    assert call(nb=8) == S.SAGA_EWORKSPACE
+    assert call(ws=0x900010) == S.SAGA_EINVAL                                   # misaligned
+    assert call(o=S.saga_mat(0x50000 + 256, 16, 128, 128)) == S.SAGA_EINVAL      # overlaps gates_x
+
+
 def test_gemm_rejects_bad_arguments(S):
     L = S.lib()
     op = S.saga_gemm_op(S.SAGA_F32, S.SAGA_GEMM_PLAIN, 0, None)
