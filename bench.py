@@ -252,6 +252,7 @@ SUITE = [  # the other workloads, one model each (Table I models at their config
     ("gat_ba", "2-layer GAT, BA(20000, m=5) symmetrised + self-loops, 512->8x8->8x8 (mean)"),
     ("sage_rmat", "GraphSAGE-pool, R-MAT scale 17, 16 edges/vertex, 256->256"),
     ("gated_rgg", "gated edge MPNN + GRU, torus RGG(100000, expected degree 12), 64 (+16 edge)"),
+    ("sage_lstm", "GraphSAGE-LSTM, R-MAT scale 17, 16 edges/vertex, 256 -> LSTM 128 -> 256"),
 ]
 
 
@@ -265,7 +266,7 @@ def _padded(a, torch, dev):
     return t[:, :f]
 
 
-def _oracle_model(name, g):
+def _oracle_model(name, g, rows=None):
     from oracle import saga_oracle as O
 
     if name == "gcn_er":
@@ -274,13 +275,16 @@ def _oracle_model(name, g):
         return O.gat_2layer(g)
     if name == "sage_rmat":
         return O.sage_layer_of(g)
+    if name == "sage_lstm":
+        return O.sage_lstm_layer_of(g, rows=rows)
     return O.gated_layer_of(g)
 
 
 def suite(dev, reps=10, oracle=True):
-    """Per-workload, per-layer timing of the other four workloads through
+    """Per-workload, per-layer timing of the other five workloads through
     saga_layer (plan built once per graph and timed separately); with
     `oracle`, the oracle's whole model on the same inputs, one thread."""
+    import numpy as np
     import torch
 
     import paper_2009_00804_amd.layers as LY
@@ -302,6 +306,8 @@ def suite(dev, reps=10, oracle=True):
             model, x, ef = LY.gat2(graph, g), _padded(g["X"], torch, dev), None
         elif name == "sage_rmat":
             model, x, ef = LY.sage_pool(graph, g), _padded(g["X"], torch, dev), None
+        elif name == "sage_lstm":
+            model, x, ef = LY.sage_lstm(graph, g), _padded(g["X"], torch, dev), None
         else:
             model = LY.gated_gru(graph, g)
             x, ef = _padded(g["H"], torch, dev), _padded(g["E_feat"], torch, dev)
@@ -337,15 +343,26 @@ def suite(dev, reps=10, oracle=True):
                         "vertices_per_s": V / (ms * 1e-3)} for ms in per]}
         log(f"suite {name}: V={V} E={E} plan {out[name]['plan_ms']:.3f} ms, layers "
             + ", ".join(f"{ms:.3f} ms" for ms in per))
+        if name == "sage_lstm":
+            # the recurrence of the longest row is the layer's critical path
+            dmax = int(np.diff(g["row_ptr"]).max())
+            out[name]["max_in_degree"] = dmax
+            out[name]["lstm_us_per_step_of_longest_row"] = per[0] * 1e3 / dmax
         if oracle:
             from threadpoolctl import threadpool_limits
 
+            rows, e_s, sample = None, E, "whole model, float64"
+            if name == "sage_lstm":
+                # the oracle's recurrence runs step by step: a bounded random sample of rows
+                rows = np.random.default_rng(7).choice(V, 1500, replace=False)
+                e_s = int(np.diff(g["row_ptr"])[rows].sum())
+                sample = f"layer on {len(rows)} random destination rows ({e_s} in-edges), float64"
             with threadpool_limits(1):
                 t0 = time.perf_counter()
-                _oracle_model(name, g)
+                _oracle_model(name, g, rows=rows)
                 t = time.perf_counter() - t0
-            out[name]["cpu_oracle"] = {"ms": t * 1e3, "edges_per_s": len(per) * E / t, "cores": 1,
-                                       "kind": "oracle", "sample": "whole model, float64"}
+            out[name]["cpu_oracle"] = {"ms": t * 1e3, "edges_per_s": len(per) * e_s / t, "cores": 1,
+                                       "kind": "oracle", "sample": sample}
             log(f"suite {name}: oracle {t:.2f} s")
         del model, graph
         torch.cuda.empty_cache()
@@ -399,7 +416,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-suite", action="store_true",
-                    help="skip the per-layer timing of the four smaller workloads")
+                    help="skip the per-layer timing of the five smaller workloads")
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip the fused-vs-unfused layer-1 aggregation comparison")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
