@@ -49,6 +49,15 @@ notes of the repository):
      [i|f|g|o] = x_t W_ih + b_ih + h W_hh + b_hh, c = f*c + i*g,
      h = o*tanh(c), with i, f, o sigmoids and g a tanh.  Then
      y_v = [x_v | a_v] W + b, no activation.
+  R9 R-GCN (Table I, R-GCN row: Scatter takes the edge and its source,
+     ApplyEdge is a per-edge MLP, Gather sums the in-edges and adds the
+     vertex itself, ApplyVertex is a sum; Sec. 3.2 "ApplyEdge": every edge
+     carries a type, and the edges of one type share one transform).  Each
+     relation r has a weight W_r; the message of an in-edge u -> v of type r
+     is x_u W_r / c(v, r), where c(v, r) counts the in-edges of v of type r
+     (the per-relation mean of the relational GCN); the vertex's own term is
+     x_v W_self; y_v = act(b + x_v W_self + sum of the messages).  The edge
+     types are an int32 array aligned with the CSR entries.
 """
 from __future__ import annotations
 
@@ -491,3 +500,97 @@ def sage_lstm_layer(row_ptr, col_idx, X, W_ih, b_ih, W_hh, b_hh, W, b, rows=None
 def sage_lstm_layer_of(g, rows=None):
     return sage_lstm_layer(g["row_ptr"], g["col_idx"], g["X"], g["W_ih"], g["b_ih"], g["W_hh"],
                            g["b_hh"], g["W"], g["b"], rows=rows)
+
+
+# ==========================================================================
+# R-GCN: typed edges (Table I, R-GCN row; Sec. 3.2 "ApplyEdge"; reading R9)
+# ==========================================================================
+
+
+def relation_counts(row_ptr, etype, num_rel, rows=None):
+    """c[i, r]: number of in-edges of destination rows[i] whose type is r."""
+    rp = np.asarray(row_ptr, dtype=np.int64)
+    et = np.asarray(etype, dtype=np.int64)
+    rows = _rows_arg(rows, rp.shape[0] - 1)
+    c = np.zeros((rows.shape[0], num_rel), dtype=np.int64)
+    for i, v in enumerate(rows):
+        np.add.at(c[i], et[rp[v]:rp[v + 1]], 1)
+    return c
+
+
+def rel_gather(row_ptr, col_idx, etype, X, num_rel, rows=None):
+    """Per destination v and relation r, the mean of the source rows over
+    v's in-edges of type r: A[i, r] = (1 / c(v, r)) sum x_u; 0 where
+    c(v, r) = 0.  Returns len(rows) x num_rel x F float64."""
+    rp = np.asarray(row_ptr, dtype=np.int64)
+    col = np.asarray(col_idx, dtype=np.int64)
+    et = np.asarray(etype, dtype=np.int64)
+    rows = _rows_arg(rows, rp.shape[0] - 1)
+    X = np.asarray(X)
+    A = np.zeros((rows.shape[0], num_rel, X.shape[1]), dtype=np.float64)
+    for i, v in enumerate(rows):
+        for e in range(rp[v], rp[v + 1]):
+            A[i, et[e]] += _f64(X[col[e]])
+    c = relation_counts(row_ptr, etype, num_rel, rows=rows)
+    nz = c > 0
+    A[nz] /= c[nz][:, None]
+    return A
+
+
+def rgcn_layer(row_ptr, col_idx, etype, X, W_rel, W_self, b, act="none", rows=None):
+    """R-GCN layer, aggregate first per relation (reading R9):
+    y_v = act(b + x_v W_self + sum_r A[v, r] W_r), W_rel[r] = W_r (F_in x
+    F_out)."""
+    rows = _rows_arg(rows, len(row_ptr) - 1)
+    W_rel = _f64(W_rel)
+    A = rel_gather(row_ptr, col_idx, etype, X, W_rel.shape[0], rows=rows)
+    Y = dense(X[rows], W_self, bias=b)
+    for r in range(W_rel.shape[0]):
+        Y = Y + dense(A[:, r, :], W_rel[r])
+    return ACTS[act](Y)
+
+
+def rgcn_layer_of(g, rows=None):
+    return rgcn_layer(g["row_ptr"], g["col_idx"], g["etype"], g["X"], g["W_rel"], g["W_self"],
+                      g["b"], act=g.get("act", "none"), rows=rows)
+
+
+def rel_layout(row_ptr, col_idx, etype, num_rel, tile):
+    """The library's typed layout (its own definition, compared bit for bit).
+
+    The per-edge transform x_u W_r depends only on the (relation, source)
+    pair, so it is computed once per distinct pair.  Pairs are numbered
+    relation by relation, sources ascending within a relation; the pair
+    range of relation r starts at rel_ptr[r], a multiple of ``tile``, and is
+    padded with -1 up to the next one.  Returns a dict:
+      rel_count[r]  distinct sources of relation r
+      rel_ptr[r]    first pair row of relation r (rel_ptr[num_rel] = total)
+      pair_src[q]   source vertex of pair row q, -1 in the padding
+      edge_pair[e]  pair row of CSR entry e
+      edge_norm[e]  float32(1 / c(v, r)) for CSR entry e = u -> v of type r
+    """
+    rp = np.asarray(row_ptr, dtype=np.int64)
+    col = np.asarray(col_idx, dtype=np.int64)
+    et = np.asarray(etype, dtype=np.int64)
+    srcs = [np.unique(col[et == r]) for r in range(num_rel)]
+    rel_count = np.array([s.shape[0] for s in srcs], dtype=np.int64)
+    rel_ptr = np.zeros(num_rel + 1, dtype=np.int64)
+    np.cumsum((rel_count + tile - 1) // tile * tile, out=rel_ptr[1:])
+    pair_src = np.full(rel_ptr[-1], -1, dtype=np.int64)
+    for r in range(num_rel):
+        pair_src[rel_ptr[r]:rel_ptr[r] + rel_count[r]] = srcs[r]
+    edge_pair = np.zeros(col.shape[0], dtype=np.int64)
+    for r in range(num_rel):
+        m = et == r
+        edge_pair[m] = rel_ptr[r] + np.searchsorted(srcs[r], col[m])
+    c = np.zeros(col.shape[0], dtype=np.int64)
+    for v in range(rp.shape[0] - 1):
+        t = et[rp[v]:rp[v + 1]]
+        if t.shape[0]:
+            cnt = np.bincount(t, minlength=num_rel)
+            c[rp[v]:rp[v + 1]] = cnt[t]
+    edge_norm = np.zeros(col.shape[0], dtype=np.float32)
+    nz = c > 0
+    edge_norm[nz] = (1.0 / c[nz]).astype(np.float32)
+    return dict(rel_count=rel_count, rel_ptr=rel_ptr, pair_src=pair_src, edge_pair=edge_pair,
+                edge_norm=edge_norm)

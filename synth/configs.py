@@ -18,6 +18,11 @@ Workloads (the paper's dataset shapes are stood in for by these graphs):
   gcn_rmat    2-layer GCN, R-MAT scale 21, 50 edges per vertex, relabelled
               + self-loops, features 602 N(0,1), 602->128->41, float32 and
               bfloat16 storage variants.
+  sage_lstm   GraphSAGE with the LSTM Gather on the sage_rmat graph and
+              features, hidden 128, output 256.
+  rgcn_rmat   R-GCN layer (typed edges), R-MAT scale 18, 16 edges per
+              vertex, relabelled, 32 relation types drawn per edge with
+              P(r) proportional to 1/(r+1), features 128 N(0,1) -> 64, ReLU.
 """
 from __future__ import annotations
 
@@ -163,6 +168,32 @@ def gcn_rmat(scale=21, avg_deg=50, f_in=602, hidden=128, f_out=41, key=5,
     return d
 
 
+def rgcn_rmat(scale=18, avg_deg=16, num_rel=32, f_in=128, f_out=64, key=7):
+    """R-GCN layer on a typed power-law graph.  The edge type (stream 2, the
+    edge-attribute stream) is drawn per edge, independently of its
+    endpoints, with P(r) proportional to 1 / (r + 1); ``etype`` is aligned
+    with the CSR entries."""
+    n = 1 << scale
+    E = avg_deg * n
+    src, dst = G.rmat(scale, E, *RMAT_ABC, key=(key, 0))
+    perm = G.rng_for(key, 4).permutation(n).astype(np.int32)
+    src, dst = G.relabel(src, dst, perm)
+    p = 1.0 / np.arange(1, num_rel + 1, dtype=np.float64)
+    et = G.rng_for(key, 2).choice(num_rel, E, p=p / p.sum()).astype(np.int32)
+    d = _csr_dict("rgcn_rmat", n, src, dst, want_eid=True)
+    d["etype"] = et[d.pop("eid")]
+    d["model"] = "rgcn"
+    d["num_rel"] = num_rel
+    d["X"] = T.normal_matrix(n, f_in, (key, 1))
+    rw = G.rng_for(key, 3)
+    d["W_rel"] = np.stack([T.glorot(f_in, f_out, rw) for _ in range(num_rel)])
+    d["W_self"] = T.glorot(f_in, f_out, rw)
+    d["b"] = T.bias(f_in, f_out, rw)
+    d["act"] = "relu"
+    d["dims"] = (f_in, f_out)
+    return d
+
+
 def add_bf16_variant(d):
     """bfloat16 storage of X and the weights (round to nearest even); the
     float32 arrays ``X_bf``, ``W1_bf``, ``W2_bf`` hold their exact values."""
@@ -183,6 +214,7 @@ BUILDERS = {
     "gated_rgg": gated_rgg,
     "gcn_rmat": gcn_rmat,
     "sage_lstm": sage_lstm,
+    "rgcn_rmat": rgcn_rmat,
 }
 
 # scaled variants used by parity tests (K + 100 seeds)
@@ -193,6 +225,7 @@ SMALL = {
     "gated_rgg": dict(n=8000, key=104),
     "gcn_rmat": dict(scale=13, avg_deg=50, key=105),
     "sage_lstm": dict(scale=10, key=106, graph_key=106),
+    "rgcn_rmat": dict(scale=11, key=107),
 }
 
 
