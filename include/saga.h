@@ -21,6 +21,12 @@
  *                                   baseline of Fig. 7a)
  *   saga_lstm_gather                GraphSAGE's LSTM Gather: a recurrence
  *                                   along each row's in-edges
+ *   saga_rel_plan_build             typed-edge layout of R-GCN: the distinct
+ *                                   (relation, source) pairs, grouped by
+ *                                   relation, and per-edge pair rows / norms
+ *   saga_rel_transform              R-GCN ApplyEdge on the matrix cores: one
+ *                                   grouped GEMM, every pair's source row
+ *                                   times its relation's weight
  *   saga_apply_vertex               dense per-vertex transform on the matrix
  *                                   cores, with fused epilogues (Sec. 3.2
  *                                   "ApplyVertex", Table III)
@@ -28,7 +34,7 @@
  *
  * Conventions (all entry points):
  *   - Every pointer argument except the host-side structs (saga_plan_opts,
- *     saga_plan, saga_edge_op, saga_edge_inputs, saga_gemm_op,
+ *     saga_plan, saga_rel_plan, saga_edge_op, saga_edge_inputs, saga_gemm_op,
  *     saga_layer_desc) is a DEVICE pointer.  The caller allocates, owns and
  *     frees all device memory; the library allocates nothing, ever.  Scratch
  *     space comes from a caller-provided workspace whose size the matching
@@ -88,7 +94,8 @@ typedef enum saga_msg {
   SAGA_MSG_COPY = 0,      /* message of edge u->v = src row u              */
   SAGA_MSG_SRC_NORM = 1,  /* src row u * d_out(u)^-1/2  (GCN normalisation) */
   SAGA_MSG_GAT = 2,       /* score LeakyReLU(el[u,k] + er[v,k]); SOFTMAX only */
-  SAGA_MSG_GATED = 3      /* sigmoid(gs[u] + gd[v] + b_e + e_uv W_ee) * src[u] */
+  SAGA_MSG_GATED = 3,     /* sigmoid(gs[u] + gd[v] + b_e + e_uv W_ee) * src[u] */
+  SAGA_MSG_TYPED = 4      /* R-GCN: edge_norm[e] * src[edge_pair[e]] (rel plan) */
 } saga_msg;
 
 typedef enum saga_act {
@@ -204,6 +211,95 @@ saga_status saga_plan_build(int32_t num_dst, int32_t num_src, int64_t num_edges,
 saga_status saga_plan_check(const saga_plan* plan, void* stream, saga_plan_counts* counts);
 
 /* ======================================================================
+ * Typed edges (R-GCN)
+ * ======================================================================
+ * Table I, R-GCN row: Scatter takes the edge and its source, ApplyEdge is an
+ * MLP picked by the edge's type, Gather sums the in-edges and adds the
+ * vertex itself.  Sec. 3.2 "ApplyEdge": every edge carries a type attribute,
+ * and the edges of one type are selected and batched into one GEMM.
+ *
+ * etype is int32[num_edges], aligned with the CSR entries, values in
+ * [0, num_rel).  The message of CSR entry e = u -> v of type r is
+ * x_u W_r / c(v, r), where c(v, r) counts the in-edges of v of type r.
+ * x_u W_r depends only on the pair (r, u), so it is computed once per
+ * distinct pair.  The rel plan holds, on the device:
+ *   rel_count[r]  number of distinct sources of relation r
+ *   rel_ptr[r]    first pair row of relation r: rel_ptr[0] = 0,
+ *                 rel_ptr[r+1] = rel_ptr[r] + rel_count[r] rounded up to a
+ *                 multiple of SAGA_REL_TILE (int32[num_rel + 1])
+ *   pair_src[q]   source vertex of pair row q: the sources of relation r in
+ *                 ascending order at rows rel_ptr[r] .. rel_ptr[r] +
+ *                 rel_count[r] - 1, then -1 up to rel_ptr[r+1]
+ *                 (int32[max_pairs]; rows from rel_ptr[num_rel] on unused)
+ *   edge_pair[e]  pair row of (etype[e], col_idx[e])      (int32[num_edges])
+ *   edge_norm[e]  1 / c(v, etype[e]) in float32, correctly rounded
+ *                                                        (float[num_edges])
+ * All integers are reproducible bit for bit.
+ */
+#define SAGA_REL_TILE 128
+#define SAGA_REL_MAX_RELATIONS 2048
+
+typedef struct saga_rel_plan {
+  int32_t num_rel;
+  int32_t num_src;
+  int64_t num_edges;
+  int64_t max_pairs;          /* rows of pair_src and of a transform output */
+  const int32_t* etype;       /* the caller's array, referenced not copied */
+  const int32_t* plan_counts; /* counters of the plan it was built on */
+  /* device arrays inside the workspace */
+  int32_t* rel_ptr;
+  int32_t* rel_count;
+  int32_t* pair_src;
+  int32_t* edge_pair;
+  float* edge_norm;
+  int32_t* counts;            /* [4]: see saga_rel_counts */
+  void* scratch;
+  size_t scratch_bytes;
+} saga_rel_plan;
+
+typedef struct saga_rel_counts {
+  int64_t pair_rows;          /* rel_ptr[num_rel]: pair rows incl. padding */
+  int64_t pairs;              /* distinct (relation, source) pairs */
+  int32_t error_flags;        /* bit 0: an etype value outside [0, num_rel) */
+} saga_rel_counts;
+
+/* Workspace bytes of saga_rel_plan_build for this plan and relation count.
+ * Errors: SAGA_EINVAL (null, num_rel outside [1, SAGA_REL_MAX_RELATIONS],
+ * more than 2^31 pair rows). */
+saga_status saga_rel_plan_workspace_size(const saga_plan* plan, int32_t num_rel, size_t* bytes);
+
+/* Build the typed layout of a built plan's graph on `stream`.  etype is
+ * referenced (it must stay alive and unchanged while the rel plan is used);
+ * workspace (device, 256-byte aligned, caller-owned) receives every array.
+ * If the plan's CSR was invalid, nothing is computed; an out-of-range etype
+ * is reported by saga_rel_plan_check as SAGA_EGRAPH, and every later call on
+ * this rel plan then leaves its outputs unwritten.  Errors: SAGA_EINVAL,
+ * SAGA_EWORKSPACE, SAGA_EDEVICE. */
+saga_status saga_rel_plan_build(const saga_plan* plan, const int32_t* etype, int32_t num_rel,
+                                void* workspace, size_t workspace_bytes, void* stream,
+                                saga_rel_plan* rel);
+
+/* Synchronise `stream` and read the rel plan's counters; SAGA_EGRAPH if the
+ * plan's CSR or an edge type was invalid. */
+saga_status saga_rel_plan_check(const saga_rel_plan* rel, void* stream, saga_rel_counts* counts);
+
+/* R-GCN ApplyEdge hoisted to the distinct pairs, on the matrix cores:
+ *     out[q] = x[pair_src[q]] w_{r(q)}     for pair rows q < rel_ptr[num_rel]
+ * where r(q) is the relation whose range holds q; padding rows are written
+ * as 0; rows from rel_ptr[num_rel] on are not written.  One grouped GEMM:
+ * each tile of SAGA_REL_TILE rows lies in one relation and uses its weight.
+ * x: num_src x K (dtype, 16-byte rows); w: the num_rel weights stacked,
+ * (num_rel * K) x N (rows r*K .. r*K+K-1 are W_r; dtype); out: max_pairs x
+ * N (dtype).  N <= 4096.  Workspace: saga_rel_transform_workspace_size()
+ * bytes, 256-byte aligned (the packed, transposed weights). */
+saga_status saga_rel_transform_workspace_size(const saga_rel_plan* rel, saga_dtype dtype,
+                                              int64_t k, int64_t n, size_t* bytes);
+
+saga_status saga_rel_transform(const saga_rel_plan* rel, saga_dtype dtype, saga_cmat x,
+                               saga_cmat w, saga_mat out, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* ======================================================================
  * Scatter + ApplyEdge + Gather (fused)
  * ======================================================================
  * For every destination v, reduce the messages of its in-edges (Sec. 3.2
@@ -224,9 +320,15 @@ saga_status saga_plan_check(const saga_plan* plan, void* stream, saga_plan_count
  *          w_edge (Fe x F, dense), gate_bias (F); message of edge e = u->v
  *          is sigmoid(gate_src[u] + gate_dst[v] + gate_bias +
  *          edge_feat[e] w_edge) * h[u] elementwise.  F == 64, Fe <= 16.
+ *   TYPED: rel (a rel plan built on this plan), src = the pair rows of
+ *          saga_rel_transform (rel->max_pairs x F); message of CSR entry e
+ *          is rel->edge_norm[e] * src[rel->edge_pair[e]].
+ * self (optional; COPY, SRC_NORM and TYPED): num_dst x out cols, same dtype,
+ * added before the bias: out[v] = act(post(agg_v) + self[v] + bias).
  * Output: num_dst x F (x F/heads if head_mean), same dtype as src.
  * Supported: COPY/SRC_NORM with SUM/MEAN/MAX in f32 and bf16, GAT with
- * SOFTMAX in f32, GATED with SUM in f32; others give SAGA_EUNSUPPORTED.
+ * SOFTMAX in f32, GATED with SUM in f32, TYPED with SUM in f32 and bf16;
+ * others give SAGA_EUNSUPPORTED.
  */
 typedef struct saga_edge_op {
   saga_msg msg;
@@ -247,6 +349,8 @@ typedef struct saga_edge_inputs {
   const float* w_edge;             /* GATED */
   const float* gate_bias;          /* GATED, nullable */
   const float* bias;               /* nullable, length = output cols */
+  const saga_rel_plan* rel;        /* TYPED */
+  saga_cmat self;                  /* nullable: added to each output row */
 } saga_edge_inputs;
 
 saga_status saga_gather_workspace_size(const saga_plan* plan, const saga_edge_op* op,
@@ -362,15 +466,21 @@ saga_status saga_apply_vertex(const saga_gemm_op* op, saga_cmat a, saga_cmat w,
  * GATED_GRU [S_src, S_dst] = X [W_e,src, W_e,dst]; gated sum-Gather with
  *           W_e,edge and b_e; out = GRU(a, X) with W_ih, W_hh, b_ih, b_hh.
  *           (W_e rows: [0,F) src part, [F,2F) dst part, [2F,2F+Fe) edge.)
+ * RGCN      T = saga_rel_transform(X, W) (W: the num_rel weights stacked,
+ *           (num_rel * F_in) x F_out); S = X W_self + b; typed sum-Gather
+ *           with self = S: out = act(S_v + sum_e edge_norm[e] T[edge_pair[e]])
+ *           (rel: a rel plan of the same graph).
  * Weights are dense device matrices (ld = cols) in the layer dtype; biases
  * and attention vectors f32.  x: num_src x F_in (num_src == num_dst).
+ * act applies to GCN, GAT and RGCN.
  */
 typedef enum saga_layer_kind {
   SAGA_LAYER_GCN = 0,
   SAGA_LAYER_GAT = 1,
   SAGA_LAYER_SAGE_POOL = 2,
   SAGA_LAYER_GATED_GRU = 3,
-  SAGA_LAYER_SAGE_LSTM = 4
+  SAGA_LAYER_SAGE_LSTM = 4,
+  SAGA_LAYER_RGCN = 5
 } saga_layer_kind;
 
 typedef struct saga_layer_desc {
@@ -379,7 +489,7 @@ typedef struct saga_layer_desc {
   int32_t in_feat, out_feat;
   int32_t heads, head_mean;       /* GAT */
   float neg_slope;                /* GAT */
-  saga_act act;                   /* GCN, GAT */
+  saga_act act;                   /* GCN, GAT, RGCN */
   int32_t edge_feat;              /* GATED_GRU: Fe */
   const void* w;  const float* b;             /* GCN, GAT, SAGE_POOL */
   const void* w_pool; const float* b_pool;    /* SAGE_POOL */
@@ -388,6 +498,8 @@ typedef struct saga_layer_desc {
   const float* w_ih; const float* b_ih;       /* GATED_GRU: F x 3F, 3F; SAGE_LSTM: F x 4H, 4H */
   const float* w_hh; const float* b_hh;       /* GATED_GRU: F x 3F;  SAGE_LSTM: H x 4H, 4H */
   int32_t hidden;                             /* SAGE_LSTM: H (32, 64 or 128) */
+  const void* w_self;                         /* RGCN: F_in x F_out (w: stacked W_r) */
+  const saga_rel_plan* rel;                   /* RGCN */
 } saga_layer_desc;
 
 saga_status saga_layer_workspace_size(const saga_plan* plan, const saga_layer_desc* desc,

@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsaga.so")
-SOURCES = ["abi.hip", "plan.hip", "gather.hip", "gemm.hip", "lstm.hip"]
+SOURCES = ["abi.hip", "plan.hip", "gather.hip", "gemm.hip", "lstm.hip", "rel.hip"]
 
 
 def hipcc() -> str:

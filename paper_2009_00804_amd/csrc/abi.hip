@@ -96,6 +96,15 @@ saga_status check_plan(const saga_plan* p) {
   return SAGA_OK;
 }
 
+saga_status check_rel(const saga_plan& p, const saga_rel_plan* r) {
+  if (!r) return fail(SAGA_EINVAL, "rel plan is null");
+  if (!r->counts || !r->rel_ptr || !r->pair_src || !r->edge_pair || !r->edge_norm)
+    return fail(SAGA_EINVAL, "rel plan is not built");
+  if (r->plan_counts != p.counts || r->num_edges != p.num_edges || r->num_src != p.num_src)
+    return fail(SAGA_EINVAL, "rel plan was built on another plan");
+  return SAGA_OK;
+}
+
 // bump allocator over a caller workspace
 struct Carve {
   char* base;
@@ -146,7 +155,14 @@ saga_status validate_edge_op(const saga_plan& p, const saga_edge_op& op,
   if (F <= 0) return fail(SAGA_EINVAL, "src: no feature columns");
   if (F > (op.dtype == SAGA_BF16 ? 1024 : 512))
     return fail(SAGA_EUNSUPPORTED, "feature width %lld too large", (long long)F);
-  saga_status s = check_mat(in.src.ptr, in.src.rows, in.src.cols, in.src.ld, p.num_src, F, es, true, "src");
+  int64_t src_rows = p.num_src;
+  if (op.msg == SAGA_MSG_TYPED) {
+    saga_status s0 = check_rel(p, in.rel);
+    if (s0) return s0;
+    if (op.reduce != SAGA_RED_SUM) return fail(SAGA_EUNSUPPORTED, "TYPED messages need SUM");
+    src_rows = in.rel->max_pairs;
+  }
+  saga_status s = check_mat(in.src.ptr, in.src.rows, in.src.cols, in.src.ld, src_rows, F, es, true, "src");
   if (s) return s;
   int64_t out_cols = F;
   switch (op.msg) {
@@ -186,11 +202,23 @@ saga_status validate_edge_op(const saga_plan& p, const saga_edge_op& op,
       if (!in.w_edge) return fail(SAGA_EINVAL, "w_edge is null");
       break;
     }
+    case SAGA_MSG_TYPED:
+      break;  // src and rel are checked above
     default:
       return fail(SAGA_EINVAL, "bad message kind");
   }
   s = check_mat(out.ptr, out.rows, out.cols, out.ld, p.num_dst, out_cols, es, true, "out");
   if (s) return s;
+  if (in.self.ptr) {
+    if (op.msg != SAGA_MSG_COPY && op.msg != SAGA_MSG_SRC_NORM && op.msg != SAGA_MSG_TYPED)
+      return fail(SAGA_EUNSUPPORTED, "self term: COPY, SRC_NORM or TYPED messages only");
+    s = check_mat(in.self.ptr, in.self.rows, in.self.cols, in.self.ld, p.num_dst, out_cols, es,
+                  false, "self");
+    if (s) return s;
+    if (range_overlap(out.ptr, mat_bytes(out.rows, out.cols, out.ld, es), in.self.ptr,
+                      mat_bytes(in.self.rows, in.self.cols, in.self.ld, es)))
+      return fail(SAGA_EINVAL, "output overlaps self");
+  }
   const size_t ob = mat_bytes(out.rows, out.cols, out.ld, es);
   const void* ins[] = {in.src.ptr, in.el.ptr, in.er.ptr, in.gate_src.ptr, in.gate_dst.ptr,
                        in.edge_feat.ptr, p.row_ptr, p.col_idx};
@@ -242,6 +270,13 @@ saga_status run_gather(const saga_plan& p, const saga_edge_op& op, const saga_ed
   a.w_edge = in.w_edge;
   a.gate_bias = in.gate_bias;
   a.bias = in.bias;
+  a.self = in.self.ptr;
+  a.ld_self = in.self.ld;
+  if (op.msg == SAGA_MSG_TYPED) {
+    a.col_idx = in.rel->edge_pair;
+    a.edge_scale = in.rel->edge_norm;
+    a.err2 = in.rel->counts + saga::kRelErr;
+  }
   a.out = out.ptr;
   a.ld_out = out.ld;
   a.partial = static_cast<float*>(ws);
@@ -475,6 +510,60 @@ saga_status run_lstm(const saga_plan& p, const saga_cmat& gx, const saga_cmat& w
   return ok();
 }
 
+// ---------------------------------------------------------------------------
+// R-GCN: per-relation transform of the distinct (relation, source) pairs
+// ---------------------------------------------------------------------------
+saga_status run_rel_transform(const saga_rel_plan& r, saga_dtype dtype, const saga_cmat& x,
+                              const saga_cmat& w, const saga_mat& out, void* ws, size_t ws_bytes,
+                              hipStream_t st) {
+  if (dtype != SAGA_F32 && dtype != SAGA_BF16) return fail(SAGA_EINVAL, "bad dtype");
+  const size_t es = esize(dtype);
+  const int64_t K = x.cols, N = w.cols, R = r.num_rel;
+  if (K <= 0 || N <= 0) return fail(SAGA_EINVAL, "rel transform: empty operand");
+  if (N > 4096) return fail(SAGA_EUNSUPPORTED, "rel transform: N too large");
+  saga_status s = check_mat(x.ptr, x.rows, x.cols, x.ld, r.num_src, K, es, true, "x");
+  if (s) return s;
+  s = check_mat(w.ptr, w.rows, w.cols, w.ld, R * K, N, es, false, "w");
+  if (s) return s;
+  s = check_mat(out.ptr, out.rows, out.cols, out.ld, r.max_pairs, N, es, false, "out");
+  if (s) return s;
+  const size_t need = saga::gemm_grouped_workspace_bytes(dtype, (int)R, N, K);
+  if (!ws || ws_bytes < need)
+    return fail(SAGA_EWORKSPACE, "rel transform workspace: need %zu bytes, got %zu", need, ws_bytes);
+  if ((uintptr_t)ws % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
+  const size_t ob = mat_bytes(out.rows, out.cols, out.ld, es);
+  const size_t xb = mat_bytes(x.rows, x.cols, x.ld, es), wb = mat_bytes(w.rows, w.cols, w.ld, es);
+  if (range_overlap(out.ptr, ob, x.ptr, xb) || range_overlap(out.ptr, ob, w.ptr, wb) ||
+      range_overlap(out.ptr, ob, ws, need))
+    return fail(SAGA_EINVAL, "output overlaps an input or the workspace");
+  if (range_overlap(ws, need, x.ptr, xb) || range_overlap(ws, need, w.ptr, wb))
+    return fail(SAGA_EINVAL, "workspace overlaps an argument");
+  if (r.max_pairs == 0) return ok();
+  saga::GemmArgs g;
+  memset(&g, 0, sizeof(g));
+  g.dtype = dtype;
+  g.mode = SAGA_GEMM_PLAIN;
+  g.M = r.max_pairs;
+  g.N = N;
+  g.K = K;
+  g.a = x.ptr;
+  g.lda = x.ld;
+  g.w = w.ptr;
+  g.ldw = w.ld;
+  g.out = out.ptr;
+  g.ldo = out.ld;
+  g.ws = ws;
+  g.ws_bytes = ws_bytes;
+  g.arow = r.pair_src;
+  g.grp_ptr = r.rel_ptr;
+  g.groups = (int)R;
+  g.err1 = r.plan_counts + saga::kErrFlags;
+  g.err2 = r.counts + saga::kRelErr;
+  hipError_t e = saga::launch_gemm_grouped(g, st);
+  if (e != hipSuccess) return dev_fail(e, "rel transform launch");
+  return ok();
+}
+
 saga_status layer_check_desc(const saga_plan& p, const saga_layer_desc& d) {
   if (p.num_dst != p.num_src) return fail(SAGA_EINVAL, "layers need num_src == num_dst");
   if (d.in_feat <= 0 || d.out_feat <= 0) return fail(SAGA_EINVAL, "layer feature sizes must be > 0");
@@ -498,6 +587,12 @@ saga_status layer_check_desc(const saga_plan& p, const saga_layer_desc& d) {
       if (d.hidden != 32 && d.hidden != 64 && d.hidden != 128)
         return fail(SAGA_EUNSUPPORTED, "SAGE-LSTM: hidden must be 32, 64 or 128");
       break;
+    case SAGA_LAYER_RGCN: {
+      if (!d.w || !d.w_self) return fail(SAGA_EINVAL, "RGCN: null weights");
+      saga_status s = check_rel(p, d.rel);
+      if (s) return s;
+      break;
+    }
     case SAGA_LAYER_GATED_GRU:
       if (d.dtype != SAGA_F32) return fail(SAGA_EUNSUPPORTED, "gated layer is float32 only");
       if (!d.w_e || !d.w_ih || !d.w_hh) return fail(SAGA_EINVAL, "gated: null weights");
@@ -574,6 +669,15 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
       op.reduce = SAGA_RED_SUM;
       gfeat = 0;
       break;
+    case SAGA_LAYER_RGCN:
+      // T: the pair rows (rel transform); S = X W_self + b (the self term)
+      b->ldz = ld_for(d.out_feat, t);
+      b->z = c.take((size_t)d.rel->max_pairs * b->ldz * es);
+      b->ldz2 = ld_for(d.out_feat, t);
+      b->z2 = c.take((size_t)V * b->ldz2 * es);
+      op.reduce = SAGA_RED_SUM;
+      gfeat = d.out_feat;
+      break;
     case SAGA_LAYER_GATED_GRU:
       b->ldz = ld_for(d.in_feat, t);
       b->z = c.take((size_t)V * b->ldz * es);
@@ -623,6 +727,10 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
       gb = std::max(gb, gemm_ws_bytes(g, Fi, d.hidden, Fo));
       break;
     }
+    case SAGA_LAYER_RGCN:
+      gb = std::max(gemm_ws_bytes(g, Fi, 0, Fo),
+                    saga::gemm_grouped_workspace_bytes(t, d.rel->num_rel, Fo, Fi));
+      break;
   }
   b->gws_bytes = gb;
   b->gws = c.take(gb);
@@ -745,6 +853,24 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       return run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, H, b.ldz2},
                       saga_cmat{w + (size_t)Fi * Fo * 4, H, Fo, Fo}, d.b, nullptr, out, b.gws,
                       b.gws_bytes, st);
+    }
+    case SAGA_LAYER_RGCN: {
+      // T = pair rows x_u W_r; S = X W_self + b; out = act(S_v + sum_e norm_e T[pair_e])
+      const saga_rel_plan& r = *d.rel;
+      s = run_rel_transform(r, d.dtype, x, saga_cmat{d.w, r.num_rel * Fi, Fo, Fo},
+                            saga_mat{b.z, r.max_pairs, Fo, b.ldz}, b.gws, b.gws_bytes, st);
+      if (s) return s;
+      g.mode = SAGA_GEMM_PLAIN;
+      s = run_gemm(g, x, saga_cmat{d.w_self, Fi, Fo, Fo}, none, none, d.b, nullptr,
+                   saga_mat{b.z2, V, Fo, b.ldz2}, b.gws, b.gws_bytes, st);
+      if (s) return s;
+      op.msg = SAGA_MSG_TYPED;
+      op.reduce = SAGA_RED_SUM;
+      op.act = d.act;
+      in.src = saga_cmat{b.z, r.max_pairs, Fo, b.ldz};
+      in.rel = &r;
+      in.self = saga_cmat{b.z2, V, Fo, b.ldz2};
+      return run_gather(p, op, in, out, b.part, b.part_bytes, st);
     }
     case SAGA_LAYER_GATED_GRU: {
       const int64_t F = Fi, Fe = d.edge_feat;
@@ -972,6 +1098,116 @@ saga_status saga_lstm_gather(const saga_plan* plan, saga_cmat gates_x, saga_cmat
     if (plan->num_dst == 0) return ok();
     return run_lstm(*plan, gates_x, w_hh, out, workspace, workspace_bytes,
                     static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_rel_plan_workspace_size(const saga_plan* plan, int32_t num_rel, size_t* bytes) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!bytes) return fail(SAGA_EINVAL, "bytes is null");
+    saga::RelLayout L;
+    if (!saga::rel_layout(plan->num_src, plan->num_edges, num_rel, &L))
+      return fail(SAGA_EINVAL, "num_rel must be in [1, %d] and pair rows below 2^31",
+                  saga::kRelMaxRelations);
+    *bytes = L.total;
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_rel_plan_build(const saga_plan* plan, const int32_t* etype, int32_t num_rel,
+                                void* workspace, size_t workspace_bytes, void* stream,
+                                saga_rel_plan* rel) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!rel) return fail(SAGA_EINVAL, "rel is null");
+    if (plan->num_edges > 0 && !etype) return fail(SAGA_EINVAL, "etype is null");
+    saga::RelLayout L;
+    if (!saga::rel_layout(plan->num_src, plan->num_edges, num_rel, &L))
+      return fail(SAGA_EINVAL, "num_rel must be in [1, %d] and pair rows below 2^31",
+                  saga::kRelMaxRelations);
+    if (!workspace || workspace_bytes < L.total)
+      return fail(SAGA_EWORKSPACE, "rel plan workspace: need %zu bytes, got %zu", L.total,
+                  workspace_bytes);
+    if ((uintptr_t)workspace % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
+    if (range_overlap(workspace, L.total, etype, (size_t)plan->num_edges * 4))
+      return fail(SAGA_EINVAL, "workspace overlaps etype");
+    char* w = static_cast<char*>(workspace);
+    saga_rel_plan r;
+    memset(&r, 0, sizeof(r));
+    r.num_rel = num_rel;
+    r.num_src = plan->num_src;
+    r.num_edges = plan->num_edges;
+    r.max_pairs = L.max_pairs;
+    r.etype = etype;
+    r.plan_counts = plan->counts;
+    r.rel_ptr = reinterpret_cast<int32_t*>(w + L.off_rel_ptr);
+    r.rel_count = reinterpret_cast<int32_t*>(w + L.off_rel_count);
+    r.pair_src = reinterpret_cast<int32_t*>(w + L.off_pair_src);
+    r.edge_pair = reinterpret_cast<int32_t*>(w + L.off_edge_pair);
+    r.edge_norm = reinterpret_cast<float*>(w + L.off_edge_norm);
+    r.counts = reinterpret_cast<int32_t*>(w + L.off_counts);
+    r.scratch = w + L.off_scratch;
+    r.scratch_bytes = L.scratch_bytes;
+    hipError_t e = saga::launch_rel_build(*plan, r, L, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return dev_fail(e, "rel plan launch");
+    *rel = r;
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_rel_plan_check(const saga_rel_plan* rel, void* stream, saga_rel_counts* counts) {
+  try {
+    if (!rel || !rel->counts || !rel->plan_counts) return fail(SAGA_EINVAL, "rel plan is not built");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    int32_t h[saga::kRelCountSlots], pc[saga::kCountSlots];
+    hipError_t e = hipMemcpyAsync(h, rel->counts, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(pc, rel->plan_counts, sizeof(pc), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return dev_fail(e, "rel plan check");
+    if (counts) {
+      counts->pair_rows = h[saga::kRelRows];
+      counts->pairs = h[saga::kRelPairs];
+      counts->error_flags = h[saga::kRelErr];
+    }
+    if (pc[saga::kErrFlags]) return fail(SAGA_EGRAPH, "the plan's CSR is invalid");
+    if (h[saga::kRelErr]) return fail(SAGA_EGRAPH, "etype value outside [0, num_rel)");
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_rel_transform_workspace_size(const saga_rel_plan* rel, saga_dtype dtype,
+                                              int64_t k, int64_t n, size_t* bytes) {
+  try {
+    if (!rel || !bytes) return fail(SAGA_EINVAL, "null argument");
+    if (dtype != SAGA_F32 && dtype != SAGA_BF16) return fail(SAGA_EINVAL, "bad dtype");
+    if (k <= 0 || n <= 0) return fail(SAGA_EINVAL, "k and n must be > 0");
+    if (rel->num_rel < 1 || rel->num_rel > saga::kRelMaxRelations)
+      return fail(SAGA_EINVAL, "rel plan is not built");
+    *bytes = saga::gemm_grouped_workspace_bytes(dtype, rel->num_rel, n, k);
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_rel_transform(const saga_rel_plan* rel, saga_dtype dtype, saga_cmat x,
+                               saga_cmat w, saga_mat out, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  try {
+    if (!rel || !rel->counts || !rel->rel_ptr || !rel->pair_src || !rel->plan_counts)
+      return fail(SAGA_EINVAL, "rel plan is not built");
+    return run_rel_transform(*rel, dtype, x, w, out, workspace, workspace_bytes,
+                             static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(SAGA_EINTERNAL, "exception");
   }

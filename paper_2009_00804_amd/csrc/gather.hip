@@ -31,6 +31,14 @@ constexpr int kThreads = 256;
 enum { kSum = 0, kMean = 1, kMax = 2, kSoftmax = 3 };
 
 template <typename T>
+__device__ __forceinline__ float load_elem(const void* p, int64_t i) {
+  if constexpr (sizeof(T) == 4)
+    return static_cast<const float*>(p)[i];
+  else
+    return bf16_to_f32(static_cast<const uint16_t*>(p)[i]);
+}
+
+template <typename T>
 __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int col0,
                                           float (&x)[Vec16<T>::N]) {
   constexpr int EPV = Vec16<T>::N;
@@ -38,6 +46,7 @@ __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int 
   for (int k = 0; k < EPV; ++k) {
     const int c = col0 + k;
     float v = x[k];
+    if (a.self && c < a.out_cols) v += load_elem<T>(a.self, row * a.ld_self + c);
     if (a.bias && c < a.out_cols) v += a.bias[c];
     x[k] = apply_act(a.act, v);
   }
@@ -65,13 +74,18 @@ __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int 
 // in profiles.
 // IDENT: the source row of edge e is row e itself (the segment reduction of
 // an edge tensor already laid out in CSR order; the unfused path).
-template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, bool SRCNORM, bool SLICED,
+// WM: message weight -- kWNone (1), kWSrcNorm (d_out(u)^-1/2, GCN) or
+// kWEdge (edge_scale[e], R-GCN's 1 / c(v, r); col_idx then holds the
+// edge's pair row).
+enum { kWNone = 0, kWSrcNorm = 1, kWEdge = 2 };
+template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, int WM, bool SLICED,
           bool IDENT = false>
 __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int nslices, int slice0) {
   constexpr int EPV = Vec16<T>::N;
   constexpr int NG = kThreads / LPR;
   const int32_t* __restrict__ counts = a.counts;
   if (counts[kErrFlags]) return;
+  if (WM == kWEdge && a.err2[0]) return;
   const int nb = counts[kNumBlocks];
   const int b = blockIdx.x / nslices;
   const int slice = slice0 + (blockIdx.x - b * nslices);
@@ -100,6 +114,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
 
     for (int e = beg; e < end; e += LPR * CPL) {
       int c[CPL];
+      float cw[CPL];
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         const int idx = e + j * LPR + gl;
@@ -107,6 +122,8 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
           c[j] = idx < end ? idx : 0;
         else
           c[j] = idx < end ? __builtin_nontemporal_load(col + idx) : 0;
+        if constexpr (WM == kWEdge)
+          cw[j] = idx < end ? __builtin_nontemporal_load(a.edge_scale + idx) : 0.0f;
       }
       const int n = (end - e) < LPR * CPL ? (end - e) : LPR * CPL;
 #pragma unroll
@@ -121,7 +138,8 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
           for (int k = 0; k < U; ++k) {
             const int tk = t + k < nq ? t + k : t;
             const int u = __shfl(c[j], gbase + tk, 64);
-            if (SRCNORM) wu[k] = rsqrt_deg(a.d_out[u]);
+            if constexpr (WM == kWSrcNorm) wu[k] = rsqrt_deg(a.d_out[u]);
+            if constexpr (WM == kWEdge) wu[k] = __shfl(cw[j], gbase + tk, 64);
 #pragma unroll
             for (int q = 0; q < VPL; ++q) {
               const int vi = v0 + gl + q * LPR;
@@ -137,7 +155,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
                 Vec16<T>::widen(raw[k][q], x);
 #pragma unroll
                 for (int i = 0; i < EPV; ++i) {
-                  const float v = SRCNORM ? x[i] * wu[k] : x[i];
+                  const float v = WM != kWNone ? x[i] * wu[k] : x[i];
                   acc[q][i] = MAXRED ? fmaxf(acc[q][i], v) : acc[q][i] + v;
                 }
               }
@@ -426,6 +444,7 @@ __global__ __launch_bounds__(kThreads) void k_combine(GatherArgs a) {
   __shared__ float fin[1024];
   const int32_t* __restrict__ counts = a.counts;
   if (counts[kErrFlags]) return;
+  if (a.err2 && a.err2[0]) return;
   const int n_split = counts[kNSplit];
   const int red = a.reduce;
   const int F = a.feat;
@@ -513,6 +532,7 @@ __global__ __launch_bounds__(kThreads) void k_combine(GatherArgs a) {
       } else {
         v = fin[c];
       }
+      if (a.self) v += load_elem<T>(a.self, (int64_t)row * a.ld_self + c);
       if (a.bias) v += a.bias[c];
       v = apply_act(a.act, v);
       T* o = static_cast<T*>(a.out) + (int64_t)row * a.ld_out + c;
@@ -575,25 +595,27 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
   const dim3 grid(blocks * conc);
   const bool srcnorm = a.msg == SAGA_MSG_SRC_NORM;
   for (int s0 = 0; s0 < nslices; s0 += conc) {
-#define SAGA_LAUNCH(MX, SN, SL)                                                              \
-  hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, SN, SL>), grid, dim3(kThreads), \
+#define SAGA_LAUNCH(MX, WM, SL)                                                              \
+  hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, WM, SL>), grid, dim3(kThreads), \
                      0, st, a, conc, s0)
 #define SAGA_LAUNCH_IDENT(MX)                                                                  \
-  hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, false, false, true>), grid,     \
+  hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, kWNone, false, true>), grid,    \
                      dim3(kThreads), 0, st, a, conc, s0)
     const bool sl = nslices > 1;
     if (a.identity) {
       if (a.reduce == kMax) SAGA_LAUNCH_IDENT(true);
       else SAGA_LAUNCH_IDENT(false);
+    } else if (a.msg == SAGA_MSG_TYPED) {
+      SAGA_LAUNCH(false, kWEdge, false);
     } else if (a.reduce == kMax) {
-      if (srcnorm) SAGA_LAUNCH(true, true, false);
-      else SAGA_LAUNCH(true, false, false);
+      if (srcnorm) SAGA_LAUNCH(true, kWSrcNorm, false);
+      else SAGA_LAUNCH(true, kWNone, false);
     } else if (srcnorm) {
-      SAGA_LAUNCH(false, true, false);
+      SAGA_LAUNCH(false, kWSrcNorm, false);
     } else if (sl) {
-      SAGA_LAUNCH(false, false, true);
+      SAGA_LAUNCH(false, kWNone, true);
     } else {
-      SAGA_LAUNCH(false, false, false);
+      SAGA_LAUNCH(false, kWNone, false);
     }
 #undef SAGA_LAUNCH
 #undef SAGA_LAUNCH_IDENT

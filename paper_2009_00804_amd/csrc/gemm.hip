@@ -291,24 +291,42 @@ struct RegA {
   static_assert(S >= 2 && (S - 2) * LMIN < 64, "vmcnt range");
   static constexpr size_t LDS_BYTES = (size_t)RING_SLOTS * 16;
 
-  // fragment (h, mt) of chunk k0: row r0 + 16 mt + lane % 16, columns
-  // k0 + (4 h + lane / 16) EPL ..  Rows >= M read row M - 1 (their results
-  // are never stored); a piece that starts at or past K reads the last piece
-  // of the row instead and is zeroed by mask() before use.  A piece that
-  // starts below K ends within the row's ld (a multiple of 16 bytes).
-  __device__ __forceinline__ static void load_a(const T* __restrict__ A, int64_t lda, int64_t M,
-                                                int64_t K, int64_t r0, int64_t k0,
+  // element offsets of this lane's A rows r0 + 16 mt + lane % 16.  Rows >=
+  // M read row M - 1 (their results are never stored).  With a row map, row
+  // q is row arow[q] of A; a negative entry reads row 0 (the caller writes
+  // zeros for it).
+  __device__ __forceinline__ static void row_offsets(const int32_t* __restrict__ arow, int64_t lda,
+                                                     int64_t M, int64_t r0, int64_t (&off)[MT]) {
+    const int lr = threadIdx.x & 15;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int64_t row = r0 + mt * 16 + lr;
+      int64_t rr = row < M ? row : M - 1;
+      if (arow) {
+        const int32_t s = arow[rr];
+        rr = s >= 0 ? s : 0;
+      }
+      off[mt] = rr * lda;
+    }
+  }
+
+  // fragment (h, mt) of chunk k0: the lane's row mt, columns
+  // k0 + (4 h + lane / 16) EPL ..  A piece that starts at or past K reads
+  // the last piece of the row instead and is zeroed by mask() before use.  A
+  // piece that starts below K ends within the row's ld (a multiple of 16
+  // bytes).
+  __device__ __forceinline__ static void load_a(const T* __restrict__ A,
+                                                const int64_t (&off)[MT], int64_t K, int64_t k0,
                                                 Frag (&a)[2][MT]) {
     constexpr int EPL = Mma<T>::EPL;
-    const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+    const int lane = threadIdx.x & 63, lg = lane >> 4;
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const int64_t row = r0 + mt * 16 + lr, k = k0 + (h * 4 + lg) * EPL;
-        const int64_t rr = row < M ? row : M - 1;
+        const int64_t k = k0 + (h * 4 + lg) * EPL;
         const int64_t kk = k < K ? k : (K - 1) / EPL * EPL;
-        const uint4 v = *reinterpret_cast<const uint4*>(A + rr * lda + kk);
+        const uint4 v = *reinterpret_cast<const uint4*>(A + off[mt] + kk);
         __builtin_memcpy(&a[h][mt], &v, 16);
       }
   }
@@ -391,8 +409,9 @@ struct RegA {
   }
 
   struct Ctx {
-    const T* A; int64_t lda, M, K;
-    const T* Wt; int64_t kp, n0, r0;
+    const T* A; int64_t K;
+    const T* Wt; int64_t kp, n0;
+    int64_t off[MT];
     uint4* ring;
     int nch, last;
   };
@@ -408,7 +427,7 @@ struct RegA {
     wait_stages(c.last - i < S - 2 ? c.last - i : S - 2);  // chunk i's loads landed
     ring_barrier();  // every wave's; stage i - 1 is free again
     if (i + S - 1 < c.nch) {
-      load_a(c.A, c.lda, c.M, c.K, c.r0, (int64_t)(i + S - 1) * KC, a[NU]);
+      load_a(c.A, c.off, c.K, (int64_t)(i + S - 1) * KC, a[NU]);
       issue_b(c.Wt, c.kp, c.n0, (int64_t)(i + S - 1) * KC, c.ring + NU * STAGE);
     }
     if (i == c.last) mask(c.K, (int64_t)i * KC, a[U]);
@@ -421,12 +440,13 @@ struct RegA {
   __device__ __forceinline__ static void phase(const T* __restrict__ A, int64_t lda, int64_t M,
                                                int64_t K, const T* __restrict__ Wt, int64_t kp,
                                                int64_t tile0, int64_t n0, uint4* ring,
-                                               f32x4 (&acc)[MT][NT]) {
+                                               f32x4 (&acc)[MT][NT],
+                                               const int32_t* __restrict__ arow = nullptr) {
     static_assert(S <= 4, "unrolled for at most four stages");
     constexpr int KC = Mma<T>::KC;
     Ctx c;
-    c.A = A; c.lda = lda; c.M = M; c.K = K; c.Wt = Wt; c.kp = kp; c.n0 = n0;
-    c.r0 = tile0 + (threadIdx.x >> 6) * MT * 16;
+    c.A = A; c.K = K; c.Wt = Wt; c.kp = kp; c.n0 = n0;
+    row_offsets(arow, lda, M, tile0 + (threadIdx.x >> 6) * MT * 16, c.off);
     c.ring = ring;
     c.nch = (int)((K + KC - 1) / KC);
     c.last = c.nch - 1;
@@ -434,7 +454,7 @@ struct RegA {
 #pragma unroll
     for (int j = 0; j < S - 1; ++j)
       if (j < c.nch) {
-        load_a(A, lda, M, K, c.r0, (int64_t)j * KC, a[j]);
+        load_a(A, c.off, K, (int64_t)j * KC, a[j]);
         issue_b(Wt, kp, n0, (int64_t)j * KC, ring + j * STAGE);
       }
     for (int i0 = 0; i0 < c.nch; i0 += S) {
@@ -538,6 +558,69 @@ __global__ __launch_bounds__(kThreads) void k_gemm_gru(GemmArgs g) {
       const float hp = Mma<T>::to_f(h[row * g.lda2 + c]);
       out[row * g.ldo + c] = Mma<T>::from_f((1.0f - zz) * nn + zz * hp);
     }
+  }
+}
+
+// Grouped: row q of the output is row arow[q] of A times the weight of the
+// group whose row range holds q (R-GCN's per-relation transform of the
+// distinct (relation, source) pairs).  Group ranges are whole tiles, so a
+// tile finds its group by a binary search of grp_ptr and multiplies by that
+// group's packed weight; tiles from grp_ptr[groups] on are idle.  Rows whose
+// map entry is negative (range padding) are written as zeros.
+template <typename T, int MT, int NT, typename R>
+__global__ __launch_bounds__(R::THREADS) void k_gemm_grouped(GemmArgs g) {
+  static_assert(R::BM == kRelTile, "grouped tiles must match the row-range padding");
+  __shared__ uint4 ring[R::RING_SLOTS];
+  if ((g.err1 && *g.err1) || (g.err2 && *g.err2)) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t tile0 = (int64_t)blockIdx.x * R::BM;
+  const int64_t rows = g.grp_ptr[g.groups];
+  if (tile0 >= rows) return;
+  int lo = 0, hi = g.groups;  // grp_ptr[lo] <= tile0 < grp_ptr[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (g.grp_ptr[mid] <= tile0) lo = mid;
+    else hi = mid;
+  }
+  const int64_t n0 = (int64_t)blockIdx.y * R::BN;
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  R::phase(static_cast<const T*>(g.a), g.lda, g.M, g.K,
+           static_cast<const T*>(g.wt) + (int64_t)lo * g.wt_group_stride, g.kp, tile0, n0, ring,
+           acc, g.arow);
+  const int64_t row0 = tile0 + wave * MT * 16;
+  T* out = static_cast<T*>(g.out);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = row0 + mt * 16 + 4 * (lane >> 4) + r;
+      const bool keep = g.arow[row] >= 0;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int64_t c = n0 + nt * 16 + (lane & 15);
+        if (c >= g.N) continue;
+        out[row * g.ldo + c] = Mma<T>::from_f(keep ? acc[mt][nt][r] : 0.0f);
+      }
+    }
+}
+
+// Wt[grp][n][k] = W[grp K + k][n] for n < N, k < K, else 0; each group's
+// packed weight is Np x Kp with ld Kp
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_pack_wt_grouped(const T* __restrict__ W,
+                                                              int64_t ldw, int64_t K, int64_t N,
+                                                              int groups, T* __restrict__ Wt,
+                                                              int64_t Kp, int64_t Np) {
+  const int64_t per = Np * Kp, total = per * groups;
+  for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kThreads) {
+    const int64_t grp = i / per, j = i - grp * per;
+    const int64_t n = j / Kp, k = j - n * Kp;
+    Wt[i] = (n < N && k < K) ? W[(grp * K + k) * ldw + n] : T(0);
   }
 }
 
@@ -666,6 +749,38 @@ hipError_t pack(const void* w, int64_t ldw, int64_t K, int64_t N, void* wt, int6
   return hipGetLastError();
 }
 
+// grouped GEMM tiling: 128-row tiles (RegA, 2 x 16 rows per wave, 4 waves,
+// 4 stages), up to 128 columns per tile
+inline int grouped_nt(int64_t N) { return (int)std::min<int64_t>(8, (N + 15) / 16); }
+
+template <typename T, int NT>
+hipError_t launch_grouped_nt(const GemmArgs& g, hipStream_t st) {
+  typedef RegA<T, 2, NT, 4> R;
+  dim3 grid((unsigned)(g.M / R::BM), (unsigned)((g.N + R::BN - 1) / R::BN));
+  hipLaunchKernelGGL((k_gemm_grouped<T, 2, NT, R>), grid, dim3(R::THREADS), 0, st, g);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t dispatch_grouped(const GemmArgs& g, hipStream_t st) {
+  switch (grouped_nt(g.N)) {
+    case 1: return launch_grouped_nt<T, 1>(g, st);
+    case 2: return launch_grouped_nt<T, 2>(g, st);
+    case 3: return launch_grouped_nt<T, 3>(g, st);
+    case 4: return launch_grouped_nt<T, 4>(g, st);
+    case 5: return launch_grouped_nt<T, 5>(g, st);
+    case 6: return launch_grouped_nt<T, 6>(g, st);
+    case 7: return launch_grouped_nt<T, 7>(g, st);
+    default: return launch_grouped_nt<T, 8>(g, st);
+  }
+}
+
+void grouped_packed(int dtype, int64_t N, int64_t K, int64_t* np, int64_t* kp) {
+  const int64_t bn = 16 * grouped_nt(N), kc = kc_of(dtype);
+  *np = (N + bn - 1) / bn * bn;
+  *kp = (K + kc - 1) / kc * kc;
+}
+
 }  // namespace
 
 size_t gemm_workspace_bytes(int dtype, int mode, int64_t N, int64_t K, int64_t K2) {
@@ -690,6 +805,40 @@ hipError_t launch_gemm(const GemmArgs& g0, hipStream_t st) {
            : pack<float>(g.w2, g.ldw2, g.K2, g.N, ws + pk.off2, pk.kp2, pk.np, st);
   if (e != hipSuccess) return e;
   return bf ? dispatch<uint16_t>(g, st) : dispatch<float>(g, st);
+}
+
+size_t gemm_grouped_workspace_bytes(int dtype, int groups, int64_t N, int64_t K) {
+  int64_t np, kp;
+  grouped_packed(dtype, N, K, &np, &kp);
+  const size_t es = dtype == SAGA_BF16 ? 2 : 4;
+  return ((size_t)groups * np * kp * es + 255) / 256 * 256;
+}
+
+hipError_t launch_gemm_grouped(const GemmArgs& g0, hipStream_t st) {
+  if (g0.M == 0) return hipSuccess;
+  if (g0.M % kRelTile != 0 || g0.groups < 1 || !g0.arow || !g0.grp_ptr) return hipErrorInvalidValue;
+  if (!g0.ws || g0.ws_bytes < gemm_grouped_workspace_bytes(g0.dtype, g0.groups, g0.N, g0.K))
+    return hipErrorInvalidValue;
+  GemmArgs g = g0;
+  int64_t np, kp;
+  grouped_packed(g.dtype, g.N, g.K, &np, &kp);
+  g.wt = g.ws;
+  g.kp = kp;
+  g.wt_group_stride = np * kp;
+  const bool bf = g.dtype == SAGA_BF16;
+  const int64_t total = np * kp * g.groups;
+  const unsigned blocks = (unsigned)std::min<int64_t>((total + kThreads - 1) / kThreads, 4096);
+  if (bf)
+    hipLaunchKernelGGL((k_pack_wt_grouped<uint16_t>), dim3(blocks), dim3(kThreads), 0, st,
+                       static_cast<const uint16_t*>(g.w), g.ldw, g.K, g.N, g.groups,
+                       static_cast<uint16_t*>(g.ws), kp, np);
+  else
+    hipLaunchKernelGGL((k_pack_wt_grouped<float>), dim3(blocks), dim3(kThreads), 0, st,
+                       static_cast<const float*>(g.w), g.ldw, g.K, g.N, g.groups,
+                       static_cast<float*>(g.ws), kp, np);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return bf ? dispatch_grouped<uint16_t>(g, st) : dispatch_grouped<float>(g, st);
 }
 
 }  // namespace saga

@@ -75,6 +75,12 @@ struct GatherArgs {
   float* partial; int64_t pstride;
   int pcols;       // partial accumulator columns; softmax m/l follow at pcols
   int identity;    // source row of edge e is row e (unfused segment reduction)
+  // typed messages: source row of CSR entry e is col_idx[e] (= the rel
+  // plan's edge_pair), scaled by edge_scale[e]; err2: the rel plan's flags
+  const float* edge_scale;
+  const int32_t* err2;
+  // added to every output row before the bias (nullable; dtype of out)
+  const void* self; int64_t ld_self;
 };
 
 int gather_partial_cols(int64_t feat);
@@ -100,6 +106,17 @@ struct GemmArgs {
   // set by launch_gemm: packed weights in the workspace, ld kp / kp2
   const void* wt; int64_t kp;
   const void* wt2; int64_t kp2;
+  // grouped mode (launch_gemm_grouped): row q of A is row arow[q] of a (a
+  // negative entry gives an all-zero output row); w holds `groups` K x N
+  // weights stacked; rows [grp_ptr[g], grp_ptr[g+1]) use weight g, ranges
+  // are whole tiles, grp_ptr[groups] is the row count; err1 / err2 nonzero:
+  // do nothing
+  const int32_t* arow;
+  const int32_t* grp_ptr;
+  int groups;
+  int64_t wt_group_stride;
+  const int32_t* err1;
+  const int32_t* err2;
 };
 // LSTM Gather (GraphSAGE): recurrence over each row's in-edges
 struct LstmArgs {
@@ -119,6 +136,26 @@ hipError_t launch_lstm_gather(const LstmArgs& a, hipStream_t st);
 // bytes of workspace launch_gemm needs for these shapes (packed weights)
 size_t gemm_workspace_bytes(int dtype, int mode, int64_t N, int64_t K, int64_t K2);
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t st);
+// grouped GEMM over row ranges of whole kRelTile-row tiles (mode ignored;
+// M = row capacity, a multiple of kRelTile)
+size_t gemm_grouped_workspace_bytes(int dtype, int groups, int64_t N, int64_t K);
+hipError_t launch_gemm_grouped(const GemmArgs& g, hipStream_t st);
+
+// ---- rel.hip ----
+constexpr int kRelTile = SAGA_REL_TILE;  // rows per grouped-GEMM tile
+constexpr int kRelMaxRelations = SAGA_REL_MAX_RELATIONS;
+enum RelCount : int { kRelRows = 0, kRelPairs = 1, kRelErr = 2, kRelCountSlots = 4 };
+struct RelLayout {
+  int64_t wp;        // bitmap words per relation (whole counting blocks)
+  int64_t bpr;       // counting blocks per relation
+  int64_t nblocks;   // counting blocks in all
+  int64_t max_pairs;
+  size_t off_rel_ptr, off_rel_count, off_pair_src, off_edge_pair, off_edge_norm, off_counts,
+      off_scratch, off_bitmap, off_word_base, off_bcnt, off_block_base, scratch_bytes, total;
+};
+bool rel_layout(int32_t num_src, int64_t num_edges, int32_t num_rel, RelLayout* L);
+hipError_t launch_rel_build(const saga_plan& p, const saga_rel_plan& rel, const RelLayout& L,
+                            hipStream_t st);
 
 // ---- layer helpers (gather.hip) ----
 hipError_t launch_fold_attention(const float* w, int64_t K, int64_t F, int heads, const float* al,

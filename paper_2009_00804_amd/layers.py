@@ -26,14 +26,15 @@ class Layer:
 
     def __init__(self, graph: S.Graph, kind: str, in_feat: int, out_feat: int, weights: dict,
                  dtype=torch.float32, act="none", heads=1, head_mean=False, neg_slope=0.2,
-                 edge_feat=0, out_ld=None, hidden=0):
+                 edge_feat=0, out_ld=None, hidden=0, rel=None):
         dev = graph.row_ptr.device
         self.graph = graph
         self.dtype = dtype
         wdt = dtype
         kinds = {"gcn": S.SAGA_LAYER_GCN, "gat": S.SAGA_LAYER_GAT, "sage_pool": S.SAGA_LAYER_SAGE_POOL,
-                 "gated_gru": S.SAGA_LAYER_GATED_GRU, "sage_lstm": S.SAGA_LAYER_SAGE_LSTM}
-        self.w = {k: (_dev(v, dev, wdt if k in ("w", "w_pool") else torch.float32))
+                 "gated_gru": S.SAGA_LAYER_GATED_GRU, "sage_lstm": S.SAGA_LAYER_SAGE_LSTM,
+                 "rgcn": S.SAGA_LAYER_RGCN}
+        self.w = {k: (_dev(v, dev, wdt if k in ("w", "w_pool", "w_self") else torch.float32))
                   for k, v in weights.items()}
         d = S.saga_layer_desc()
         d.kind = kinds[kind]
@@ -47,9 +48,12 @@ class Layer:
         d.edge_feat = edge_feat
         d.hidden = hidden
         for k in ("w", "b", "w_pool", "b_pool", "attn_l", "attn_r", "w_e", "b_e", "w_ih", "b_ih",
-                  "w_hh", "b_hh"):
+                  "w_hh", "b_hh", "w_self"):
             t = self.w.get(k)
             setattr(d, k, None if t is None else t.data_ptr())
+        self.rel = rel  # keeps the RelGraph (and its device arrays) alive
+        if rel is not None:
+            d.rel = C.pointer(rel.rel)
         self.desc = d
         self.ws_bytes = S.saga_layer_workspace_size(graph.plan, d)
         self.ws = S.workspace(self.ws_bytes, dev)
@@ -104,6 +108,14 @@ def sage_lstm(graph, g):
     return [Layer(graph, "sage_lstm", F, g["W"].shape[1],
                   {"w": g["W"], "b": g["b"], "w_ih": g["W_ih"], "b_ih": g["b_ih"],
                    "w_hh": g["W_hh"], "b_hh": g["b_hh"]}, hidden=G4 // 4)]
+
+
+def rgcn(graph, rel, g, dtype=torch.float32):
+    """R-GCN layer: act(x_v W_self + b + sum over in-edges of x_u W_r / c(v, r))."""
+    R, Fi, Fo = g["W_rel"].shape
+    return [Layer(graph, "rgcn", Fi, Fo,
+                  {"w": g["W_rel"].reshape(R * Fi, Fo), "w_self": g["W_self"], "b": g["b"]},
+                  dtype=dtype, act=g.get("act", "none"), rel=rel)]
 
 
 def run(layers, x, edge_feat=None, stream=None):

@@ -23,10 +23,13 @@ LIB_PATH = os.path.join(_PKG, "libsaga.so")
 SAGA_OK, SAGA_EINVAL, SAGA_EGRAPH, SAGA_EUNSUPPORTED, SAGA_EDEVICE, SAGA_EWORKSPACE, SAGA_EINTERNAL = range(7)
 SAGA_F32, SAGA_BF16 = 0, 1
 SAGA_RED_SUM, SAGA_RED_MEAN, SAGA_RED_MAX, SAGA_RED_SOFTMAX = range(4)
-SAGA_MSG_COPY, SAGA_MSG_SRC_NORM, SAGA_MSG_GAT, SAGA_MSG_GATED = range(4)
+SAGA_MSG_COPY, SAGA_MSG_SRC_NORM, SAGA_MSG_GAT, SAGA_MSG_GATED, SAGA_MSG_TYPED = range(5)
 SAGA_ACT_NONE, SAGA_ACT_RELU, SAGA_ACT_ELU, SAGA_ACT_SIGMOID, SAGA_ACT_TANH = range(5)
 SAGA_GEMM_PLAIN, SAGA_GEMM_CONCAT, SAGA_GEMM_GRU = range(3)
-SAGA_LAYER_GCN, SAGA_LAYER_GAT, SAGA_LAYER_SAGE_POOL, SAGA_LAYER_GATED_GRU, SAGA_LAYER_SAGE_LSTM = range(5)
+(SAGA_LAYER_GCN, SAGA_LAYER_GAT, SAGA_LAYER_SAGE_POOL, SAGA_LAYER_GATED_GRU, SAGA_LAYER_SAGE_LSTM,
+ SAGA_LAYER_RGCN) = range(6)
+SAGA_REL_TILE = 128
+SAGA_REL_MAX_RELATIONS = 2048
 
 ACT = {"none": 0, "relu": 1, "elu": 2, "sigmoid": 3, "tanh": 4}
 
@@ -35,6 +38,8 @@ EXPORTS = [
     "saga_gather_workspace_size", "saga_scatter_apply_edge_gather",
     "saga_unfused_workspace_size", "saga_scatter_gather_unfused",
     "saga_lstm_gather_workspace_size", "saga_lstm_gather",
+    "saga_rel_plan_workspace_size", "saga_rel_plan_build", "saga_rel_plan_check",
+    "saga_rel_transform_workspace_size", "saga_rel_transform",
     "saga_apply_vertex_workspace_size", "saga_apply_vertex",
     "saga_layer_workspace_size", "saga_layer", "saga_status_str", "saga_last_error",
     "saga_version",
@@ -72,6 +77,20 @@ class saga_plan_counts(C.Structure):
                 ("s_split", C.c_int64), ("error_flags", C.c_int32), ("max_in_degree", C.c_int32)]
 
 
+class saga_rel_plan(C.Structure):
+    _fields_ = [
+        ("num_rel", C.c_int32), ("num_src", C.c_int32), ("num_edges", C.c_int64),
+        ("max_pairs", C.c_int64), ("etype", C.c_void_p), ("plan_counts", C.c_void_p),
+        ("rel_ptr", C.c_void_p), ("rel_count", C.c_void_p), ("pair_src", C.c_void_p),
+        ("edge_pair", C.c_void_p), ("edge_norm", C.c_void_p), ("counts", C.c_void_p),
+        ("scratch", C.c_void_p), ("scratch_bytes", C.c_size_t),
+    ]
+
+
+class saga_rel_counts(C.Structure):
+    _fields_ = [("pair_rows", C.c_int64), ("pairs", C.c_int64), ("error_flags", C.c_int32)]
+
+
 class saga_edge_op(C.Structure):
     _fields_ = [("msg", C.c_int), ("reduce", C.c_int), ("dtype", C.c_int), ("heads", C.c_int32),
                 ("head_mean", C.c_int32), ("dst_norm", C.c_int32), ("neg_slope", C.c_float),
@@ -81,7 +100,8 @@ class saga_edge_op(C.Structure):
 class saga_edge_inputs(C.Structure):
     _fields_ = [("src", saga_cmat), ("el", saga_cmat), ("er", saga_cmat), ("gate_src", saga_cmat),
                 ("gate_dst", saga_cmat), ("edge_feat", saga_cmat), ("w_edge", C.c_void_p),
-                ("gate_bias", C.c_void_p), ("bias", C.c_void_p)]
+                ("gate_bias", C.c_void_p), ("bias", C.c_void_p), ("rel", C.POINTER(saga_rel_plan)),
+                ("self", saga_cmat)]
 
 
 class saga_gemm_op(C.Structure):
@@ -97,7 +117,7 @@ class saga_layer_desc(C.Structure):
         ("w", C.c_void_p), ("b", C.c_void_p), ("w_pool", C.c_void_p), ("b_pool", C.c_void_p),
         ("attn_l", C.c_void_p), ("attn_r", C.c_void_p), ("w_e", C.c_void_p), ("b_e", C.c_void_p),
         ("w_ih", C.c_void_p), ("b_ih", C.c_void_p), ("w_hh", C.c_void_p), ("b_hh", C.c_void_p),
-        ("hidden", C.c_int32),
+        ("hidden", C.c_int32), ("w_self", C.c_void_p), ("rel", C.POINTER(saga_rel_plan)),
     ]
 
 
@@ -128,6 +148,14 @@ def lib():
         "saga_lstm_gather_workspace_size": (S, [P(saga_plan), C.c_int64, P(C.c_size_t)]),
         "saga_lstm_gather": (S, [P(saga_plan), saga_cmat, saga_cmat, saga_mat, C.c_void_p, C.c_size_t,
                                  C.c_void_p]),
+        "saga_rel_plan_workspace_size": (S, [P(saga_plan), C.c_int32, P(C.c_size_t)]),
+        "saga_rel_plan_build": (S, [P(saga_plan), C.c_void_p, C.c_int32, C.c_void_p, C.c_size_t,
+                                    C.c_void_p, P(saga_rel_plan)]),
+        "saga_rel_plan_check": (S, [P(saga_rel_plan), C.c_void_p, P(saga_rel_counts)]),
+        "saga_rel_transform_workspace_size": (S, [P(saga_rel_plan), C.c_int, C.c_int64, C.c_int64,
+                                                  P(C.c_size_t)]),
+        "saga_rel_transform": (S, [P(saga_rel_plan), C.c_int, saga_cmat, saga_cmat, saga_mat,
+                                   C.c_void_p, C.c_size_t, C.c_void_p]),
         "saga_apply_vertex_workspace_size": (S, [P(saga_gemm_op), C.c_int64, C.c_int64, C.c_int64,
                                                  P(C.c_size_t)]),
         "saga_apply_vertex": (S, [P(saga_gemm_op), saga_cmat, saga_cmat, saga_cmat, saga_cmat, C.c_void_p,
@@ -222,6 +250,38 @@ def saga_lstm_gather_workspace_size(plan, hidden):
 def saga_lstm_gather(plan, gates_x, w_hh, out, workspace, ws_bytes, stream):
     return _check(lib().saga_lstm_gather(C.byref(plan), gates_x, w_hh, out, workspace, ws_bytes, stream),
                   "saga_lstm_gather")
+
+
+def saga_rel_plan_workspace_size(plan, num_rel):
+    out = C.c_size_t(0)
+    _check(lib().saga_rel_plan_workspace_size(C.byref(plan), num_rel, C.byref(out)),
+           "saga_rel_plan_workspace_size")
+    return out.value
+
+
+def saga_rel_plan_build(plan, etype, num_rel, workspace, ws_bytes, stream):
+    rel = saga_rel_plan()
+    _check(lib().saga_rel_plan_build(C.byref(plan), etype, num_rel, workspace, ws_bytes, stream,
+                                     C.byref(rel)), "saga_rel_plan_build")
+    return rel
+
+
+def saga_rel_plan_check(rel, stream):
+    counts = saga_rel_counts()
+    st = lib().saga_rel_plan_check(C.byref(rel), stream, C.byref(counts))
+    return st, counts
+
+
+def saga_rel_transform_workspace_size(rel, dtype, k, n):
+    out = C.c_size_t(0)
+    _check(lib().saga_rel_transform_workspace_size(C.byref(rel), dtype, k, n, C.byref(out)),
+           "saga_rel_transform_workspace_size")
+    return out.value
+
+
+def saga_rel_transform(rel, dtype, x, w, out, workspace, ws_bytes, stream):
+    return _check(lib().saga_rel_transform(C.byref(rel), dtype, x, w, out, workspace, ws_bytes,
+                                           stream), "saga_rel_transform")
 
 
 def saga_apply_vertex_workspace_size(op, k, k2, n):
@@ -367,3 +427,49 @@ class Graph:
             perm=self._view(p.perm, V), row_seg_first=self._view(p.row_seg_first, V + 1),
             seg_row=self._view(p.seg_row, S), seg_beg=self._view(p.seg_beg, S),
             seg_end=self._view(p.seg_end, S), block_ptr=self._view(p.block_ptr, nb + 1))
+
+
+class RelGraph:
+    """The typed layout of a Graph's edges (R-GCN): etype is an int32 device
+    tensor aligned with the CSR entries; memory owned by torch."""
+
+    def __init__(self, graph: Graph, etype, num_rel, stream=None, check=True):
+        assert etype.dtype == torch.int32 and etype.numel() == graph.num_edges
+        self.graph = graph
+        self.etype = etype
+        self.num_rel = num_rel
+        self.stream = stream
+        self.ws_bytes = saga_rel_plan_workspace_size(graph.plan, num_rel)
+        self.ws = workspace(self.ws_bytes, etype.device)
+        self.build()
+        self.counts = None
+        if check:
+            self.check()
+
+    def build(self):
+        self.rel = saga_rel_plan_build(self.graph.plan, _ptr(self.etype) if self.etype.numel() else None,
+                                       self.num_rel, _ptr(self.ws), self.ws.numel(),
+                                       stream_handle(self.stream))
+        return self.rel
+
+    def check(self):
+        st, counts = saga_rel_plan_check(self.rel, stream_handle(self.stream))
+        self.counts = counts
+        _check(st, "saga_rel_plan_check")
+        return counts
+
+    def _view(self, ptr, n, dtype=torch.int32):
+        if n == 0:
+            return torch.zeros(0, dtype=dtype, device=self.ws.device)
+        off = ptr - self.ws.data_ptr()
+        return self.ws[off:off + 4 * n].view(dtype)
+
+    def arrays(self):
+        c = self.counts or self.check()
+        r = self.rel
+        E = self.graph.num_edges
+        return dict(rel_ptr=self._view(r.rel_ptr, self.num_rel + 1),
+                    rel_count=self._view(r.rel_count, self.num_rel),
+                    pair_src=self._view(r.pair_src, c.pair_rows),
+                    edge_pair=self._view(r.edge_pair, E),
+                    edge_norm=self._view(r.edge_norm, E, torch.float32))

@@ -212,3 +212,105 @@ def test_layer_rejects_bad_descriptors(S):
     out = S.saga_mat(0x60000, 16, 8, 8)
     none = S.saga_cmat(None, 0, 0, 0)
     assert L.saga_layer(C.byref(p), C.byref(d), x, none, out, None, 0, None) == S.SAGA_EWORKSPACE
+
+
+def _fake_rel(S, p, R=4):
+    r = S.saga_rel_plan()
+    r.num_rel, r.num_src, r.num_edges = R, p.num_src, p.num_edges
+    r.max_pairs = 256
+    r.etype = 0x70000
+    r.plan_counts = p.counts
+    for f in ("rel_ptr", "rel_count", "pair_src", "edge_pair", "edge_norm", "counts"):
+        setattr(r, f, 0x80000)
+    return r
+
+
+def test_rel_plan_rejects_bad_arguments(S):
+    p = _fake_plan(S)
+    L = S.lib()
+    n = S.saga_rel_plan_workspace_size(p, 4)
+    assert n > 0 and n % 256 == 0
+    assert S.saga_rel_plan_workspace_size(p, S.SAGA_REL_MAX_RELATIONS) > n
+    sz = C.c_size_t()
+    for R in (0, -1, S.SAGA_REL_MAX_RELATIONS + 1):
+        assert L.saga_rel_plan_workspace_size(C.byref(p), R, C.byref(sz)) == S.SAGA_EINVAL
+    rel = S.saga_rel_plan()
+
+    def build(et=0x70000, R=4, ws=0x1000000, nb=n):
+        return L.saga_rel_plan_build(C.byref(p), et, R, ws, nb, None, C.byref(rel))
+
+    assert build(et=None) == S.SAGA_EINVAL
+    assert build(R=0) == S.SAGA_EINVAL
+    assert build(nb=n - 1) == S.SAGA_EWORKSPACE
+    assert build(ws=0x1000010) == S.SAGA_EINVAL                    # misaligned
+    assert build(ws=0x70000 - 256, nb=n) == S.SAGA_EINVAL          # overlaps etype
+    unbuilt = S.saga_plan()
+    assert L.saga_rel_plan_build(C.byref(unbuilt), 0x70000, 4, 0x1000000, n, None,
+                                 C.byref(rel)) == S.SAGA_EINVAL
+
+
+def test_rel_transform_rejects_bad_arguments(S):
+    p = _fake_plan(S)
+    r = _fake_rel(S, p)
+    L = S.lib()
+    need = S.saga_rel_transform_workspace_size(r, S.SAGA_F32, 32, 16)
+    assert need > 0
+    x = S.saga_cmat(0x100000, 16, 32, 32)
+    w = S.saga_cmat(0x200000, 4 * 32, 16, 16)
+    out = S.saga_mat(0x300000, 256, 16, 16)
+
+    def call(x=x, w=w, o=out, ws=0x900000, nb=need, dt=S.SAGA_F32):
+        return L.saga_rel_transform(C.byref(r), dt, x, w, o, ws, nb, None)
+
+    assert call(w=S.saga_cmat(0x200000, 3 * 32, 16, 16)) == S.SAGA_EINVAL   # not num_rel stacked
+    assert call(x=S.saga_cmat(0x100000, 15, 32, 32)) == S.SAGA_EINVAL       # rows != num_src
+    assert call(o=S.saga_mat(0x300000, 255, 16, 16)) == S.SAGA_EINVAL       # rows != max_pairs
+    assert call(nb=need - 1) == S.SAGA_EWORKSPACE
+    assert call(ws=0x900010) == S.SAGA_EINVAL
+    assert call(o=S.saga_mat(0x100000 + 256, 256, 16, 16)) == S.SAGA_EINVAL  # overlaps x
+    assert call(dt=5) == S.SAGA_EINVAL
+    assert L.saga_rel_transform(None, S.SAGA_F32, x, w, out, 0x900000, need, None) == S.SAGA_EINVAL
+
+
+def test_typed_gather_and_layer_reject_bad_arguments(S):
+    p = _fake_plan(S)
+    r = _fake_rel(S, p)
+    L = S.lib()
+    op = S.saga_edge_op(S.SAGA_MSG_TYPED, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 0, 0.0, 0)
+    inp = S.saga_edge_inputs()
+    inp.src = S.saga_cmat(0x100000, 256, 8, 8)
+    out = S.saga_mat(0x400000, 16, 8, 8)
+
+    def call(o=op):
+        return L.saga_scatter_apply_edge_gather(C.byref(p), C.byref(o), C.byref(inp), out, None, 0,
+                                                None)
+
+    assert call() == S.SAGA_EINVAL                       # no rel plan
+    inp.rel = C.pointer(r)
+    mean = S.saga_edge_op(S.SAGA_MSG_TYPED, S.SAGA_RED_MEAN, S.SAGA_F32, 1, 0, 0, 0.0, 0)
+    assert call(o=mean) == S.SAGA_EUNSUPPORTED
+    inp.src = S.saga_cmat(0x100000, 16, 8, 8)            # rows must be max_pairs
+    assert call() == S.SAGA_EINVAL
+    inp.src = S.saga_cmat(0x100000, 256, 8, 8)
+    other = _fake_rel(S, p)
+    other.plan_counts = 0x31000                          # built on another plan
+    inp.rel = C.pointer(other)
+    assert call() == S.SAGA_EINVAL
+    inp.rel = C.pointer(r)
+    inp.self = S.saga_cmat(0x500000, 15, 8, 8)           # self rows != num_dst
+    assert call() == S.SAGA_EINVAL
+    inp.self = S.saga_cmat(0x400000 + 64, 16, 8, 8)      # overlaps out
+    assert call() == S.SAGA_EINVAL
+    # the layer needs w, w_self and a rel plan of the same graph
+    d = S.saga_layer_desc()
+    d.kind = S.SAGA_LAYER_RGCN
+    d.dtype = S.SAGA_F32
+    d.in_feat, d.out_feat = 8, 8
+    d.w = 0x1000
+    n = C.c_size_t()
+    assert L.saga_layer_workspace_size(C.byref(p), C.byref(d), C.byref(n)) == S.SAGA_EINVAL
+    d.w_self = 0x2000
+    assert L.saga_layer_workspace_size(C.byref(p), C.byref(d), C.byref(n)) == S.SAGA_EINVAL
+    d.rel = C.pointer(r)
+    assert L.saga_layer_workspace_size(C.byref(p), C.byref(d), C.byref(n)) == S.SAGA_OK
+    assert n.value > 0
