@@ -253,6 +253,8 @@ SUITE = [  # the other workloads, one model each (Table I models at their config
     ("sage_rmat", "GraphSAGE-pool, R-MAT scale 17, 16 edges/vertex, 256->256"),
     ("gated_rgg", "gated edge MPNN + GRU, torus RGG(100000, expected degree 12), 64 (+16 edge)"),
     ("sage_lstm", "GraphSAGE-LSTM, R-MAT scale 17, 16 edges/vertex, 256 -> LSTM 128 -> 256"),
+    ("rgcn_rmat", "R-GCN, R-MAT scale 18, 16 edges/vertex, 32 relation types (P(r) ~ 1/(r+1)), "
+                  "128 -> 64, ReLU"),
 ]
 
 
@@ -277,13 +279,16 @@ def _oracle_model(name, g, rows=None):
         return O.sage_layer_of(g)
     if name == "sage_lstm":
         return O.sage_lstm_layer_of(g, rows=rows)
+    if name == "rgcn_rmat":
+        return O.rgcn_layer_of(g, rows=rows)
     return O.gated_layer_of(g)
 
 
 def suite(dev, reps=10, oracle=True):
-    """Per-workload, per-layer timing of the other five workloads through
+    """Per-workload, per-layer timing of the other six workloads through
     saga_layer (plan built once per graph and timed separately); with
-    `oracle`, the oracle's whole model on the same inputs, one thread."""
+    `oracle`, the oracle's whole model on the same inputs (or a bounded row
+    sample of it), one thread."""
     import numpy as np
     import torch
 
@@ -308,6 +313,10 @@ def suite(dev, reps=10, oracle=True):
             model, x, ef = LY.sage_pool(graph, g), _padded(g["X"], torch, dev), None
         elif name == "sage_lstm":
             model, x, ef = LY.sage_lstm(graph, g), _padded(g["X"], torch, dev), None
+        elif name == "rgcn_rmat":
+            et = torch.from_numpy(g["etype"]).to(dev)
+            relg = S.RelGraph(graph, et, g["num_rel"])
+            model, x, ef = LY.rgcn(graph, relg, g), _padded(g["X"], torch, dev), None
         else:
             model = LY.gated_gru(graph, g)
             x, ef = _padded(g["H"], torch, dev), _padded(g["E_feat"], torch, dev)
@@ -343,6 +352,10 @@ def suite(dev, reps=10, oracle=True):
                         "vertices_per_s": V / (ms * 1e-3)} for ms in per]}
         log(f"suite {name}: V={V} E={E} plan {out[name]['plan_ms']:.3f} ms, layers "
             + ", ".join(f"{ms:.3f} ms" for ms in per))
+        if name == "rgcn_rmat":
+            out[name].update(rgcn_detail(S, torch, graph, relg, model[0], x, g, dev, reps))
+            log(f"suite rgcn_rmat: {out[name]['rel_plan_ms']:.3f} ms rel plan, stages "
+                + ", ".join(f"{k} {v:.3f}" for k, v in out[name]["stage_ms"].items()))
         if name == "sage_lstm":
             # the recurrence of the longest row is the layer's critical path
             dmax = int(np.diff(g["row_ptr"]).max())
@@ -352,9 +365,10 @@ def suite(dev, reps=10, oracle=True):
             from threadpoolctl import threadpool_limits
 
             rows, e_s, sample = None, E, "whole model, float64"
-            if name == "sage_lstm":
-                # the oracle's recurrence runs step by step: a bounded random sample of rows
-                rows = np.random.default_rng(7).choice(V, 1500, replace=False)
+            if name in ("sage_lstm", "rgcn_rmat"):
+                # the oracle loops over rows (and, for the LSTM, steps): a bounded sample
+                rows = np.random.default_rng(7).choice(V, 1500 if name == "sage_lstm" else 4000,
+                                                       replace=False)
                 e_s = int(np.diff(g["row_ptr"])[rows].sum())
                 sample = f"layer on {len(rows)} random destination rows ({e_s} in-edges), float64"
             with threadpool_limits(1):
@@ -367,6 +381,70 @@ def suite(dev, reps=10, oracle=True):
         del model, graph
         torch.cuda.empty_cache()
     return out
+
+
+def rgcn_detail(S, torch, graph, relg, layer, x, g, dev, reps):
+    """R-GCN stage times (typed layout, grouped per-relation transform, self
+    GEMM, typed Gather) through the op-level entry points, on the layer's
+    own buffers, and the pair counts that size the transform."""
+    import ctypes as C
+
+    c = relg.check()
+    R, Fi, Fo = g["W_rel"].shape
+    rel = relg.rel
+    st = torch.cuda.current_stream()
+    sh = S.stream_handle(st)
+    T = torch.empty((rel.max_pairs, S.gather_ld(Fo, 4)), dtype=torch.float32, device=dev)[:, :Fo]
+    SELF = torch.empty((graph.num_dst, S.gather_ld(Fo, 4)), dtype=torch.float32, device=dev)[:, :Fo]
+    out = torch.empty_like(SELF)
+    Wr = layer.w["w"]
+    Ws = layer.w["w_self"]
+    b = layer.w["b"]
+    tws = S.workspace(S.saga_rel_transform_workspace_size(rel, S.SAGA_F32, Fi, Fo), dev)
+    gop = S.saga_gemm_op(S.SAGA_F32, S.SAGA_GEMM_PLAIN, S.SAGA_ACT_NONE, None)
+    gws = S.workspace(S.saga_apply_vertex_workspace_size(gop, Fi, 0, Fo), dev)
+    op = S.saga_edge_op(S.SAGA_MSG_TYPED, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 0, 0.0, S.SAGA_ACT_RELU)
+    inp = S.saga_edge_inputs()
+    inp.src = S.cmat(T)
+    inp.rel = C.pointer(rel)
+    inp.self = S.cmat(SELF)
+    pws = S.workspace(S.saga_gather_workspace_size(graph.plan, op, Fo), dev)
+    none = S.saga_cmat(None, 0, 0, 0)
+
+    def f_plan():
+        relg.build()
+
+    def f_transform():
+        S.saga_rel_transform(rel, S.SAGA_F32, S.cmat(x), S.cmat(Wr), S.mat(T),
+                             C.c_void_p(tws.data_ptr()), tws.numel(), sh)
+
+    def f_self():
+        S.saga_apply_vertex(gop, S.cmat(x), S.cmat(Ws), none, none, C.c_void_p(b.data_ptr()), None,
+                            S.mat(SELF), C.c_void_p(gws.data_ptr()), gws.numel(), sh)
+
+    def f_gather():
+        S.saga_scatter_apply_edge_gather(graph.plan, op, inp, S.mat(out), C.c_void_p(pws.data_ptr()),
+                                         pws.numel(), sh)
+
+    res = {}
+    for name, f in (("rel_plan", f_plan), ("rel_transform", f_transform), ("self_gemm", f_self),
+                    ("typed_gather", f_gather)):
+        f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(reps):
+            f()
+        e1.record(st)
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / reps
+    pairs = int(c.pairs)
+    E, V = graph.num_edges, graph.num_dst
+    return {"rel_plan_ms": res.pop("rel_plan"), "stage_ms": res, "relations": int(R),
+            "distinct_pairs": pairs, "pair_rows": int(c.pair_rows),
+            "transform_TFLOPs": 2.0 * c.pair_rows * Fi * Fo / (res["rel_transform"] * 1e-3) / 1e12,
+            "flops_vs_per_edge": pairs / E,
+            "flops_vs_all_relations": pairs / (V * R)}
 
 
 def cpu_baseline(g, budget_s=12.0):
@@ -416,7 +494,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-suite", action="store_true",
-                    help="skip the per-layer timing of the five smaller workloads")
+                    help="skip the per-layer timing of the six smaller workloads")
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip the fused-vs-unfused layer-1 aggregation comparison")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
