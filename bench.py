@@ -357,10 +357,12 @@ def suite(dev, reps=10, oracle=True):
             log(f"suite rgcn_rmat: {out[name]['rel_plan_ms']:.3f} ms rel plan, stages "
                 + ", ".join(f"{k} {v:.3f}" for k, v in out[name]["stage_ms"].items()))
         if name == "sage_lstm":
-            # the recurrence of the longest row is the layer's critical path
-            dmax = int(np.diff(g["row_ptr"]).max())
-            out[name]["max_in_degree"] = dmax
-            out[name]["lstm_us_per_step_of_longest_row"] = per[0] * 1e3 / dmax
+            out[name].update(lstm_detail(S, torch, graph, g, x, dev))
+            d = out[name]
+            log(f"suite sage_lstm: LSTM Gather {d['lstm_gather_ms']:.3f} ms persistent "
+                f"({d['lstm_us_per_step_of_longest_row']:.3f} us/step of the longest row), "
+                f"{d['degree_traversal_ms']:.3f} ms as {d['degree_traversal_launches']} "
+                f"per-degree launches")
         if oracle:
             from threadpoolctl import threadpool_limits
 
@@ -381,6 +383,61 @@ def suite(dev, reps=10, oracle=True):
         del model, graph
         torch.cuda.empty_cache()
     return out
+
+
+def lstm_detail(S, torch, graph, g, x, dev, reps=5):
+    """The LSTM Gather alone: the single persistent call against the degree
+    traversal the paper profiles (Sec. 3.2, Fig. 8b: one launch per distinct
+    in-degree, rows of equal degree batched), through saga_lstm_gather_rows
+    on the same P = X W_ih + b_ih + b_hh."""
+    import ctypes as C
+
+    import numpy as np
+
+    H = g["W_hh"].shape[0]
+    V = graph.num_dst
+    st = torch.cuda.current_stream()
+    sh = S.stream_handle(st)
+    P = torch.empty((V, 4 * H), dtype=torch.float32, device=dev)
+    Wih = torch.from_numpy(g["W_ih"]).to(dev)
+    Whh = torch.from_numpy(g["W_hh"]).to(dev)
+    bih = torch.from_numpy(g["b_ih"]).to(dev)
+    bhh = torch.from_numpy(g["b_hh"]).to(dev)
+    gop = S.saga_gemm_op(S.SAGA_F32, S.SAGA_GEMM_PLAIN, S.SAGA_ACT_NONE, None)
+    gws = S.workspace(S.saga_apply_vertex_workspace_size(gop, Wih.shape[0], 0, 4 * H), dev)
+    none = S.saga_cmat(None, 0, 0, 0)
+    S.saga_apply_vertex(gop, S.cmat(x), S.cmat(Wih), none, none, C.c_void_p(bih.data_ptr()),
+                        C.c_void_p(bhh.data_ptr()), S.mat(P), C.c_void_p(gws.data_ptr()), gws.numel(), sh)
+    out = torch.empty((V, H), dtype=torch.float32, device=dev)
+    ws = S.workspace(S.saga_lstm_gather_workspace_size(graph.plan, H), dev)
+    # runs of equal in-degree in the plan's order (d_in descending, id ascending)
+    d = np.diff(g["row_ptr"].astype(np.int64))
+    ds = np.sort(d)[::-1]
+    cuts = np.concatenate([[0], np.flatnonzero(np.diff(ds)) + 1, [V]]).tolist()
+
+    def persistent():
+        S.saga_lstm_gather(graph.plan, S.cmat(P), S.cmat(Whh), S.mat(out),
+                           C.c_void_p(ws.data_ptr()), ws.numel(), sh)
+
+    def traversal():
+        for a, b in zip(cuts[:-1], cuts[1:]):
+            S.saga_lstm_gather_rows(graph.plan, a, b, S.cmat(P), S.cmat(Whh), S.mat(out),
+                                    C.c_void_p(ws.data_ptr()), ws.numel(), sh)
+
+    res = {}
+    for name, f, n in (("persistent", persistent, reps), ("traversal", traversal, 2)):
+        f()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n):
+            f()
+        torch.cuda.synchronize()
+        res[name] = (time.perf_counter() - t0) * 1e3 / n
+    dmax = int(d.max())
+    return {"max_in_degree": dmax, "lstm_gather_ms": res["persistent"],
+            "lstm_us_per_step_of_longest_row": res["persistent"] * 1e3 / dmax,
+            "degree_traversal_ms": res["traversal"], "degree_traversal_launches": len(cuts) - 1,
+            "degree_traversal_slowdown": res["traversal"] / res["persistent"]}
 
 
 def rgcn_detail(S, torch, graph, relg, layer, x, g, dev, reps):

@@ -396,8 +396,9 @@ saga_status saga_scatter_gather_unfused(const saga_plan* plan, const saga_edge_o
  * of the gates, computed once per source vertex: x_u W_ih + b_ih + b_hh
  * (saga_apply_vertex with bias and bias2), num_src x 4H.  w_hh: H x 4H.
  * out: num_dst x H.  All float32; H = 32, 64 or 128 (SAGA_EUNSUPPORTED
- * otherwise).  Rows run longest first on a persistent grid; the time is
- * bounded below by the longest row's d sequential steps.
+ * otherwise).  Rows run longest first on a persistent grid (one workgroup
+ * per CU); the time is bounded below by the longest row's d sequential
+ * steps.
  * Workspace: saga_lstm_gather_workspace_size() bytes (a work-queue counter,
  * cleared by the call itself), 256-byte aligned.
  * ---------------------------------------------------------------------- */
@@ -407,6 +408,17 @@ saga_status saga_lstm_gather_workspace_size(const saga_plan* plan, int64_t hidde
 saga_status saga_lstm_gather(const saga_plan* plan, saga_cmat gates_x, saga_cmat w_hh,
                              saga_mat out, void* workspace, size_t workspace_bytes,
                              void* stream);
+
+/* The LSTM Gather of the rows at perm positions [perm_begin, perm_end) only
+ * (0 <= perm_begin <= perm_end <= num_dst, else SAGA_EINVAL); the other
+ * output rows are not written.  perm lists rows by in-degree, largest
+ * first, so a run of equal in-degrees is a range: one call per distinct
+ * degree is the degree traversal of Sec. 3.2 (Fig. 8b), kept for
+ * comparison with the single persistent call.  Calls that share a
+ * workspace must be ordered (same stream). */
+saga_status saga_lstm_gather_rows(const saga_plan* plan, int32_t perm_begin, int32_t perm_end,
+                                  saga_cmat gates_x, saga_cmat w_hh, saga_mat out,
+                                  void* workspace, size_t workspace_bytes, void* stream);
 
 /* ======================================================================
  * ApplyVertex: dense transform on the matrix cores

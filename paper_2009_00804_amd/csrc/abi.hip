@@ -471,7 +471,12 @@ saga_status run_gather_unfused(const saga_plan& p, const saga_edge_op& op,
 constexpr size_t kLstmWs = 256;
 
 saga_status run_lstm(const saga_plan& p, const saga_cmat& gx, const saga_cmat& whh,
-                     const saga_mat& out, void* ws, size_t ws_bytes, hipStream_t st) {
+                     const saga_mat& out, void* ws, size_t ws_bytes, hipStream_t st,
+                     int64_t perm_begin = 0, int64_t perm_end = -1) {
+  if (perm_end < 0) perm_end = p.num_dst;
+  if (perm_begin < 0 || perm_begin > perm_end || perm_end > p.num_dst)
+    return fail(SAGA_EINVAL, "lstm gather: perm range [%lld, %lld) outside [0, %d]",
+                (long long)perm_begin, (long long)perm_end, p.num_dst);
   const int64_t H = whh.rows;
   if (H != 32 && H != 64 && H != 128)
     return fail(SAGA_EUNSUPPORTED, "lstm gather: hidden size must be 32, 64 or 128 (got %lld)",
@@ -505,6 +510,8 @@ saga_status run_lstm(const saga_plan& p, const saga_cmat& gx, const saga_cmat& w
   a.out = static_cast<float*>(out.ptr);
   a.ld_out = out.ld;
   a.queue = static_cast<int32_t*>(ws);
+  a.perm_begin = (int32_t)perm_begin;
+  a.perm_end = (int32_t)perm_end;
   hipError_t e = saga::launch_lstm_gather(a, st);
   if (e != hipSuccess) return dev_fail(e, "lstm gather launch");
   return ok();
@@ -1208,6 +1215,19 @@ saga_status saga_rel_transform(const saga_rel_plan* rel, saga_dtype dtype, saga_
       return fail(SAGA_EINVAL, "rel plan is not built");
     return run_rel_transform(*rel, dtype, x, w, out, workspace, workspace_bytes,
                              static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_lstm_gather_rows(const saga_plan* plan, int32_t perm_begin, int32_t perm_end,
+                                  saga_cmat gates_x, saga_cmat w_hh, saga_mat out,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    return run_lstm(*plan, gates_x, w_hh, out, workspace, workspace_bytes,
+                    static_cast<hipStream_t>(stream), perm_begin, perm_end);
   } catch (...) {
     return fail(SAGA_EINTERNAL, "exception");
   }

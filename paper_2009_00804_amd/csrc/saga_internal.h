@@ -130,6 +130,7 @@ struct LstmArgs {
   const float* w_hh; int64_t ld_whh;   // H x 4H
   float* out; int64_t ld_out;          // num_dst x H
   int32_t* queue;                      // work-queue counter (workspace)
+  int32_t perm_begin, perm_end;        // rows at these perm positions
 };
 hipError_t launch_lstm_gather(const LstmArgs& a, hipStream_t st);
 

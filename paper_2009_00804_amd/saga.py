@@ -37,7 +37,7 @@ EXPORTS = [
     "saga_plan_workspace_size", "saga_plan_build", "saga_plan_check",
     "saga_gather_workspace_size", "saga_scatter_apply_edge_gather",
     "saga_unfused_workspace_size", "saga_scatter_gather_unfused",
-    "saga_lstm_gather_workspace_size", "saga_lstm_gather",
+    "saga_lstm_gather_workspace_size", "saga_lstm_gather", "saga_lstm_gather_rows",
     "saga_rel_plan_workspace_size", "saga_rel_plan_build", "saga_rel_plan_check",
     "saga_rel_transform_workspace_size", "saga_rel_transform",
     "saga_apply_vertex_workspace_size", "saga_apply_vertex",
@@ -148,6 +148,8 @@ def lib():
         "saga_lstm_gather_workspace_size": (S, [P(saga_plan), C.c_int64, P(C.c_size_t)]),
         "saga_lstm_gather": (S, [P(saga_plan), saga_cmat, saga_cmat, saga_mat, C.c_void_p, C.c_size_t,
                                  C.c_void_p]),
+        "saga_lstm_gather_rows": (S, [P(saga_plan), C.c_int32, C.c_int32, saga_cmat, saga_cmat,
+                                      saga_mat, C.c_void_p, C.c_size_t, C.c_void_p]),
         "saga_rel_plan_workspace_size": (S, [P(saga_plan), C.c_int32, P(C.c_size_t)]),
         "saga_rel_plan_build": (S, [P(saga_plan), C.c_void_p, C.c_int32, C.c_void_p, C.c_size_t,
                                     C.c_void_p, P(saga_rel_plan)]),
@@ -282,6 +284,13 @@ def saga_rel_transform_workspace_size(rel, dtype, k, n):
 def saga_rel_transform(rel, dtype, x, w, out, workspace, ws_bytes, stream):
     return _check(lib().saga_rel_transform(C.byref(rel), dtype, x, w, out, workspace, ws_bytes,
                                            stream), "saga_rel_transform")
+
+
+def saga_lstm_gather_rows(plan, perm_begin, perm_end, gates_x, w_hh, out, workspace, ws_bytes,
+                          stream):
+    return _check(lib().saga_lstm_gather_rows(C.byref(plan), perm_begin, perm_end, gates_x, w_hh, out,
+                                              workspace, ws_bytes, stream),
+                  "saga_lstm_gather_rows")
 
 
 def saga_apply_vertex_workspace_size(op, k, k2, n):

@@ -169,6 +169,11 @@ def test_lstm_gather_rejects_bad_arguments(S):
     assert call(nb=8) == S.SAGA_EWORKSPACE
     assert call(ws=0x900010) == S.SAGA_EINVAL                                   # misaligned
     assert call(o=S.saga_mat(0x50000 + 256, 16, 128, 128)) == S.SAGA_EINVAL      # overlaps gates_x
+    rows = lambda b, e: L.saga_lstm_gather_rows(C.byref(p), b, e, gx, whh, out, 0x900000, 256,  # noqa: E731
+                                                 None)
+    assert rows(-1, 4) == S.SAGA_EINVAL
+    assert rows(5, 4) == S.SAGA_EINVAL
+    assert rows(0, 17) == S.SAGA_EINVAL                                          # past num_dst
 
 
 def test_gemm_rejects_bad_arguments(S):

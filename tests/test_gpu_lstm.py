@@ -97,3 +97,44 @@ def test_sage_lstm_layer():
     y = to_np(LY.run(LY.sage_lstm(gr, g), dev_padded(g["X"])))
     want = O.sage_lstm_layer_of(g)
     assert rel_err(y, want) <= FP32_TOL
+
+
+def test_lstm_rows_degree_traversal_equals_single_call():
+    """One saga_lstm_gather_rows call per run of equal in-degree (the degree
+    traversal of Sec. 3.2) writes the same bytes as the single call; a
+    partial range writes only its own rows."""
+    S = lib()
+    name, n, rp, col = _graphs()[-2]
+    H = 64
+    rng = np.random.default_rng(11)
+    P = rng.standard_normal((n, 4 * H)).astype(np.float32)
+    W_hh = rng.uniform(-0.12, 0.12, (H, 4 * H)).astype(np.float32)
+    g = graph(rp, col, num_src=n)
+    print("lstm degree traversal", flush=True)
+    full = run_lstm(g, P, W_hh)
+    arr = g.arrays()
+    perm = arr["perm"].cpu().numpy()
+    dsorted = arr["d_in"].cpu().numpy()[perm]
+    cuts = np.concatenate([[0], np.flatnonzero(np.diff(dsorted)) + 1, [n]])
+    Pt = dev_padded(P)
+    Wt = torch.from_numpy(W_hh).to(device())
+    out = dev_padded(np.zeros((n, H)), fill=5.0)
+    ws = S.workspace(S.saga_lstm_gather_workspace_size(g.plan, H), device())
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        S.saga_lstm_gather_rows(g.plan, int(a), int(b), S.cmat(Pt), S.cmat(Wt), S.mat(out),
+                                C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(out), full)
+    # a partial range leaves the other rows untouched
+    out2 = dev_padded(np.full((n, H), 5.0))
+    S.saga_lstm_gather_rows(g.plan, int(cuts[1]), int(cuts[3]), S.cmat(Pt), S.cmat(Wt), S.mat(out2),
+                            C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
+    torch.cuda.synchronize()
+    got = to_np(out2)
+    inside = perm[cuts[1]:cuts[3]]
+    outside = np.setdiff1d(np.arange(n), inside)
+    assert np.array_equal(got[inside], full[inside])
+    assert np.all(got[outside] == 5.0)
+    with pytest.raises(S.SagaError):
+        S.saga_lstm_gather_rows(g.plan, 3, 2, S.cmat(Pt), S.cmat(Wt), S.mat(out2),
+                                C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
