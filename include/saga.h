@@ -11,6 +11,8 @@
  *
  *   saga_plan_build                 graph layout: degrees, degree-sorted row
  *                                   order, row segments and row blocks
+ *                                   (saga_plan_build_split: the out-degree
+ *                                   and row-order branches on two streams)
  *   saga_scatter_apply_edge_gather  fused Scatter + ApplyEdge + Gather: a
  *                                   per-destination segment reduction over
  *                                   the in-CSR (the fused Gather is the
@@ -204,6 +206,30 @@ saga_status saga_plan_build(int32_t num_dst, int32_t num_src, int64_t num_edges,
                             const int32_t* row_ptr, const int32_t* col_idx,
                             const saga_plan_opts* opts, void* workspace,
                             size_t workspace_bytes, void* stream, saga_plan* plan);
+
+/* The same plan built as two concurrent branches, so that the stage that
+ * follows the out-degrees can overlap the row order (the paper's outlook of
+ * pipelining stages instead of running them one after another, Sec. 3
+ * "Forward Looking"):
+ *   - on `stream`: the counters are cleared, then the out-degree count
+ *     (d_out); a d_out-scaled transform enqueued on `stream` after this call
+ *     waits for d_out only;
+ *   - on `order_stream` (made to wait for the cleared counters through
+ *     fork_event): in-degrees, CSR validation, the degree order, segments and
+ *     row blocks; join_event is recorded on order_stream when they are done.
+ * Before anything that uses perm, segments or blocks (every Gather) runs on
+ * `stream`, the caller makes `stream` wait for join_event
+ * (hipStreamWaitEvent).  fork_event and join_event are caller-created
+ * hipEvent_t; order_stream must differ from `stream`; keep both streams at
+ * the same priority.  Graphs small enough that the out-degrees are counted
+ * in one pass run entirely on `stream` (join_event is then recorded there).
+ * The arrays are the same, bit for bit, as saga_plan_build's.  Errors as
+ * saga_plan_build, and SAGA_EINVAL if a stream or event is missing. */
+saga_status saga_plan_build_split(int32_t num_dst, int32_t num_src, int64_t num_edges,
+                                  const int32_t* row_ptr, const int32_t* col_idx,
+                                  const saga_plan_opts* opts, void* workspace,
+                                  size_t workspace_bytes, void* stream, void* order_stream,
+                                  void* fork_event, void* join_event, saga_plan* plan);
 
 /* Synchronise `stream` and read the plan's counters.  Returns SAGA_EGRAPH
  * if the device validation found a CSR error (details in counts->error_flags

@@ -945,10 +945,35 @@ saga_status saga_plan_workspace_size(int32_t num_dst, int32_t num_src, int64_t n
   }
 }
 
+saga_status build_plan(int32_t num_dst, int32_t num_src, int64_t num_edges,
+                       const int32_t* row_ptr, const int32_t* col_idx, const saga_plan_opts* opts,
+                       void* workspace, size_t workspace_bytes, void* stream, void* order_stream,
+                       void* fork_event, void* join_event, saga_plan* plan);
+
 saga_status saga_plan_build(int32_t num_dst, int32_t num_src, int64_t num_edges,
                             const int32_t* row_ptr, const int32_t* col_idx,
                             const saga_plan_opts* opts, void* workspace, size_t workspace_bytes,
                             void* stream, saga_plan* plan) {
+  return build_plan(num_dst, num_src, num_edges, row_ptr, col_idx, opts, workspace,
+                    workspace_bytes, stream, nullptr, nullptr, nullptr, plan);
+}
+
+saga_status saga_plan_build_split(int32_t num_dst, int32_t num_src, int64_t num_edges,
+                                  const int32_t* row_ptr, const int32_t* col_idx,
+                                  const saga_plan_opts* opts, void* workspace,
+                                  size_t workspace_bytes, void* stream, void* order_stream,
+                                  void* fork_event, void* join_event, saga_plan* plan) {
+  if (!order_stream || !fork_event || !join_event)
+    return fail(SAGA_EINVAL, "plan split: order_stream, fork_event and join_event are required");
+  if (order_stream == stream) return fail(SAGA_EINVAL, "plan split: order_stream is the stream");
+  return build_plan(num_dst, num_src, num_edges, row_ptr, col_idx, opts, workspace,
+                    workspace_bytes, stream, order_stream, fork_event, join_event, plan);
+}
+
+saga_status build_plan(int32_t num_dst, int32_t num_src, int64_t num_edges,
+                       const int32_t* row_ptr, const int32_t* col_idx, const saga_plan_opts* opts,
+                       void* workspace, size_t workspace_bytes, void* stream, void* order_stream,
+                       void* fork_event, void* join_event, saga_plan* plan) {
   try {
     if (!plan) return fail(SAGA_EINVAL, "plan is null");
     int32_t T, B, c;
@@ -988,7 +1013,10 @@ saga_status saga_plan_build(int32_t num_dst, int32_t num_src, int64_t num_edges,
     p.counts = reinterpret_cast<int32_t*>(w + L.off_counts);
     p.scratch = w + L.off_scratch;
     p.scratch_bytes = L.scratch_bytes;
-    hipError_t e = saga::launch_plan_build(p, L, static_cast<hipStream_t>(stream));
+    hipError_t e = saga::launch_plan_build(p, L, static_cast<hipStream_t>(stream),
+                                           static_cast<hipStream_t>(order_stream),
+                                           static_cast<hipEvent_t>(fork_event),
+                                           static_cast<hipEvent_t>(join_event));
     if (e != hipSuccess) return dev_fail(e, "plan launch");
     *plan = p;
     return ok();

@@ -626,6 +626,7 @@ bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t
   take(V); take(V); take(V); take(V);
   take(hist_n);
   take(scan_tiles + 1);
+  take(L->outdeg_bucketed ? scan_tiles + 1 : 0);  // tile sums of the out-degree branch
   take(L->max_segments);
   take(L->outdeg_bucketed ? cdiv(E, 2) : 0);
   take(L->outdeg_bucketed ? L->outdeg_nb * L->edge_tiles : 0);
@@ -635,7 +636,8 @@ bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t
   return true;
 }
 
-hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_t st) {
+hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_t st,
+                             hipStream_t order_st, hipEvent_t fork, hipEvent_t join) {
   const int32_t V = p.num_dst, Vs = p.num_src, T = p.seg_len;
   const int64_t E = p.num_edges;
   char* sc = static_cast<char*>(p.scratch);
@@ -657,6 +659,7 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   if (L.outdeg_bucketed && cdiv(L.outdeg_nb * L.edge_tiles, kTile) > scan_tiles)
     scan_tiles = cdiv(L.outdeg_nb * L.edge_tiles, kTile);
   int32_t* tile_sums = reinterpret_cast<int32_t*>(take(scan_tiles + 1));
+  int32_t* tile_sums2 = reinterpret_cast<int32_t*>(take(L.outdeg_bucketed ? scan_tiles + 1 : 0));
   int32_t* P = reinterpret_cast<int32_t*>(take(L.max_segments));
   uint16_t* bucketed = reinterpret_cast<uint16_t*>(take(L.outdeg_bucketed ? cdiv(E, 2) : 0));
   int32_t* ohist = reinterpret_cast<int32_t*>(take(L.outdeg_bucketed ? L.outdeg_nb * L.edge_tiles : 0));
@@ -666,16 +669,37 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   hipLaunchKernelGGL(k_zero, dim3(1), dim3(64), 0, st, p.counts, (int64_t)kCountSlots);
   if (Vs > 0 && !L.outdeg_bucketed)
     hipLaunchKernelGGL(k_zero, dim3(grid_for(Vs)), dim3(kThreads), 0, st, p.d_out, (int64_t)Vs);
-  if (V == 0) return hipGetLastError();
+  // Two independent branches: the out-degree count (col_idx only) and the
+  // row order (row_ptr only: in-degrees, CSR validation, degree sort,
+  // segments, row blocks).  With an order stream, the row order runs there
+  // after the counters are cleared, so that whatever the caller enqueues on
+  // `st` after the out-degrees (the d_out-scaled transform) overlaps it.
+  // The graphs whose out-degrees are counted inside k_degrees (no buckets)
+  // run both on `st`.
+  const bool split = order_st && fork && join && L.outdeg_bucketed && V > 0;
+  hipStream_t qst = st;
+  if (split) {
+    hipError_t e = hipEventRecord(fork, st);
+    if (e == hipSuccess) e = hipStreamWaitEvent(order_st, fork, 0);
+    if (e != hipSuccess) return e;
+    qst = order_st;
+  }
+  if (V == 0) {
+    if (join) {
+      hipError_t e = hipEventRecord(join, st);
+      if (e != hipSuccess) return e;
+    }
+    return hipGetLastError();
+  }
   const int edges_too = L.outdeg_bucketed ? 0 : 1;
-  hipLaunchKernelGGL(k_degrees, dim3(grid_for(edges_too && E > V ? E : V, 2048)), dim3(kThreads), 0, st,
+  hipLaunchKernelGGL(k_degrees, dim3(grid_for(edges_too && E > V ? E : V, 2048)), dim3(kThreads), 0, qst,
                      p.row_ptr, p.col_idx, V, Vs, E, edges_too, p.d_in, p.d_out, p.counts);
   if (L.outdeg_bucketed) {
     const int nb = (int)L.outdeg_nb;
     const int64_t et = L.edge_tiles;
     hipLaunchKernelGGL(k_outdeg_hist, dim3(et), dim3(kThreads), (kThreads / 64) * nb * 4, st,
                        p.col_idx, E, Vs, nb, ohist, et, p.counts);
-    scan(ArrF{ohist}, (int64_t)nb * et, nullptr, ohist, nullptr, tile_sums, p.counts, st);
+    scan(ArrF{ohist}, (int64_t)nb * et, nullptr, ohist, nullptr, tile_sums2, p.counts, st);
     hipLaunchKernelGGL(k_outdeg_scatter, dim3(et), dim3(kThreads),
                        3 * nb * 4 + 2 * kEdgeTile * 2, st, p.col_idx, E, nb, ohist, et, bucketed,
                        p.counts);
@@ -684,6 +708,7 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
     hipLaunchKernelGGL(k_outdeg_reduce, dim3(grid_for(Vs)), dim3(kThreads), 0, st, opart, nb, Vs,
                        p.d_out, p.counts);
   }
+  st = qst;  // the row order
 
   // degree order: 4 stable passes of 8 bits over key = 0x7fffffff - d_in
   const uint32_t* kin[4] = {nullptr, keysA, keysB, keysA};
@@ -724,7 +749,9 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
        nullptr, tile_sums, p.counts, st);
   hipLaunchKernelGGL(k_blocks, dim3(grid_for(L.max_segments)), dim3(kThreads), 0, st, P,
                      p.block_cost, L.max_segments, L.max_blocks, p.block_ptr, p.counts);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && join) e = hipEventRecord(join, st);
+  return e;
 }
 
 }  // namespace saga

@@ -36,7 +36,10 @@ struct PlanLayout {
 bool plan_layout(int32_t num_dst, int32_t num_src, int64_t num_edges, int32_t seg_len,
                  int32_t block_cost, int32_t row_cost, PlanLayout* L);
 
-hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_t st);
+// order_st, fork, join: see saga_plan_build_split (all null: one stream)
+hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_t st,
+                             hipStream_t order_st = nullptr, hipEvent_t fork = nullptr,
+                             hipEvent_t join = nullptr);
 
 // ---- gather.hip ----
 struct GatherArgs {

@@ -34,7 +34,7 @@ SAGA_REL_MAX_RELATIONS = 2048
 ACT = {"none": 0, "relu": 1, "elu": 2, "sigmoid": 3, "tanh": 4}
 
 EXPORTS = [
-    "saga_plan_workspace_size", "saga_plan_build", "saga_plan_check",
+    "saga_plan_workspace_size", "saga_plan_build", "saga_plan_build_split", "saga_plan_check",
     "saga_gather_workspace_size", "saga_scatter_apply_edge_gather",
     "saga_unfused_workspace_size", "saga_scatter_gather_unfused",
     "saga_lstm_gather_workspace_size", "saga_lstm_gather", "saga_lstm_gather_rows",
@@ -138,6 +138,9 @@ def lib():
         "saga_plan_workspace_size": (S, [C.c_int32, C.c_int32, C.c_int64, P(saga_plan_opts), P(C.c_size_t)]),
         "saga_plan_build": (S, [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p, P(saga_plan_opts),
                                 C.c_void_p, C.c_size_t, C.c_void_p, P(saga_plan)]),
+        "saga_plan_build_split": (S, [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p,
+                                      P(saga_plan_opts), C.c_void_p, C.c_size_t, C.c_void_p,
+                                      C.c_void_p, C.c_void_p, C.c_void_p, P(saga_plan)]),
         "saga_plan_check": (S, [P(saga_plan), C.c_void_p, P(saga_plan_counts)]),
         "saga_gather_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64, P(C.c_size_t)]),
         "saga_scatter_apply_edge_gather": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs), saga_mat,
@@ -207,6 +210,16 @@ def saga_plan_build(num_dst, num_src, num_edges, row_ptr, col_idx, opts, workspa
     _check(lib().saga_plan_build(num_dst, num_src, num_edges, row_ptr, col_idx,
                                  C.byref(opts) if opts else None, workspace, ws_bytes, stream,
                                  C.byref(plan)), "saga_plan_build")
+    return plan
+
+
+def saga_plan_build_split(num_dst, num_src, num_edges, row_ptr, col_idx, opts, workspace, ws_bytes,
+                          stream, order_stream, fork_event, join_event):
+    plan = saga_plan()
+    _check(lib().saga_plan_build_split(num_dst, num_src, num_edges, row_ptr, col_idx,
+                                       C.byref(opts) if opts else None, workspace, ws_bytes, stream,
+                                       order_stream, fork_event, join_event, C.byref(plan)),
+           "saga_plan_build_split")
     return plan
 
 

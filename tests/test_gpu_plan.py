@@ -79,3 +79,84 @@ def test_plan_rejects_invalid_csr():
         st, counts = S.saga_plan_check(g.plan, S.stream_handle())
         assert st == S.SAGA_EGRAPH
         assert counts.error_flags & bit
+
+
+def test_split_plan_equals_single_stream_plan_and_overlaps_the_transform():
+    """saga_plan_build_split (out-degree branch on the stream, row order on a
+    second stream) gives the arrays of saga_plan_build bit for bit, and a
+    2-layer GCN whose transform is enqueued between the branches gives the
+    same output as the sequential order."""
+    import ctypes as C
+
+    import torch
+
+    from gpu_util import dev_int, device, lib, to_np
+    from synth import configs as Cfg
+    from paper_2009_00804_amd import layers as LY
+
+    S = lib()
+    g = Cfg.build("gcn_rmat", small=True)
+    V, E = g["num_vertices"], g["num_edges"]
+    print(f"split plan V={V} E={E}", flush=True)
+    rp, col = dev_int(g["row_ptr"]), dev_int(g["col_idx"])
+    ref = S.Graph(rp, col)
+    want = {k: v.cpu().numpy() for k, v in ref.arrays().items()}
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    fork, join = torch.cuda.Event(), torch.cuda.Event()
+    fork.record(main)
+    join.record(main)  # creates both events
+    for _ in range(2):  # twice, each into a workspace filled with garbage
+        ws = torch.full((ref.ws.numel(),), 0xAB, dtype=torch.uint8, device=device())
+        plan = S.saga_plan_build_split(V, V, E, C.c_void_p(rp.data_ptr()), C.c_void_p(col.data_ptr()),
+                                       ref.opts, C.c_void_p(ws.data_ptr()), ws.numel(),
+                                       S.stream_handle(main), S.stream_handle(side),
+                                       C.c_void_p(fork.cuda_event), C.c_void_p(join.cuda_event))
+        main.wait_event(join)
+        st, counts = S.saga_plan_check(plan, S.stream_handle(main))
+        assert st == S.SAGA_OK
+        gr = S.Graph.__new__(S.Graph)
+        gr.__dict__.update(ref.__dict__)
+        gr.plan, gr.ws, gr.counts = plan, ws, counts
+        got = {k: v.cpu().numpy() for k, v in gr.arrays().items()}
+        for k in want:
+            assert np.array_equal(got[k], want[k]), k
+    # layer 1 of the GCN with its transform enqueued between the branches
+    X = torch.from_numpy(np.ascontiguousarray(g["X"][:, :g["dims"][0]])).to(device())
+    X = torch.nn.functional.pad(X, (0, (-X.shape[1]) % 4))[:, :g["dims"][0]]
+    W1 = torch.from_numpy(g["W1"]).to(device())
+    b1 = torch.from_numpy(g["b1"]).to(device())
+    F = W1.shape[1]
+    none = S.saga_cmat(None, 0, 0, 0)
+
+    def layer1(pl, wait=None):
+        Z = torch.empty((V, F), device=device())
+        H = torch.empty((V, F), device=device())
+        gop = S.saga_gemm_op(S.SAGA_F32, S.SAGA_GEMM_PLAIN, S.SAGA_ACT_NONE, pl.d_out)
+        mws = S.workspace(S.saga_apply_vertex_workspace_size(gop, X.shape[1], 0, F), device())
+        S.saga_apply_vertex(gop, S.cmat(X), S.cmat(W1), none, none, None, None, S.mat(Z),
+                            C.c_void_p(mws.data_ptr()), mws.numel(), S.stream_handle(main))
+        if wait is not None:
+            main.wait_event(wait)
+        op = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 1, 0.0, S.SAGA_ACT_RELU)
+        inp = S.saga_edge_inputs()
+        inp.src = S.cmat(Z)
+        inp.bias = b1.data_ptr()
+        gws = S.workspace(S.saga_gather_workspace_size(pl, op, F), device())
+        S.saga_scatter_apply_edge_gather(pl, op, inp, S.mat(H), C.c_void_p(gws.data_ptr()), gws.numel(),
+                                         S.stream_handle(main))
+        torch.cuda.synchronize()
+        return to_np(H)
+
+    seq = layer1(ref.plan)
+    ws2 = torch.empty_like(ref.ws)
+    plan2 = S.saga_plan_build_split(V, V, E, C.c_void_p(rp.data_ptr()), C.c_void_p(col.data_ptr()),
+                                    ref.opts, C.c_void_p(ws2.data_ptr()), ws2.numel(),
+                                    S.stream_handle(main), S.stream_handle(side),
+                                    C.c_void_p(fork.cuda_event), C.c_void_p(join.cuda_event))
+    assert np.array_equal(layer1(plan2, wait=join), seq)
+    with pytest.raises(S.SagaError):
+        S.saga_plan_build_split(V, V, E, C.c_void_p(rp.data_ptr()), C.c_void_p(col.data_ptr()),
+                                ref.opts, C.c_void_p(ws.data_ptr()), ws.numel(),
+                                S.stream_handle(main), S.stream_handle(main),
+                                C.c_void_p(fork.cuda_event), C.c_void_p(join.cuda_event))
