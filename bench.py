@@ -92,7 +92,18 @@ class Step:
         self.Z1 = torch.empty((self.V, S.gather_ld(hid, es)), dtype=tdt, device=dev)[:, :hid]
         self.H1_base = torch.empty((self.V, ld(hid)), dtype=tdt, device=dev)
         self.H1 = self.H1_base[:, :hid]
-        self.Z2 = torch.empty((self.V, S.gather_ld(f_out, es)), dtype=tdt, device=dev)[:, :f_out]
+        # Z2 rows longer than one 128-byte line but not whole lines (41 float32
+        # columns) are written as two matrices: the whole-line columns and
+        # the rest, each gathered by its own call (what saga_layer does)
+        per_line = 128 // es
+        self.split2 = f_out // per_line * per_line if f_out > per_line and f_out % per_line else 0
+        if self.split2:
+            self.Z2 = torch.empty((self.V, S.gather_ld(self.split2, es)), dtype=tdt,
+                                  device=dev)[:, :self.split2]
+            rest = f_out - self.split2
+            self.Z2t = torch.empty((self.V, S.gather_ld(rest, es)), dtype=tdt, device=dev)[:, :rest]
+        else:
+            self.Z2 = torch.empty((self.V, S.gather_ld(f_out, es)), dtype=tdt, device=dev)[:, :f_out]
         self.Y = torch.empty((self.V, ld(f_out)), dtype=tdt, device=dev)[:, :f_out]
         self.graph = S.Graph(self.rp, self.col)     # allocates + builds + checks once
         self.plan_ws = self.graph.ws
@@ -107,6 +118,10 @@ class Step:
         n2 = S.saga_gather_workspace_size(p, self.op2, f_out)
         self.gws = S.workspace(max(n1, n2), dev)
         self.gop = S.saga_gemm_op(S.dtype_code(tdt), S.SAGA_GEMM_PLAIN, S.SAGA_ACT_NONE, p.d_out)
+        self.gop2 = S.saga_gemm_op(S.dtype_code(tdt), S.SAGA_GEMM_PLAIN, S.SAGA_ACT_NONE, p.d_out)
+        if self.split2:
+            self.gop2.split_col = self.split2
+            self.gop2.tail = S.mat(self.Z2t)
         m1 = S.saga_apply_vertex_workspace_size(self.gop, self.W1.shape[0], 0, self.W1.shape[1])
         m2 = S.saga_apply_vertex_workspace_size(self.gop, self.W2.shape[0], 0, self.W2.shape[1])
         self.mws = S.workspace(max(m1, m2), dev)
@@ -117,6 +132,14 @@ class Step:
         self.in2 = S.saga_edge_inputs()
         self.in2.src = S.cmat(self.Z2)
         self.in2.bias = self.b2.data_ptr()
+        self.out2 = S.mat(self.Y)
+        if self.split2:
+            sp = self.split2
+            self.out2 = S.mat(self.Y[:, :sp])
+            self.in2t = S.saga_edge_inputs()
+            self.in2t.src = S.cmat(self.Z2t)
+            self.in2t.bias = self.b2[sp:].data_ptr()
+            self.out2t = S.mat(self.Y[:, sp:])
         self.stream = torch.cuda.current_stream()
         self.sh = S.stream_handle(self.stream)
         self.names = ["plan", "gemm1", "gather1", "gemm2", "gather2"]
@@ -184,13 +207,17 @@ class Step:
                                          C.c_void_p(self.gws.data_ptr()), self.gws.numel(), self.sh)
         if ev:
             ev[3].record(self.stream)
-        S.saga_apply_vertex(self.gop, S.cmat(self.H1), S.cmat(self.W2), self.none, self.none, None,
+        S.saga_apply_vertex(self.gop2, S.cmat(self.H1), S.cmat(self.W2), self.none, self.none, None,
                             None, S.mat(self.Z2), C.c_void_p(self.mws.data_ptr()), self.mws.numel(),
                             self.sh)
         if ev:
             ev[4].record(self.stream)
-        S.saga_scatter_apply_edge_gather(p, self.op2, self.in2, S.mat(self.Y),
+        S.saga_scatter_apply_edge_gather(p, self.op2, self.in2, self.out2,
                                          C.c_void_p(self.gws.data_ptr()), self.gws.numel(), self.sh)
+        if self.split2:
+            S.saga_scatter_apply_edge_gather(p, self.op2, self.in2t, self.out2t,
+                                             C.c_void_p(self.gws.data_ptr()), self.gws.numel(),
+                                             self.sh)
         if ev:
             ev[5].record(self.stream)
 

@@ -459,6 +459,12 @@ saga_status saga_lstm_gather_rows(const saga_plan* plan, int32_t perm_begin, int
  *              width F = a2.cols), r = s(gi_r + gh_r), z = s(gi_z + gh_z),
  *              n = tanh(gi_n + r * gh_n), out = (1 - z) n + z a2.
  * rs = row_scale_deg ? (deg[i] > 0 ? deg[i]^-1/2 : 0) : 1  (row i).
+ * Split output (split_col = s > 0, PLAIN and CONCAT): the result is written
+ * as two matrices, columns [0, s) to out and [s, N) to op->tail.  A result
+ * that a Gather reads by rows can so be cut at a 128-byte boundary (s = 32
+ * float32 or 64 bfloat16 columns) into a part of whole L2 lines and a
+ * narrow rest, each gathered by its own call (e.g. N = 41: 32 + 9 columns
+ * instead of one 192-byte row that spans two lines).
  * a: M x K, w: K x N (dense weights, ld may exceed N), out: M x N; bf16 or
  * f32 storage per op->dtype, float32 accumulation; N <= 4096 per call.
  *
@@ -476,6 +482,9 @@ typedef struct saga_gemm_op {
   saga_gemm_mode mode;
   saga_act act;                   /* PLAIN / CONCAT */
   const int32_t* row_scale_deg;   /* nullable, int32[M] */
+  int32_t split_col;              /* PLAIN / CONCAT: 0 = one output matrix; s > 0: columns
+                                     [0, s) go to `out` (M x s) and [s, N) to `tail` */
+  saga_mat tail;                  /* M x (N - s), same dtype; used when split_col > 0 */
 } saga_gemm_op;
 
 /* Workspace bytes for saga_apply_vertex with op's dtype and mode, k =

@@ -316,14 +316,27 @@ saga_status validate_gemm(const saga_gemm_op& op, const saga_cmat& a, const saga
   } else if (N > 4096) {
     return fail(SAGA_EUNSUPPORTED, "gemm: N too large");
   }
-  s = check_mat(out.ptr, out.rows, out.cols, out.ld, M, out_cols, es, false, "out");
+  if (op.split_col < 0 || (op.split_col > 0 && (op.mode == SAGA_GEMM_GRU || op.split_col >= out_cols)))
+    return fail(SAGA_EINVAL, "split_col must be 0, or in (0, N) for PLAIN / CONCAT");
+  const int64_t head = op.split_col > 0 ? op.split_col : out_cols;
+  s = check_mat(out.ptr, out.rows, out.cols, out.ld, M, head, es, false, "out");
   if (s) return s;
   const size_t ob = mat_bytes(out.rows, out.cols, out.ld, es);
-  if (range_overlap(out.ptr, ob, a.ptr, mat_bytes(a.rows, a.cols, a.ld, es)) ||
-      range_overlap(out.ptr, ob, w.ptr, mat_bytes(w.rows, w.cols, w.ld, es)) ||
-      range_overlap(out.ptr, ob, a2.ptr, mat_bytes(a2.rows, a2.cols, a2.ld, es)) ||
-      range_overlap(out.ptr, ob, w2.ptr, mat_bytes(w2.rows, w2.cols, w2.ld, es)))
-    return fail(SAGA_EINVAL, "output overlaps an input");
+  const saga_mat& t = op.tail;
+  const size_t tb = op.split_col > 0 ? mat_bytes(t.rows, t.cols, t.ld, es) : 0;
+  if (op.split_col > 0) {
+    s = check_mat(t.ptr, t.rows, t.cols, t.ld, M, out_cols - op.split_col, es, false, "tail");
+    if (s) return s;
+    if (range_overlap(out.ptr, ob, t.ptr, tb)) return fail(SAGA_EINVAL, "tail overlaps out");
+  }
+  const void* outs[2] = {out.ptr, op.split_col > 0 ? t.ptr : nullptr};
+  const size_t outb[2] = {ob, tb};
+  for (int i = 0; i < 2; ++i)
+    if (range_overlap(outs[i], outb[i], a.ptr, mat_bytes(a.rows, a.cols, a.ld, es)) ||
+        range_overlap(outs[i], outb[i], w.ptr, mat_bytes(w.rows, w.cols, w.ld, es)) ||
+        range_overlap(outs[i], outb[i], a2.ptr, mat_bytes(a2.rows, a2.cols, a2.ld, es)) ||
+        range_overlap(outs[i], outb[i], w2.ptr, mat_bytes(w2.rows, w2.cols, w2.ld, es)))
+      return fail(SAGA_EINVAL, "output overlaps an input");
   return SAGA_OK;
 }
 
@@ -344,6 +357,8 @@ saga_status run_gemm(const saga_gemm_op& op, const saga_cmat& a, const saga_cmat
   {
     const size_t es = esize(op.dtype);
     if (range_overlap(ws, need, out.ptr, mat_bytes(out.rows, out.cols, out.ld, es)) ||
+        (op.split_col > 0 &&
+         range_overlap(ws, need, op.tail.ptr, mat_bytes(op.tail.rows, op.tail.cols, op.tail.ld, es))) ||
         range_overlap(ws, need, a.ptr, mat_bytes(a.rows, a.cols, a.ld, es)) ||
         range_overlap(ws, need, w.ptr, mat_bytes(w.rows, w.cols, w.ld, es)) ||
         range_overlap(ws, need, a2.ptr, mat_bytes(a2.rows, a2.cols, a2.ld, es)) ||
@@ -372,6 +387,11 @@ saga_status run_gemm(const saga_gemm_op& op, const saga_cmat& a, const saga_cmat
   g.row_scale_deg = op.row_scale_deg;
   g.out = out.ptr;
   g.ldo = out.ld;
+  if (op.split_col > 0) {
+    g.split = op.split_col;
+    g.out2 = op.tail.ptr;
+    g.ldo2 = op.tail.ld;
+  }
   g.ws = ws;
   g.ws_bytes = ws_bytes;
   hipError_t e = saga::launch_gemm(g, st);
@@ -626,6 +646,18 @@ struct LayerBufs {
 
 bool gcn_transform_first(const saga_layer_desc& d) { return d.out_feat <= d.in_feat; }
 
+// Columns of a gathered row that fill whole 128-byte L2 lines, when the row
+// is longer than one line but not a whole number of lines (0 otherwise):
+// the transform then writes those columns and the rest as two matrices, and
+// each is gathered by its own call, so no gathered row straddles a line
+// shared with its neighbour (F = 41 float32: 32 + 9 columns instead of one
+// 192-byte row over two lines).
+int64_t line_split(int64_t cols, saga_dtype t) {
+  const int64_t es = t == SAGA_BF16 ? 2 : 4, per_line = 128 / es;
+  if (cols <= per_line || cols % per_line == 0) return 0;
+  return cols / per_line * per_line;
+}
+
 size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, LayerBufs* b) {
   Carve c(base, (size_t)-1);
   const int64_t V = p.num_dst;
@@ -637,8 +669,13 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
   switch (d.kind) {
     case SAGA_LAYER_GCN:
       if (gcn_transform_first(d)) {
-        b->ldz = ld_for(d.out_feat, t);
+        const int64_t sp = line_split(d.out_feat, t);
+        b->ldz = ld_for(sp > 0 ? sp : d.out_feat, t);
         b->z = c.take((size_t)V * b->ldz * es);
+        if (sp > 0) {  // the columns past the last whole line
+          b->ldz3 = ld_for(d.out_feat - sp, t);
+          b->z3 = c.take((size_t)V * b->ldz3 * es);
+        }
         gfeat = d.out_feat;
       } else {
         b->ldz2 = ld_for(d.in_feat, t);
@@ -779,18 +816,35 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
     case SAGA_LAYER_GCN: {
       if (gcn_transform_first(d)) {
         // Z = d_out^-1/2 (X W); out = act(d_in^-1/2 sum_u Z_u + b)
+        const int64_t sp = line_split(Fo, d.dtype);
         g.mode = SAGA_GEMM_PLAIN;
         g.row_scale_deg = p.d_out;
+        if (sp > 0) {
+          g.split_col = (int32_t)sp;
+          g.tail = saga_mat{b.z3, V, Fo - sp, b.ldz3};
+        }
         s = run_gemm(g, x, saga_cmat{d.w, Fi, Fo, Fo}, none, none, nullptr, nullptr,
-                     saga_mat{b.z, V, Fo, b.ldz}, b.gws, b.gws_bytes, st);
+                     saga_mat{b.z, V, sp > 0 ? sp : Fo, b.ldz}, b.gws, b.gws_bytes, st);
         if (s) return s;
         op.msg = SAGA_MSG_COPY;
         op.reduce = SAGA_RED_SUM;
         op.dst_norm = 1;
         op.act = d.act;
-        in.src = saga_cmat{b.z, V, Fo, b.ldz};
+        if (sp == 0) {
+          in.src = saga_cmat{b.z, V, Fo, b.ldz};
+          in.bias = d.b;
+          return run_gather(p, op, in, out, b.part, b.part_bytes, st);
+        }
+        // the whole-line columns, then the rest, into the two column ranges of out
+        in.src = saga_cmat{b.z, V, sp, b.ldz};
         in.bias = d.b;
-        return run_gather(p, op, in, out, b.part, b.part_bytes, st);
+        s = run_gather(p, op, in, saga_mat{out.ptr, out.rows, sp, out.ld}, b.part, b.part_bytes, st);
+        if (s) return s;
+        in.src = saga_cmat{b.z3, V, Fo - sp, b.ldz3};
+        in.bias = d.b ? d.b + sp : nullptr;
+        return run_gather(p, op, in,
+                          saga_mat{static_cast<char*>(out.ptr) + sp * es, out.rows, Fo - sp, out.ld},
+                          b.part, b.part_bytes, st);
       }
       // aggregate first: agg = d_in^-1/2 sum_u d_out(u)^-1/2 X_u; out = act(agg W + b)
       op.msg = SAGA_MSG_SRC_NORM;

@@ -514,7 +514,10 @@ __global__ __launch_bounds__(R::THREADS) void k_gemm(GemmArgs g) {
         float v = acc[mt][nt][r] * rs;
         if (g.bias) v += g.bias[c];
         if (g.bias2) v += g.bias2[c];
-        out[row * g.ldo + c] = Mma<T>::from_f(apply_act(g.act, v));
+        if (g.split > 0 && c >= g.split)
+          static_cast<T*>(g.out2)[row * g.ldo2 + (c - g.split)] = Mma<T>::from_f(apply_act(g.act, v));
+        else
+          out[row * g.ldo + c] = Mma<T>::from_f(apply_act(g.act, v));
       }
     }
 }

@@ -104,6 +104,8 @@ struct GemmArgs {
   const float* bias2;
   const int32_t* row_scale_deg;
   void* out; int64_t ldo;
+  // split output: columns >= split go to out2 (ld ldo2) at column c - split
+  int64_t split; void* out2; int64_t ldo2;
   // scratch for the packed transposed weights (gemm_workspace_bytes)
   void* ws; size_t ws_bytes;
   // set by launch_gemm: packed weights in the workspace, ld kp / kp2

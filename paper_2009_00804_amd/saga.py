@@ -106,7 +106,7 @@ class saga_edge_inputs(C.Structure):
 
 class saga_gemm_op(C.Structure):
     _fields_ = [("dtype", C.c_int), ("mode", C.c_int), ("act", C.c_int),
-                ("row_scale_deg", C.c_void_p)]
+                ("row_scale_deg", C.c_void_p), ("split_col", C.c_int32), ("tail", saga_mat)]
 
 
 class saga_layer_desc(C.Structure):

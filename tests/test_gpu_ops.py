@@ -296,3 +296,40 @@ def test_gemm_gru(F):
     out = run_gemm(a, Wih, "f32", bias=bih, A2=h, W2=Whh, bias2=bhh, mode="gru", out_cols=F)
     ref = O.gru_cell(a, h, Wih, bih, Whh, bhh)
     assert rel_err(to_np(out), ref) <= FP32_TOL
+
+
+@pytest.mark.parametrize("dtype,N,split", [("f32", 41, 32), ("f32", 100, 64), ("bf16", 100, 64)])
+def test_gemm_split_output_equals_single_output(dtype, N, split):
+    """split_col writes columns [0, s) to out and [s, N) to the tail matrix:
+    the same values, bit for bit, as one output matrix (row scale, bias and
+    activation included)."""
+    S = lib()
+    rng = np.random.default_rng(N)
+    M, K = 777, 150
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = rng.standard_normal((K, N)).astype(np.float32) / np.sqrt(K)
+    b = rng.standard_normal(N).astype(np.float32)
+    deg = torch.from_numpy(rng.integers(0, 9, M).astype(np.int32)).to(device())
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    a = dev_padded(A, dtype=tdt)
+    w = torch.from_numpy(W).to(device()).to(tdt)
+    bias = torch.from_numpy(b).to(device())
+    op = S.saga_gemm_op(S.dtype_code(tdt), S.SAGA_GEMM_PLAIN, S.SAGA_ACT_ELU, deg.data_ptr())
+    ws = S.workspace(S.saga_apply_vertex_workspace_size(op, K, 0, N), device())
+    none = S.saga_cmat(None, 0, 0, 0)
+    print(f"gemm split {dtype} N={N} s={split}", flush=True)
+    one = torch.full((M, N), 7.0, dtype=tdt, device=device())
+    S.saga_apply_vertex(op, S.cmat(a), S.cmat(w), none, none, bias.data_ptr(), None, S.mat(one),
+                        C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
+    head = torch.full((M, split), 7.0, dtype=tdt, device=device())
+    tail = torch.full((M, N - split + 3), 7.0, dtype=tdt, device=device())[:, :N - split]
+    op.split_col = split
+    op.tail = S.mat(tail)
+    S.saga_apply_vertex(op, S.cmat(a), S.cmat(w), none, none, bias.data_ptr(), None, S.mat(head),
+                        C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
+    torch.cuda.synchronize()
+    assert torch.equal(head, one[:, :split]) and torch.equal(tail, one[:, split:])
+    op.split_col = N  # must be inside (0, N)
+    with pytest.raises(S.SagaError):
+        S.saga_apply_vertex(op, S.cmat(a), S.cmat(w), none, none, None, None, S.mat(head),
+                            C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
