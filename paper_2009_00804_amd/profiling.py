@@ -28,14 +28,21 @@ import re
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 
-# stage -> (kernel-name prefix per dtype, source file)
+# stage -> ({dtype: [(kernel-name prefix, dispatches per launch), ...]}, source file).
+# gather1 runs one dispatch per 128-byte column slice; the float32 gather2
+# runs two kernels (the 32 whole-line columns and the 9-column rest).
 STAGES = {
-    "gather1": ({"f32": "k_gather_simple<float, 8, 1, 8, 4, false, false, true",
-                 "bf16": "k_gather_simple<unsigned short, 8, 1, 8, 4, false, false, true"}, "gather.hip"),
-    "gather2": ({"f32": "k_gather_simple<float, 16, 1, 8, 4, false, false, false",
-                 "bf16": "k_gather_simple<unsigned short, 8, 1, 8, 4, false, false, false"}, "gather.hip"),
-    "gemm1": ({"f32": "k_gemm<float, 2, 8,", "bf16": "k_gemm<unsigned short, 1, 8,"}, "gemm.hip"),
-    "gemm2": ({"f32": "k_gemm<float, 2, 3,", "bf16": "k_gemm<unsigned short, 2, 3,"}, "gemm.hip"),
+    "gather1": ({"f32": [("k_gather_simple<float, 8, 1, 8, 4, false, 0, true", 4)],
+                 "bf16": [("k_gather_simple<unsigned short, 8, 1, 8, 4, false, 0, true", 2)]},
+                "gather.hip"),
+    "gather2": ({"f32": [("k_gather_simple<float, 8, 1, 8, 4, false, 0, false", 1),
+                         ("k_gather_simple<float, 4, 1, 4, 8, false, 0, false", 1)],
+                 "bf16": [("k_gather_simple<unsigned short, 8, 1, 8, 4, false, 0, false", 1)]},
+                "gather.hip"),
+    "gemm1": ({"f32": [("k_gemm<float, 2, 8,", 1)], "bf16": [("k_gemm<unsigned short, 1, 8,", 1)]},
+              "gemm.hip"),
+    "gemm2": ({"f32": [("k_gemm<float, 2, 3,", 1)], "bf16": [("k_gemm<unsigned short, 2, 3,", 1)]},
+              "gemm.hip"),
 }
 
 
@@ -92,14 +99,10 @@ def main():
     ap.add_argument("--write")
     ap.add_argument("--copy-mib", type=float, default=1024)
     ap.add_argument("--dtype", default="f32")
-    ap.add_argument("--slices", type=int, default=0,
-                    help="gather1 dispatches per call (default: 4 for f32, 2 for bf16)")
     ap.add_argument("--command", default="")
     ap.add_argument("--out", default="profiles")
     ap.add_argument("--tag", default="gcn_rmat21")
     a = ap.parse_args()
-    if a.slices <= 0:
-        a.slices = 4 if a.dtype == "f32" else 2
     os.makedirs(a.out, exist_ok=True)
 
     st = kernel_stats(a.trace)
@@ -134,20 +137,27 @@ def main():
     rec_path = os.path.join(a.out, "traffic.json")
     rec = json.load(open(rec_path)) if os.path.exists(rec_path) else {}
     for stage, (pats, src) in STAGES.items():
-        pat = pats[a.dtype]
-        keys = [k for k in set(fe) | set(wr) if k.startswith(pat)]
-        if len(keys) != 1:
+        parts = []
+        for pat, per in pats[a.dtype]:
+            keys = [k for k in set(fe) | set(wr) if k.startswith(pat)]
+            if len(keys) != 1:
+                break
+            parts.append((keys[0], per))
+        if len(parts) != len(pats[a.dtype]):
             continue
-        k = keys[0]
-        per = 1 if not stage.startswith("gather1") else a.slices
-        f_ = sum(fe[k]) / len(fe[k])
-        w_ = sum(wr[k]) / len(wr[k])
-        n_avg = st.get(k, (0, 0.0, 0.0))[1]
-        rec[f"{stage}:{a.dtype}"] = {
-            "kernel": k, "dispatches_per_launch": per, "source": src, "src_sha": src_sha(src),
-            "fetch_bytes_per_dispatch": f_ * cf * 1024, "write_bytes_per_dispatch": w_ * cw * 1024,
-            "bytes_per_launch": per * (f_ * cf + w_ * cw) * 1024,
-            "trace_avg_us_per_dispatch": n_avg, "calibration": {"fetch": cf, "write": cw}}
+        entry = {"kernels": [], "source": src, "src_sha": src_sha(src), "bytes_per_launch": 0.0,
+                 "trace_us_per_launch": 0.0, "calibration": {"fetch": cf, "write": cw}}
+        for k, per in parts:
+            f_ = sum(fe[k]) / len(fe[k])
+            w_ = sum(wr[k]) / len(wr[k])
+            n_avg = st.get(k, (0, 0.0, 0.0))[1]
+            entry["kernels"].append({
+                "kernel": k, "dispatches_per_launch": per,
+                "fetch_bytes_per_dispatch": f_ * cf * 1024,
+                "write_bytes_per_dispatch": w_ * cw * 1024, "trace_avg_us_per_dispatch": n_avg})
+            entry["bytes_per_launch"] += per * (f_ * cf + w_ * cw) * 1024
+            entry["trace_us_per_launch"] += per * n_avg
+        rec[f"{stage}:{a.dtype}"] = entry
     with open(rec_path, "w") as f:
         json.dump(rec, f, indent=1, sort_keys=True)
 
