@@ -584,11 +584,10 @@ def rel_layout(row_ptr, col_idx, etype, num_rel, tile):
         m = et == r
         edge_pair[m] = rel_ptr[r] + np.searchsorted(srcs[r], col[m])
     c = np.zeros(col.shape[0], dtype=np.int64)
-    for v in range(rp.shape[0] - 1):
+    for v in np.flatnonzero(rp[1:] > rp[:-1]):  # rows with in-edges
         t = et[rp[v]:rp[v + 1]]
-        if t.shape[0]:
-            cnt = np.bincount(t, minlength=num_rel)
-            c[rp[v]:rp[v + 1]] = cnt[t]
+        cnt = np.bincount(t, minlength=num_rel)
+        c[rp[v]:rp[v + 1]] = cnt[t]
     edge_norm = np.zeros(col.shape[0], dtype=np.float32)
     nz = c > 0
     edge_norm[nz] = (1.0 / c[nz]).astype(np.float32)

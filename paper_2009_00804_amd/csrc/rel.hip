@@ -17,10 +17,12 @@
 //
 // Pairs are found without sorting: one bit per (relation, source) in a
 // bitmap (relation-major, each relation's words padded to whole counting
-// blocks), set by the edges; the pair row of a set bit is the number of set
-// bits before it in its relation plus the relation's offset, i.e. a scan of
-// block popcounts, then of word popcounts, then a popcount under a mask.
-// The per-row type counts use an LDS histogram private to one wave.
+// blocks), set by the edges -- through byte flags packed into bits when the
+// flags fit in 256 MB, else by bitmap atomics.  The pair row of a set bit is
+// the number of set bits before it in its relation plus the relation's
+// offset: a scan of block popcounts, then of word popcounts, then a popcount
+// under a mask.  The per-row type counts use LDS histograms (one per
+// workgroup for the long rows, one per wave for the others).
 #include <algorithm>
 
 #include "saga_device.h"
@@ -221,11 +223,53 @@ __global__ __launch_bounds__(kThreads) void k_rel_edges(const int32_t* __restric
   }
 }
 
-// edge_norm[e] = 1 / c(v, r_e).  One wave per destination row, rows taken in
-// the plan's degree order (longest first); the wave counts the row's types
-// in its own LDS histogram of R bins (atomics), reads the counts back, then
-// clears the bins it touched.  A wave's LDS operations complete in issue
-// order, and each pass waits for the previous one.
+// The three passes over a row's types, STEP threads apart, four loads in
+// flight per thread: count (LDS atomics), read back into edge_norm, clear.
+template <int STEP>
+__device__ __forceinline__ void count_types(const int32_t* __restrict__ et, int beg, int end, int t,
+                                            int R, int32_t* hist) {
+  for (int e0 = beg + t; e0 < end; e0 += 4 * STEP) {
+    int r[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = e0 + j * STEP < end ? et[e0 + j * STEP] : -1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (r[j] >= 0 && r[j] < R) atomicAdd(&hist[r[j]], 1);
+  }
+}
+template <int STEP>
+__device__ __forceinline__ void write_norms(const int32_t* __restrict__ et, int beg, int end, int t,
+                                            int R, const int32_t* hist,
+                                            float* __restrict__ edge_norm) {
+  for (int e0 = beg + t; e0 < end; e0 += 4 * STEP) {
+    int r[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = e0 + j * STEP < end ? et[e0 + j * STEP] : -1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (e0 + j * STEP < end)
+        edge_norm[e0 + j * STEP] = (r[j] >= 0 && r[j] < R) ? 1.0f / (float)hist[r[j]] : 0.0f;
+  }
+}
+template <int STEP>
+__device__ __forceinline__ void clear_types(const int32_t* __restrict__ et, int beg, int end, int t,
+                                            int R, int32_t* hist) {
+  for (int e0 = beg + t; e0 < end; e0 += 4 * STEP) {
+    int r[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = e0 + j * STEP < end ? et[e0 + j * STEP] : -1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (r[j] >= 0 && r[j] < R) hist[r[j]] = 0;
+  }
+}
+
+// edge_norm[e] = 1 / c(v, r_e), rows taken in the plan's degree order.  The
+// long rows (the plan's split rows, perm positions 0 .. n_split - 1) are
+// counted by a whole workgroup sharing one LDS histogram of R bins; every
+// other row by one wave with its own.  Each pass waits for the previous one
+// (a workgroup barrier, or for a wave its own LDS operations, which complete
+// in issue order).
 __global__ __launch_bounds__(kThreads) void k_rel_norm(const int32_t* __restrict__ rp,
                                                        const int32_t* __restrict__ et,
                                                        const int32_t* __restrict__ perm, int32_t V,
@@ -234,28 +278,75 @@ __global__ __launch_bounds__(kThreads) void k_rel_norm(const int32_t* __restrict
   if (plan_counts[kErrFlags]) return;
   extern __shared__ int32_t hist_all[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int32_t* hist = hist_all + (int64_t)wave * R;
   for (int i = threadIdx.x; i < (kThreads / 64) * R; i += kThreads) hist_all[i] = 0;
   __syncthreads();
-  const int64_t nw = (int64_t)gridDim.x * (kThreads / 64);
-  for (int64_t i = (int64_t)blockIdx.x * (kThreads / 64) + wave; i < V; i += nw) {
+  const int n_long = plan_counts[kNSplit];
+  for (int64_t i = blockIdx.x; i < n_long; i += gridDim.x) {  // uniform per workgroup
     const int v = perm[i];
     const int beg = rp[v], end = rp[v + 1];
-    for (int e = beg + lane; e < end; e += 64) {
-      const int r = et[e];
-      if (r >= 0 && r < R) atomicAdd(&hist[r], 1);
-    }
+    count_types<kThreads>(et, beg, end, threadIdx.x, R, hist_all);
+    __syncthreads();
+    write_norms<kThreads>(et, beg, end, threadIdx.x, R, hist_all, edge_norm);
+    __syncthreads();
+    clear_types<kThreads>(et, beg, end, threadIdx.x, R, hist_all);
+    __syncthreads();
+  }
+  int32_t* hist = hist_all + (int64_t)wave * R;
+  const int64_t nw = (int64_t)gridDim.x * (kThreads / 64);
+  for (int64_t i = n_long + (int64_t)blockIdx.x * (kThreads / 64) + wave; i < V; i += nw) {
+    const int v = perm[i];
+    const int beg = rp[v], end = rp[v + 1];
+    count_types<64>(et, beg, end, lane, R, hist);
     lds_wait();
-    for (int e = beg + lane; e < end; e += 64) {
-      const int r = et[e];
-      edge_norm[e] = (r >= 0 && r < R) ? 1.0f / (float)hist[r] : 0.0f;
-    }
+    write_norms<64>(et, beg, end, lane, R, hist, edge_norm);
     lds_wait();
-    for (int e = beg + lane; e < end; e += 64) {
-      const int r = et[e];
-      if (r >= 0 && r < R) hist[r] = 0;
-    }
+    clear_types<64>(et, beg, end, lane, R, hist);
     lds_wait();
+  }
+}
+
+// Byte flags instead of bitmap atomics (when R x W x 32 bytes is modest):
+// flags[r * 32 W + u] = 1 for every (relation, source) an edge carries --
+// plain byte stores of the same value, no atomics -- then packed into the
+// bitmap, 32 flags per word.
+__global__ __launch_bounds__(kThreads) void k_rel_flag(const int32_t* __restrict__ col,
+                                                       const int32_t* __restrict__ et, int64_t E,
+                                                       int R, int64_t wp,
+                                                       uint8_t* __restrict__ flags,
+                                                       const int32_t* __restrict__ plan_counts,
+                                                       int32_t* rcounts) {
+  if (plan_counts[kErrFlags]) return;
+  bool bad = false;
+  for (int64_t e = blockIdx.x * (int64_t)kThreads + threadIdx.x; e < E;
+       e += (int64_t)gridDim.x * kThreads) {
+    const int r = et[e];
+    if (r < 0 || r >= R) {
+      bad = true;
+      continue;
+    }
+    uint8_t* f = flags + ((int64_t)r * wp) * 32 + col[e];
+    if (*f == 0) *f = 1;
+  }
+  if (bad) atomicOr(&rcounts[kRelErr], 1);
+}
+
+__global__ __launch_bounds__(kThreads) void k_rel_pack(const uint8_t* __restrict__ flags,
+                                                       int64_t nwords, uint32_t* __restrict__ bm,
+                                                       const int32_t* __restrict__ plan_counts) {
+  if (plan_counts[kErrFlags]) return;
+  for (int64_t w = blockIdx.x * (int64_t)kThreads + threadIdx.x; w < nwords;
+       w += (int64_t)gridDim.x * kThreads) {
+    const uint4* f = reinterpret_cast<const uint4*>(flags + w * 32);
+    const uint4 a = f[0], b = f[1];
+    const uint32_t x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    uint32_t word = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {  // four 0/1 bytes -> four bits
+      const uint32_t q = x[k];
+      const uint32_t nib = (q & 1u) | ((q >> 7) & 2u) | ((q >> 14) & 4u) | ((q >> 21) & 8u);
+      word |= nib << (4 * k);
+    }
+    bm[w] = word;
   }
 }
 
@@ -292,6 +383,9 @@ bool rel_layout(int32_t num_src, int64_t num_edges, int32_t num_rel, RelLayout* 
   L->off_counts = take(kRelCountSlots * 4);
   L->off_scratch = off;
   L->off_bitmap = take((size_t)R * L->wp * 4);
+  // byte flags (32 per bitmap word) when they stay under 256 MB
+  L->use_flags = (size_t)R * L->wp * 32 <= (size_t(1) << 28);
+  L->off_flags = take(L->use_flags ? (size_t)R * L->wp * 32 : 0);
   L->off_word_base = take((size_t)R * L->wp * 4);
   L->off_bcnt = take((size_t)L->nblocks * 4);
   L->off_block_base = take((size_t)L->nblocks * 4);
@@ -312,11 +406,23 @@ hipError_t launch_rel_build(const saga_plan& p, const saga_rel_plan& rel, const 
   const int64_t nbm = (int64_t)R * L.wp;
   hipLaunchKernelGGL(k_rel_fill, dim3(1), dim3(64), 0, st, reinterpret_cast<uint32_t*>(rel.counts),
                      (int64_t)kRelCountSlots, 0u);
-  hipLaunchKernelGGL(k_rel_fill, dim3(grid_for(nbm, kThreads * 4, 4096)), dim3(kThreads), 0, st,
-                     bm, nbm, 0u);
-  if (E > 0)
-    hipLaunchKernelGGL(k_rel_mark, dim3(grid_for(E, kThreads * 8, 8192)), dim3(kThreads), 0, st,
-                       p.col_idx, rel.etype, E, R, L.wp, bm, p.counts, rel.counts);
+  if (L.use_flags) {
+    uint32_t* flags = reinterpret_cast<uint32_t*>(scratch + (L.off_flags - L.off_scratch));
+    hipLaunchKernelGGL(k_rel_fill, dim3(grid_for(nbm * 8, kThreads * 4, 8192)), dim3(kThreads), 0,
+                       st, flags, nbm * 8, 0u);
+    if (E > 0)
+      hipLaunchKernelGGL(k_rel_flag, dim3(grid_for(E, kThreads * 8, 8192)), dim3(kThreads), 0, st,
+                         p.col_idx, rel.etype, E, R, L.wp, reinterpret_cast<uint8_t*>(flags),
+                         p.counts, rel.counts);
+    hipLaunchKernelGGL(k_rel_pack, dim3(grid_for(nbm, kThreads, 8192)), dim3(kThreads), 0, st,
+                       reinterpret_cast<const uint8_t*>(flags), nbm, bm, p.counts);
+  } else {
+    hipLaunchKernelGGL(k_rel_fill, dim3(grid_for(nbm, kThreads * 4, 4096)), dim3(kThreads), 0, st,
+                       bm, nbm, 0u);
+    if (E > 0)
+      hipLaunchKernelGGL(k_rel_mark, dim3(grid_for(E, kThreads * 8, 8192)), dim3(kThreads), 0, st,
+                         p.col_idx, rel.etype, E, R, L.wp, bm, p.counts, rel.counts);
+  }
   hipLaunchKernelGGL(k_rel_bcount, dim3(grid_for(L.nblocks, 1, 8192)), dim3(kThreads), 0, st, bm,
                      L.nblocks, bcnt, p.counts);
   hipLaunchKernelGGL(k_rel_scan, dim3(1), dim3(1024), 0, st, bcnt, R, L.bpr, (int)kRelTile,
@@ -329,7 +435,7 @@ hipError_t launch_rel_build(const saga_plan& p, const saga_rel_plan& rel, const 
     hipLaunchKernelGGL(k_rel_edges, dim3(grid_for(E, kThreads * 8, 8192)), dim3(kThreads), 0, st,
                        p.col_idx, rel.etype, E, R, L.wp, bm, word_base, rel.edge_pair, p.counts);
     const size_t lds = (size_t)(kThreads / 64) * R * 4;
-    hipLaunchKernelGGL(k_rel_norm, dim3(grid_for(p.num_dst, kThreads / 64, 4096)), dim3(kThreads),
+    hipLaunchKernelGGL(k_rel_norm, dim3(grid_for(p.num_dst, kThreads / 64, 16384)), dim3(kThreads),
                        lds, st, p.row_ptr, rel.etype, p.perm, p.num_dst, R, rel.edge_norm,
                        p.counts);
   }

@@ -158,6 +158,8 @@ struct RelLayout {
   int64_t max_pairs;
   size_t off_rel_ptr, off_rel_count, off_pair_src, off_edge_pair, off_edge_norm, off_counts,
       off_scratch, off_bitmap, off_word_base, off_bcnt, off_block_base, scratch_bytes, total;
+  bool use_flags;    // byte flags packed into the bitmap (else bitmap atomics)
+  size_t off_flags;
 };
 bool rel_layout(int32_t num_src, int64_t num_edges, int32_t num_rel, RelLayout* L);
 hipError_t launch_rel_build(const saga_plan& p, const saga_rel_plan& rel, const RelLayout& L,

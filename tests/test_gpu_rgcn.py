@@ -296,3 +296,28 @@ def test_rgcn_full_workload_sampled():
     for k in ("rel_ptr", "pair_src", "edge_pair"):
         assert np.array_equal(arr[k].astype(np.int64), L[k]), k
     assert np.array_equal(arr["edge_norm"], L["edge_norm"])
+
+
+def test_rel_layout_bitmap_atomics_path():
+    """Many sources x many relations: the pair bitmap is set with atomics
+    instead of byte flags (R x 32 W bytes above 256 MB); same layout."""
+    n, R, E = 1 << 21, 200, 60000
+    rng = np.random.default_rng(17)
+    src = rng.integers(0, n, E)
+    dst = np.sort(rng.integers(0, n, E))
+    # hub sources and hub destinations with repeated types as well
+    src[:5000] = 7
+    dst[-4000:] = n - 3
+    order = np.lexsort((src, dst))
+    src, dst = src[order], dst[order]
+    rp = np.zeros(n + 1, np.int64)
+    np.cumsum(np.bincount(dst, minlength=n), out=rp[1:])
+    et = rng.integers(0, R, E).astype(np.int32)
+    et[:5000] = rng.integers(0, 3, 5000)
+    print(f"rel layout bitmap path V={n} E={E} R={R}", flush=True)
+    graph, rg = _rel(n, R, rp.astype(np.int32), src.astype(np.int32), et)
+    want = O.rel_layout(rp, src, et, R, TILE)
+    got = {k: v.cpu().numpy() for k, v in rg.arrays().items()}
+    for k in ("rel_ptr", "rel_count", "pair_src", "edge_pair"):
+        assert np.array_equal(got[k].astype(np.int64), want[k]), k
+    assert np.array_equal(got["edge_norm"], want["edge_norm"])
