@@ -214,15 +214,26 @@ __global__ __launch_bounds__(LstmCfg<H>::THREADS) void k_lstm_gather(LstmArgs a)
                      : "=v"(pq)
                      : "v"(ring_base + (uint32_t)(((s % (kPF + 1)) * G + q * H + i) * 4))
                      : "memory");
+        // this thread's quarter of h, all of it read before the first
+        // multiply-add (one LDS wait per step)
         const float* hb = hbuf[s & 1];
-        float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f, z3 = 0.0f;
+        float hk[KPT];
 #pragma unroll
         for (int k = 0; k < KPT; k += 4) {
           const float4 hv = *reinterpret_cast<const float4*>(hb + k0 + k);
-          z0 += w[0][k] * hv.x + w[0][k + 1] * hv.y + w[0][k + 2] * hv.z + w[0][k + 3] * hv.w;
-          z1 += w[1][k] * hv.x + w[1][k + 1] * hv.y + w[1][k + 2] * hv.z + w[1][k + 3] * hv.w;
-          z2 += w[2][k] * hv.x + w[2][k + 1] * hv.y + w[2][k + 2] * hv.z + w[2][k + 3] * hv.w;
-          z3 += w[3][k] * hv.x + w[3][k + 1] * hv.y + w[3][k + 2] * hv.z + w[3][k + 3] * hv.w;
+          hk[k] = hv.x;
+          hk[k + 1] = hv.y;
+          hk[k + 2] = hv.z;
+          hk[k + 3] = hv.w;
+        }
+        __builtin_amdgcn_sched_barrier(0);  // keep every read ahead of the multiply-adds
+        float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f, z3 = 0.0f;
+#pragma unroll
+        for (int k = 0; k < KPT; ++k) {  // four independent chains
+          z0 = fmaf(w[0][k], hk[k], z0);
+          z1 = fmaf(w[1][k], hk[k], z1);
+          z2 = fmaf(w[2][k], hk[k], z2);
+          z3 = fmaf(w[3][k], hk[k], z3);
         }
         asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(pq) : : "memory");
         // reduce-scatter over the quad: lane q ends with the full sum of gate
