@@ -256,6 +256,7 @@ saga_status run_gather(const saga_plan& p, const saga_edge_op& op, const saga_ed
   a.out_cols = (int)out.cols;
   a.src = in.src.ptr;
   a.ld_src = in.src.ld;
+  a.src_rows = in.src.rows;
   a.el = static_cast<const float*>(in.el.ptr);
   a.ld_el = in.el.ld;
   a.er = static_cast<const float*>(in.er.ptr);

@@ -573,24 +573,37 @@ inline int next_pow2(int x) {
   return p;
 }
 
-// slices processed concurrently by one launch; the rest run as further
-// launches.  One slice per launch keeps the working set of source rows
-// (rows x 128 B) close to the 256 MB Infinity Cache and measured fastest;
-// SAGA_GATHER_CONCURRENT_SLICES overrides it (0 = all in one launch)
-int concurrent_slices() {
-  static int v = [] {
+// Slices processed concurrently by one launch; the rest run as further
+// launches.  The source rows one launch touches (src_rows x the slices'
+// bytes) are kept within 192 MB, under the 256 MB Infinity Cache: on the
+// 2^21-row source one 128-byte slice per launch (268 MB) measured fastest,
+// while a source of 131,072 rows has all eight 128-byte slices of its
+// 1 KB rows in one launch (134 MB), which also spares the launches their
+// ramp and tail.  SAGA_GATHER_CONCURRENT_SLICES overrides the choice
+// (0 = all in one launch).
+constexpr int64_t kSliceBudget = int64_t(192) << 20;
+
+int concurrent_slices(const GatherArgs& a, int nslices, int slice_bytes_) {
+  static int env = [] {
     const char* e = getenv("SAGA_GATHER_CONCURRENT_SLICES");
-    int x = e ? atoi(e) : 1;
-    return x >= 0 ? x : 1;
+    return e ? atoi(e) : -1;
   }();
-  return v;
+  if (env >= 0) return env;
+  const int64_t per = std::max<int64_t>(1, a.src_rows) * slice_bytes_;
+  int c = 1;
+  for (int k = nslices; k >= 1; --k)
+    if (nslices % k == 0 && k * per <= kSliceBudget) {
+      c = k;
+      break;
+    }
+  return c;
 }
 
 template <typename T, int LPR, int VPL>
 hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, hipStream_t st) {
   constexpr int U = LPR >= 8 ? (VPL == 1 ? 8 : 4) : LPR;
   constexpr int CPL = LPR >= 32 ? 1 : (LPR >= 8 ? 4 : 8);
-  int conc = concurrent_slices();
+  int conc = concurrent_slices(a, nslices, LPR * VPL * 16);
   if (conc <= 0 || conc > nslices || nslices % conc != 0) conc = nslices;
   const dim3 grid(blocks * conc);
   const bool srcnorm = a.msg == SAGA_MSG_SRC_NORM;

@@ -64,6 +64,7 @@ struct GatherArgs {
   int out_cols;    // F or F/heads
   // inputs
   const void* src; int64_t ld_src;
+  int64_t src_rows;  // rows of src (sizes the slices run per launch)
   const float* el; int64_t ld_el;
   const float* er; int64_t ld_er;
   const float* gsrc; int64_t ld_gsrc;
