@@ -333,3 +333,30 @@ def test_gemm_split_output_equals_single_output(dtype, N, split):
     with pytest.raises(S.SagaError):
         S.saga_apply_vertex(op, S.cmat(a), S.cmat(w), none, none, None, None, S.mat(head),
                             C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
+
+
+@pytest.mark.parametrize("dtype,F", [("f32", 512), ("bf16", 1024), ("f32", 508), ("bf16", 1000)])
+def test_gather_maximum_widths(dtype, F):
+    """The widest rows the simple Gather takes (512 float32 / 1024 bfloat16
+    columns, whole and ragged), sum with both norms and max, on the
+    power-law graph with split rows."""
+    S = lib()
+    rp, col, n, g = _get_graph("rmat")
+    rng = np.random.default_rng(F)
+    X = rng.standard_normal((n, F)).astype(np.float32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    if dtype == "bf16":
+        X = _bf16_round(X)
+    Xt = dev_padded(X, tdt)
+    tol = FP32_TOL if dtype == "f32" else BF16_TOL
+    print(f"gather max width {dtype} F={F}", flush=True)
+    out = run_gather(g, Xt, dict(reduce=S.SAGA_RED_SUM, msg=S.SAGA_MSG_SRC_NORM, dst_norm=1,
+                                 act="none"), F, tdt)
+    ref = _ref_simple(rp, col, X, "sum", "src_norm", 1, None, "none", n)
+    assert rel_err(to_np(out), ref) <= tol
+    out = run_gather(g, Xt, dict(reduce=S.SAGA_RED_MAX), F, tdt)
+    assert np.array_equal(to_np(out), O.gather(rp, col, X, "max"))
+    limit = 512 if dtype == "f32" else 1024  # one column past the widest row is refused
+    wider = dev_padded(np.zeros((n, limit + 1), np.float32), tdt)
+    with pytest.raises(S.SagaError):
+        run_gather(g, wider, dict(reduce=S.SAGA_RED_SUM), limit + 1, tdt)
