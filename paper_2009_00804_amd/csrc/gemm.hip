@@ -480,11 +480,174 @@ __global__ __launch_bounds__(kThreads) void k_pack_wt(const T* __restrict__ W, i
   }
 }
 
+// ---------------------------------------------------------------------------
+// epilogue.  Lane l of a wave holds rows 4 (l / 16) + r (r < 4), column
+// l % 16 of each 16 x 16 accumulator tile (mt, nt).
+// ---------------------------------------------------------------------------
+
+template <int ACT, int MT, int NT>
+__device__ __forceinline__ void act_tile(f32x4 (&acc)[MT][NT]) {
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[mt][nt][r] = apply_act(ACT, acc[mt][nt][r]);
+}
+
+// Row scale, biases and activation applied to the accumulators in place,
+// in that order (v = acc * rs + b1 + b2, then act).  Each optional step is
+// one uniform branch around the whole tile, and every load happens before
+// the first store (the compiler cannot tell the output from the loaded
+// arrays, so a load after a store would wait for it).
+template <int MT, int NT>
+__device__ __forceinline__ void finish_tile(const GemmArgs& g, int64_t row0, int64_t n0,
+                                            f32x4 (&acc)[MT][NT]) {
+  const int lane = threadIdx.x & 63;
+  if (g.row_scale_deg) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = row0 + mt * 16 + 4 * (lane >> 4) + r;
+        const float rs = row < g.M ? rsqrt_deg(g.row_scale_deg[row]) : 0.0f;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt][r] *= rs;
+      }
+  }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const float* bias = k == 0 ? g.bias : g.bias2;
+    if (!bias) continue;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int64_t c = n0 + nt * 16 + (lane & 15);
+      const float b = c < g.N ? bias[c] : 0.0f;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[mt][nt][r] += b;
+    }
+  }
+  switch (g.act) {
+    case SAGA_ACT_RELU: act_tile<SAGA_ACT_RELU>(acc); break;
+    case SAGA_ACT_ELU: act_tile<SAGA_ACT_ELU>(acc); break;
+    case SAGA_ACT_SIGMOID: act_tile<SAGA_ACT_SIGMOID>(acc); break;
+    case SAGA_ACT_TANH: act_tile<SAGA_ACT_TANH>(acc); break;
+    default: break;
+  }
+}
+
+// output element (row, c) of the finished tile: columns >= split go to out2
+template <typename T>
+__device__ __forceinline__ void store_elem(const GemmArgs& g, int64_t row, int64_t c, float v) {
+  if (g.split > 0 && c >= g.split)
+    static_cast<T*>(g.out2)[row * g.ldo2 + (c - g.split)] = Mma<T>::from_f(v);
+  else
+    static_cast<T*>(g.out)[row * g.ldo + c] = Mma<T>::from_f(v);
+}
+
+// element by element, straight from the accumulators
+template <typename T, int MT, int NT>
+__device__ __forceinline__ void store_direct(const GemmArgs& g, int64_t row0, int64_t n0,
+                                             const f32x4 (&acc)[MT][NT]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = row0 + mt * 16 + 4 * (lane >> 4) + r;
+      if (row >= g.M) continue;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int64_t c = n0 + nt * 16 + (lane & 15);
+        if (c < g.N) store_elem<T>(g, row, c, acc[mt][nt][r]);
+      }
+    }
+}
+
+// Through LDS: the wave writes its 16 MT rows x 128 columns (already in
+// the output type) to its own region, then each lane reads back whole
+// 16-byte pieces of rows, so one store instruction covers 1 KB of full
+// output rows instead of 64-byte pieces of four rows.  A piece is stored
+// whole when it lies inside the output, on one side of the split column,
+// and both outputs allow 16-byte accesses; otherwise element by element.
+// Piece p of local row lr sits at piece p ^ (((lr >> 2) & 3) << SH) of the
+// row in LDS: the four rows one write instruction touches then fall on
+// different banks.  Only this wave's region is touched, so no workgroup
+// barrier is needed once every wave is past the last read of the ring.
+template <typename T, int MT>
+__device__ __forceinline__ void store_staged(const GemmArgs& g, int64_t row0, int64_t n0,
+                                             const f32x4 (&acc)[MT][8], T* region) {
+  constexpr int NT = 8, BN = 16 * NT, EPL = Mma<T>::EPL, PR = BN / EPL, ROWS = 16 * MT;
+  constexpr int SH = EPL == 4 ? 2 : 1;  // pieces per 16 columns: 4 or 2
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int lr = mt * 16 + 4 * (lane >> 4) + r;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int col = nt * 16 + (lane & 15);
+        const int pp = (col / EPL) ^ (((lr >> 2) & 3) << SH);
+        region[lr * BN + pp * EPL + col % EPL] = Mma<T>::from_f(acc[mt][nt][r]);
+      }
+    }
+  const size_t es = sizeof(T);
+  const bool vec = (reinterpret_cast<uintptr_t>(g.out) & 15) == 0 && (g.ldo * es) % 16 == 0 &&
+                   (g.split <= 0 || ((reinterpret_cast<uintptr_t>(g.out2) & 15) == 0 &&
+                                     (g.ldo2 * es) % 16 == 0));
+  const uint4* src = reinterpret_cast<const uint4*>(region);
+#pragma unroll
+  for (int i = 0; i < ROWS * PR / 64; ++i) {
+    const int k = i * 64 + lane, lr = k / PR, p = k % PR;
+    const uint4 v = src[lr * PR + (p ^ (((lr >> 2) & 3) << SH))];
+    const int64_t row = row0 + lr, c = n0 + (int64_t)p * EPL;
+    if (row >= g.M) continue;
+    const bool whole = c + EPL <= g.N && (g.split <= 0 || c + EPL <= g.split || c >= g.split);
+    if (vec && whole) {
+      T* dst = g.split > 0 && c >= g.split
+                   ? static_cast<T*>(g.out2) + row * g.ldo2 + (c - g.split)
+                   : static_cast<T*>(g.out) + row * g.ldo + c;
+      *reinterpret_cast<uint4*>(dst) = v;
+    } else {
+      T e[EPL];
+      __builtin_memcpy(e, &v, 16);
+#pragma unroll
+      for (int j = 0; j < EPL; ++j)
+        if (c + j < g.N) {
+          if (g.split > 0 && c + j >= g.split)
+            static_cast<T*>(g.out2)[row * g.ldo2 + (c + j - g.split)] = e[j];
+          else
+            static_cast<T*>(g.out)[row * g.ldo + c + j] = e[j];
+        }
+    }
+  }
+}
+
+// staged stores need 128-column tiles and room in the ring for every
+// wave's rows
+template <typename T, int MT, int NT, typename R>
+constexpr bool kStaged =
+    NT == 8 && (size_t)(R::THREADS / 64) * 16 * MT * 16 * NT * sizeof(T) <= R::LDS_BYTES;
+
+template <typename T, int MT, int NT, typename R>
+__device__ __forceinline__ void store_tile(const GemmArgs& g, int64_t row0, int64_t n0,
+                                           const f32x4 (&acc)[MT][NT], uint4* ring) {
+  if constexpr (kStaged<T, MT, NT, R>) {
+    const int wave = threadIdx.x >> 6;
+    store_staged<T, MT>(g, row0, n0, acc, reinterpret_cast<T*>(ring) + (size_t)wave * 16 * MT * 16 * NT);
+  } else {
+    store_direct<T, MT, NT>(g, row0, n0, acc);
+  }
+}
+
 // PLAIN / CONCAT
 template <typename T, int MT, int NT, typename R>
 __global__ __launch_bounds__(R::THREADS) void k_gemm(GemmArgs g) {
   __shared__ uint4 ring[R::RING_SLOTS];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wave = threadIdx.x >> 6;
   const int64_t tile0 = (int64_t)blockIdx.x * R::BM;
   const int64_t n0 = (int64_t)blockIdx.y * R::BN;
   f32x4 acc[MT][NT];
@@ -497,29 +660,9 @@ __global__ __launch_bounds__(R::THREADS) void k_gemm(GemmArgs g) {
   if (g.mode == SAGA_GEMM_CONCAT)
     R::phase(static_cast<const T*>(g.a2), g.lda2, g.M, g.K2, static_cast<const T*>(g.wt2), g.kp2,
              tile0, n0, ring, acc);
-  // epilogue: lane holds rows 4*(lane/16) + r, column lane % 16 of each tile
   const int64_t row0 = tile0 + wave * MT * 16;
-  T* out = static_cast<T*>(g.out);
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t row = row0 + mt * 16 + 4 * (lane >> 4) + r;
-      if (row >= g.M) continue;
-      const float rs = g.row_scale_deg ? rsqrt_deg(g.row_scale_deg[row]) : 1.0f;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int64_t c = n0 + nt * 16 + (lane & 15);
-        if (c >= g.N) continue;
-        float v = acc[mt][nt][r] * rs;
-        if (g.bias) v += g.bias[c];
-        if (g.bias2) v += g.bias2[c];
-        if (g.split > 0 && c >= g.split)
-          static_cast<T*>(g.out2)[row * g.ldo2 + (c - g.split)] = Mma<T>::from_f(apply_act(g.act, v));
-        else
-          out[row * g.ldo + c] = Mma<T>::from_f(apply_act(g.act, v));
-      }
-    }
+  finish_tile(g, row0, n0, acc);
+  store_tile<T, MT, NT, R>(g, row0, n0, acc, ring);
 }
 
 // GRU: acc1 = a w (input gates), acc2 = a2 w2 (hidden gates), column blocks
@@ -544,6 +687,23 @@ __global__ __launch_bounds__(kThreads) void k_gemm_gru(GemmArgs g) {
   const int F = NT3 * 16;
   const int64_t row0 = tile0 + wave * 16;
   T* out = static_cast<T*>(g.out);
+  // biases and previous states are all loaded before the first store (a
+  // load after a store the compiler cannot tell apart from it would wait)
+  float bi[3][NT3], bh[3][NT3], hp[4][NT3];
+#pragma unroll
+  for (int t = 0; t < NT3; ++t) {
+    const int c = t * 16 + (lane & 15);
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      bi[q][t] = g.bias ? g.bias[q * F + c] : 0.f;
+      bh[q][t] = g.bias2 ? g.bias2[q * F + c] : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = row0 + 4 * (lane >> 4) + r;
+      hp[r][t] = row < g.M ? Mma<T>::to_f(h[row * g.lda2 + c]) : 0.f;
+    }
+  }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int64_t row = row0 + 4 * (lane >> 4) + r;
@@ -551,15 +711,11 @@ __global__ __launch_bounds__(kThreads) void k_gemm_gru(GemmArgs g) {
 #pragma unroll
     for (int t = 0; t < NT3; ++t) {
       const int c = t * 16 + (lane & 15);
-      const float bi_r = g.bias ? g.bias[c] : 0.f, bi_z = g.bias ? g.bias[F + c] : 0.f,
-                  bi_n = g.bias ? g.bias[2 * F + c] : 0.f;
-      const float bh_r = g.bias2 ? g.bias2[c] : 0.f, bh_z = g.bias2 ? g.bias2[F + c] : 0.f,
-                  bh_n = g.bias2 ? g.bias2[2 * F + c] : 0.f;
-      const float rr = sigmoidf_(acc1[0][t][r] + bi_r + acc2[0][t][r] + bh_r);
-      const float zz = sigmoidf_(acc1[0][t + NT3][r] + bi_z + acc2[0][t + NT3][r] + bh_z);
-      const float nn = tanhf(acc1[0][t + 2 * NT3][r] + bi_n + rr * (acc2[0][t + 2 * NT3][r] + bh_n));
-      const float hp = Mma<T>::to_f(h[row * g.lda2 + c]);
-      out[row * g.ldo + c] = Mma<T>::from_f((1.0f - zz) * nn + zz * hp);
+      const float rr = sigmoidf_(acc1[0][t][r] + bi[0][t] + acc2[0][t][r] + bh[0][t]);
+      const float zz = sigmoidf_(acc1[0][t + NT3][r] + bi[1][t] + acc2[0][t + NT3][r] + bh[1][t]);
+      const float nn =
+          tanhf(acc1[0][t + 2 * NT3][r] + bi[2][t] + rr * (acc2[0][t + 2 * NT3][r] + bh[2][t]));
+      out[row * g.ldo + c] = Mma<T>::from_f((1.0f - zz) * nn + zz * hp[r][t]);
     }
   }
 }
@@ -595,20 +751,16 @@ __global__ __launch_bounds__(R::THREADS) void k_gemm_grouped(GemmArgs g) {
            static_cast<const T*>(g.wt) + (int64_t)lo * g.wt_group_stride, g.kp, tile0, n0, ring,
            acc, g.arow);
   const int64_t row0 = tile0 + wave * MT * 16;
-  T* out = static_cast<T*>(g.out);
+  // rows of range padding (map entry < 0) are written as zeros
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t row = row0 + mt * 16 + 4 * (lane >> 4) + r;
-      const bool keep = g.arow[row] >= 0;
+    for (int r = 0; r < 4; ++r)
+      if (g.arow[row0 + mt * 16 + 4 * (lane >> 4) + r] < 0) {
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int64_t c = n0 + nt * 16 + (lane & 15);
-        if (c >= g.N) continue;
-        out[row * g.ldo + c] = Mma<T>::from_f(keep ? acc[mt][nt][r] : 0.0f);
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt][r] = 0.0f;
       }
-    }
+  store_tile<T, MT, NT, R>(g, row0, n0, acc, ring);
 }
 
 // Wt[grp][n][k] = W[grp K + k][n] for n < N, k < K, else 0; each group's
