@@ -254,6 +254,25 @@ def test_gemm_plain(M, K, N, dtype):
     assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gemm_plain_many_tiles(dtype):
+    """More 128-row tiles than the device runs workgroups at once: the
+    persistent kernel takes several tiles per workgroup (ragged last tile,
+    K tail), with the row scale, bias and activation epilogue."""
+    rng = np.random.default_rng(9)
+    M, K, N = 200_003, 150, 128
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((K, N)) / np.sqrt(K)).astype(np.float32)
+    if dtype == "bf16":
+        A, W = _bf16_round(A), _bf16_round(W)
+    bias = rng.standard_normal(N)
+    deg = rng.integers(0, 9, M)
+    print(f"gemm plain many tiles M={M} K={K} N={N} {dtype}", flush=True)
+    out = run_gemm(A, W, dtype, bias=bias, act="relu", deg=deg)
+    ref = O.dense(A, W, bias=bias, act="relu", row_scale=O.degree_scale(deg))
+    assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
+
+
 def test_gemm_small_integers_exact():
     rng = np.random.default_rng(1)
     A = rng.integers(-8, 9, (333, 64)).astype(np.float32)
