@@ -256,9 +256,9 @@ def test_gemm_plain(M, K, N, dtype):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_gemm_plain_many_tiles(dtype):
-    """More 128-row tiles than the device runs workgroups at once: the
-    persistent kernel takes several tiles per workgroup (ragged last tile,
-    K tail), with the row scale, bias and activation epilogue."""
+    """More 128-row tiles than the device holds workgroups at once (later
+    waves of workgroups reuse the LDS of earlier ones), a ragged last tile
+    and a K tail, with the row scale, bias and activation epilogue."""
     rng = np.random.default_rng(9)
     M, K, N = 200_003, 150, 128
     A = rng.standard_normal((M, K)).astype(np.float32)
