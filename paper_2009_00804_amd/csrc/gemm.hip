@@ -566,21 +566,23 @@ __device__ __forceinline__ void store_direct(const GemmArgs& g, int64_t row0, in
     }
 }
 
-// Through LDS: the wave writes its 16 MT rows x 128 columns (already in
+// Through LDS: the wave writes its 16 MT rows x 16 NT columns (already in
 // the output type) to its own region, then each lane reads back whole
-// 16-byte pieces of rows, so one store instruction covers 1 KB of full
-// output rows instead of 64-byte pieces of four rows.  A piece is stored
+// 16-byte pieces of rows, so one store instruction covers 1 KB of whole
+// row pieces instead of 64-byte pieces of four rows.  A piece is stored
 // whole when it lies inside the output, on one side of the split column,
 // and both outputs allow 16-byte accesses; otherwise element by element.
-// Piece p of local row lr sits at piece p ^ (((lr >> 2) & 3) << SH) of the
-// row in LDS: the four rows one write instruction touches then fall on
-// different banks.  Only this wave's region is touched, so no workgroup
+// For 128-column tiles, piece p of local row lr sits at piece
+// p ^ (((lr >> 2) & 3) << SH) of the row in LDS: the four rows one write
+// instruction touches then fall on different banks (narrower tiles keep
+// the plain order).  Only this wave's region is touched, so no workgroup
 // barrier is needed once every wave is past the last read of the ring.
-template <typename T, int MT>
+template <typename T, int MT, int NT>
 __device__ __forceinline__ void store_staged(const GemmArgs& g, int64_t row0, int64_t n0,
-                                             const f32x4 (&acc)[MT][8], T* region) {
-  constexpr int NT = 8, BN = 16 * NT, EPL = Mma<T>::EPL, PR = BN / EPL, ROWS = 16 * MT;
-  constexpr int SH = EPL == 4 ? 2 : 1;  // pieces per 16 columns: 4 or 2
+                                             const f32x4 (&acc)[MT][NT], T* region) {
+  constexpr int BN = 16 * NT, EPL = Mma<T>::EPL, PR = BN / EPL, ROWS = 16 * MT;
+  constexpr int SH = NT == 8 ? (EPL == 4 ? 2 : 1) : 0;  // log2 pieces per 16 columns
+  constexpr int SW = NT == 8 ? 3 : 0;                    // row bits that pick the swizzle
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
@@ -590,7 +592,7 @@ __device__ __forceinline__ void store_staged(const GemmArgs& g, int64_t row0, in
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const int col = nt * 16 + (lane & 15);
-        const int pp = (col / EPL) ^ (((lr >> 2) & 3) << SH);
+        const int pp = (col / EPL) ^ (((lr >> 2) & SW) << SH);
         region[lr * BN + pp * EPL + col % EPL] = Mma<T>::from_f(acc[mt][nt][r]);
       }
     }
@@ -600,9 +602,10 @@ __device__ __forceinline__ void store_staged(const GemmArgs& g, int64_t row0, in
                                      (g.ldo2 * es) % 16 == 0));
   const uint4* src = reinterpret_cast<const uint4*>(region);
 #pragma unroll
-  for (int i = 0; i < ROWS * PR / 64; ++i) {
+  for (int i = 0; i < (ROWS * PR + 63) / 64; ++i) {
     const int k = i * 64 + lane, lr = k / PR, p = k % PR;
-    const uint4 v = src[lr * PR + (p ^ (((lr >> 2) & 3) << SH))];
+    if (k >= ROWS * PR) break;
+    const uint4 v = src[lr * PR + (p ^ (((lr >> 2) & SW) << SH))];
     const int64_t row = row0 + lr, c = n0 + (int64_t)p * EPL;
     if (row >= g.M) continue;
     const bool whole = c + EPL <= g.N && (g.split <= 0 || c + EPL <= g.split || c >= g.split);
@@ -626,18 +629,18 @@ __device__ __forceinline__ void store_staged(const GemmArgs& g, int64_t row0, in
   }
 }
 
-// staged stores need 128-column tiles and room in the ring for every
-// wave's rows
+// staged stores need room in the ring for every wave's rows
 template <typename T, int MT, int NT, typename R>
 constexpr bool kStaged =
-    NT == 8 && (size_t)(R::THREADS / 64) * 16 * MT * 16 * NT * sizeof(T) <= R::LDS_BYTES;
+    (size_t)(R::THREADS / 64) * 16 * MT * 16 * NT * sizeof(T) <= R::LDS_BYTES;
 
 template <typename T, int MT, int NT, typename R>
 __device__ __forceinline__ void store_tile(const GemmArgs& g, int64_t row0, int64_t n0,
                                            const f32x4 (&acc)[MT][NT], uint4* ring) {
   if constexpr (kStaged<T, MT, NT, R>) {
     const int wave = threadIdx.x >> 6;
-    store_staged<T, MT>(g, row0, n0, acc, reinterpret_cast<T*>(ring) + (size_t)wave * 16 * MT * 16 * NT);
+    store_staged<T, MT, NT>(g, row0, n0, acc,
+                            reinterpret_cast<T*>(ring) + (size_t)wave * 16 * MT * 16 * NT);
   } else {
     store_direct<T, MT, NT>(g, row0, n0, acc);
   }
