@@ -596,6 +596,10 @@ __device__ __forceinline__ void store_staged(const GemmArgs& g, int64_t row0, in
         region[lr * BN + pp * EPL + col % EPL] = Mma<T>::from_f(acc[mt][nt][r]);
       }
     }
+  // the region is written as T and read back as 16-byte vectors: keep the
+  // compiler from moving a read above a write (the wave's LDS accesses then
+  // complete in program order)
+  asm volatile("" ::: "memory");
   const size_t es = sizeof(T);
   const bool vec = (reinterpret_cast<uintptr_t>(g.out) & 15) == 0 && (g.ldo * es) % 16 == 0 &&
                    (g.split <= 0 || ((reinterpret_cast<uintptr_t>(g.out2) & 15) == 0 &&
