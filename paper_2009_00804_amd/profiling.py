@@ -65,12 +65,13 @@ def src_sha(name):
 
 
 def kernel_stats(trace_dir):
-    """{short kernel name: (calls, avg_us, total_us)} from the kernel trace."""
+    """{short kernel name: (calls, avg_us, total_us, min_us, max_us)} from
+    the kernel trace."""
     rows = list(csv.DictReader(open(_csv(trace_dir, "kernel_trace.csv"))))
     acc = collections.defaultdict(list)
     for r in rows:
         acc[_short(r["Kernel_Name"])].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
-    return {k: (len(v), sum(v) / len(v), sum(v)) for k, v in acc.items()}
+    return {k: (len(v), sum(v) / len(v), sum(v), min(v), max(v)) for k, v in acc.items()}
 
 
 def counter_avgs(counter_dir, counter):
@@ -109,9 +110,10 @@ def main():
     tot = sum(v[2] for v in st.values())
     lines = [f"# Kernel trace summary: {a.tag} ({a.dtype})", "",
              f"command: {a.command}", "",
-             f"{'kernel':70s} {'calls':>6s} {'avg us':>10s} {'% time':>7s}"]
-    for k, (n, avg, total) in sorted(st.items(), key=lambda kv: -kv[1][2]):
-        lines.append(f"{k[:70]:70s} {n:6d} {avg:10.1f} {100 * total / tot:7.2f}")
+             f"{'kernel':70s} {'calls':>6s} {'avg us':>10s} {'min us':>10s} {'max us':>10s} "
+             f"{'% time':>7s}"]
+    for k, (n, avg, total, lo, hi) in sorted(st.items(), key=lambda kv: -kv[1][2]):
+        lines.append(f"{k[:70]:70s} {n:6d} {avg:10.1f} {lo:10.1f} {hi:10.1f} {100 * total / tot:7.2f}")
     with open(os.path.join(a.out, f"kernel_trace_{a.tag}_{a.dtype}.txt"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
