@@ -153,6 +153,24 @@ __global__ __launch_bounds__(kThreads) void k_degrees(const int32_t* __restrict_
 // offsets within their bucket, (4) count each bucket in a 32 KB LDS
 // histogram and store the counts.
 // ------------------------------------------------------------------------
+// Tile of this workgroup in an XCD-blocked order.  Workgroups are handed to
+// the eight XCDs in turn (w % 8), so with tile = w the tiles one L2 sees are
+// eight apart, and the tile-minor histogram entries of neighbouring tiles
+// (32 to a 128-byte line) are written and read as partial lines through
+// eight different L2s.  Here XCD x takes the contiguous run
+// [x * per, (x + 1) * per) of tiles.  The grid is xcd_grid(ntiles)
+// workgroups; the spare ones get -1.  Any dispatch order gives the same
+// result; only the locality depends on it.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int64_t xcd_tile(int64_t ntiles) {
+  const int64_t per = (ntiles + kXcds - 1) / kXcds;
+  const int64_t w = blockIdx.x, t = (w % kXcds) * per + w / kXcds;
+  return t < ntiles ? t : -1;
+}
+inline unsigned xcd_grid(int64_t ntiles) {
+  return (unsigned)(kXcds * ((ntiles + kXcds - 1) / kXcds));
+}
+
 constexpr int kBucketBits = 13;
 constexpr int kBucketSize = 1 << kBucketBits;
 constexpr int kMaxBuckets = 2048;  // keeps the scatter's LDS within 64 KB
@@ -167,11 +185,13 @@ __global__ __launch_bounds__(kThreads) void k_outdeg_hist(const int32_t* __restr
                                                           int64_t ntiles, int32_t* counts) {
   extern __shared__ int32_t h[];  // [kThreads / 64][nb]
   constexpr int NW = kThreads / 64;
+  const int64_t tile = xcd_tile(ntiles);
+  if (tile < 0) return;
   for (int b = threadIdx.x; b < NW * nb; b += kThreads) h[b] = 0;
   __syncthreads();
   int32_t* hw = h + (threadIdx.x >> 6) * nb;
   int err = 0;
-  const int64_t base = blockIdx.x * (int64_t)kEdgeTile;
+  const int64_t base = tile * (int64_t)kEdgeTile;
   int32_t c[kEdgeItems];
 #pragma unroll
   for (int j = 0; j < kEdgeItems; ++j) {
@@ -196,7 +216,7 @@ __global__ __launch_bounds__(kThreads) void k_outdeg_hist(const int32_t* __restr
     int32_t t = 0;
 #pragma unroll
     for (int w = 0; w < NW; ++w) t += h[w * nb + b];
-    hist[(int64_t)b * ntiles + blockIdx.x] = t;
+    hist[(int64_t)b * ntiles + tile] = t;
   }
 }
 
@@ -219,7 +239,8 @@ __global__ __launch_bounds__(kThreads) void k_outdeg_scatter(const int32_t* __re
   int32_t* cur = sm + 2 * nb;     // [nb] local cursor
   uint16_t* sval = reinterpret_cast<uint16_t*>(sm + 3 * nb);  // [kEdgeTile]
   uint16_t* sbkt = sval + kEdgeTile;                           // [kEdgeTile]
-  const int64_t tile = blockIdx.x;
+  const int64_t tile = xcd_tile(ntiles);
+  if (tile < 0) return;
   const int64_t base = tile * (int64_t)kEdgeTile;
   const int n = (int)(E - base < kEdgeTile ? E - base : kEdgeTile);
   for (int b = threadIdx.x; b < nb; b += kThreads) {
@@ -356,9 +377,10 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(const int32_t* __restri
                                                          const int32_t* counts) {
   if (counts[kErrFlags]) return;
   __shared__ int32_t h[kBins];
+  const int64_t tile = xcd_tile(ntiles);
+  if (tile < 0) return;
   h[threadIdx.x] = 0;
   __syncthreads();
-  const int64_t tile = blockIdx.x;
 #pragma unroll
   for (int j = 0; j < kItems; ++j) {
     int64_t i = tile * kTile + j * kThreads + threadIdx.x;
@@ -385,7 +407,8 @@ __global__ __launch_bounds__(kThreads) void k_radix_scatter(
   __shared__ int32_t running[kBins];
   __shared__ int32_t wcnt[kThreads / 64][kBins];
   const int t = threadIdx.x, w = t >> 6;
-  const int64_t tile = blockIdx.x;
+  const int64_t tile = xcd_tile(ntiles);
+  if (tile < 0) return;
   running[t] = offsets[(int64_t)t * ntiles + tile];
 #pragma unroll
   for (int k = 0; k < kThreads / 64; ++k) wcnt[k][t] = 0;
@@ -697,10 +720,10 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   if (L.outdeg_bucketed) {
     const int nb = (int)L.outdeg_nb;
     const int64_t et = L.edge_tiles;
-    hipLaunchKernelGGL(k_outdeg_hist, dim3(et), dim3(kThreads), (kThreads / 64) * nb * 4, st,
+    hipLaunchKernelGGL(k_outdeg_hist, dim3(xcd_grid(et)), dim3(kThreads), (kThreads / 64) * nb * 4, st,
                        p.col_idx, E, Vs, nb, ohist, et, p.counts);
     scan(ArrF{ohist}, (int64_t)nb * et, nullptr, ohist, nullptr, tile_sums2, p.counts, st);
-    hipLaunchKernelGGL(k_outdeg_scatter, dim3(et), dim3(kThreads),
+    hipLaunchKernelGGL(k_outdeg_scatter, dim3(xcd_grid(et)), dim3(kThreads),
                        3 * nb * 4 + 2 * kEdgeTile * 2, st, p.col_idx, E, nb, ohist, et, bucketed,
                        p.counts);
     hipLaunchKernelGGL(k_outdeg_count, dim3(kOutdegSplit, nb), dim3(1024), 0, st, bucketed, ohist,
@@ -718,22 +741,22 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 8 * pass;
     if (pass == 0)
-      hipLaunchKernelGGL(k_radix_hist<true>, dim3(ntiles), dim3(kThreads), 0, st, p.d_in,
+      hipLaunchKernelGGL(k_radix_hist<true>, dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st, p.d_in,
                          kin[pass], V, shift, hist, ntiles, p.counts);
     else
-      hipLaunchKernelGGL(k_radix_hist<false>, dim3(ntiles), dim3(kThreads), 0, st, p.d_in,
+      hipLaunchKernelGGL(k_radix_hist<false>, dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st, p.d_in,
                          kin[pass], V, shift, hist, ntiles, p.counts);
     scan(ArrF{hist}, (int64_t)kBins * ntiles, nullptr, hist, nullptr, tile_sums, p.counts, st);
     if (pass == 0)
-      hipLaunchKernelGGL((k_radix_scatter<true, false>), dim3(ntiles), dim3(kThreads), 0, st,
+      hipLaunchKernelGGL((k_radix_scatter<true, false>), dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st,
                          p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
                          vout[pass], p.counts);
     else if (pass < 3)
-      hipLaunchKernelGGL((k_radix_scatter<false, false>), dim3(ntiles), dim3(kThreads), 0, st,
+      hipLaunchKernelGGL((k_radix_scatter<false, false>), dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st,
                          p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
                          vout[pass], p.counts);
     else
-      hipLaunchKernelGGL((k_radix_scatter<false, true>), dim3(ntiles), dim3(kThreads), 0, st,
+      hipLaunchKernelGGL((k_radix_scatter<false, true>), dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st,
                          p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
                          vout[pass], p.counts);
   }
