@@ -189,7 +189,10 @@ typedef struct saga_plan_counts {
 
 /* Bytes of workspace saga_plan_build needs for this graph size.
  * Errors: SAGA_EINVAL on null `bytes`, negative sizes, num_edges >= 2^31,
- * or invalid options (opts may be NULL for the defaults). */
+ * a total segment cost num_edges + row_cost * (num_dst + ceil(num_edges /
+ * seg_len)) of 2^31 - 1 or more (with the options in effect: every edge
+ * offset and cost prefix is an int32), or invalid options (opts may be NULL
+ * for the defaults). */
 saga_status saga_plan_workspace_size(int32_t num_dst, int32_t num_src, int64_t num_edges,
                                      const saga_plan_opts* opts, size_t* bytes);
 

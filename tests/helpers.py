@@ -65,3 +65,21 @@ def tiny_graphs():
     d = (rng.integers(0, n, 300) // 2).tolist()  # upper half of ids: empty rows
     out.append(("random", n, s, d))
     return out
+
+
+def plan_edge_limit(num_dst, seg_len, row_cost):
+    """Largest num_edges a plan accepts (the header's rule): num_edges < 2^31
+    and the total segment cost num_edges + row_cost * (num_dst +
+    ceil(num_edges / seg_len)) below 2^31 - 1."""
+    def ok(e):
+        return e < 2**31 and e + row_cost * (num_dst + -(-e // seg_len)) <= 2**31 - 2
+
+    lo, hi = 0, 2**31 - 1
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        if ok(mid):
+            lo = mid
+        else:
+            hi = mid - 1
+    return lo
+

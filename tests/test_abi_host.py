@@ -60,6 +60,21 @@ def test_plan_workspace_size_rules(S):
         assert e.value.status == S.SAGA_EINVAL
 
 
+def test_plan_edge_limit(S):
+    """The largest graph a plan takes: every int32 edge offset and segment
+    cost prefix must fit, so the limit depends on num_dst, seg_len and
+    row_cost; one edge more is refused before anything is allocated."""
+    from helpers import plan_edge_limit
+
+    for V, T, c in [(1 << 21, 512, 4), (1000, 64, 1), (1 << 27, 4096, 8), (0, 512, 4)]:
+        opts = S.saga_plan_opts(T, T + c, c)
+        E = plan_edge_limit(V, T, c)
+        assert S.saga_plan_workspace_size(V, V, E, opts) > 0
+        with pytest.raises(S.SagaError) as e:
+            S.saga_plan_workspace_size(V, V, E + 1, opts)
+        assert e.value.status == S.SAGA_EINVAL
+
+
 def test_plan_build_rejects_bad_arguments_without_launching(S):
     ws = C.create_string_buffer(1 << 16)
     with pytest.raises(S.SagaError) as e:
