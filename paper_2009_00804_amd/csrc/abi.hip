@@ -121,6 +121,7 @@ struct Carve {
 saga::GatherArgs gather_args_from_plan(const saga_plan& p) {
   saga::GatherArgs a;
   memset(&a, 0, sizeof(a));
+  a.block_cost = p.block_cost;
   a.row_ptr = p.row_ptr;
   a.col_idx = p.col_idx;
   a.d_in = p.d_in;

@@ -57,6 +57,8 @@ struct GatherArgs {
   const int32_t* counts;
   int64_t max_blocks;
   int64_t max_split;
+  int block_cost;  // the plan's row-block cost
+  int bpw;         // row blocks per workgroup (set by the launchers; >= 1)
   // op
   int msg, reduce, dtype, heads, head_mean, dst_norm, act;
   float neg_slope;

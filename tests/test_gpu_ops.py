@@ -186,6 +186,78 @@ def test_gather_gated(gname):
     assert rel_err(to_np(out), ref) <= FP32_TOL
 
 
+@pytest.fixture(scope="module")
+def blocky():
+    """R-MAT with 2^16 vertices and 1 M edges, planned with 256-cost row
+    blocks and 64-edge segments: about 5,400 blocks, so the launcher hands
+    each workgroup four consecutive blocks (blocks are paired up while a
+    workgroup holds at most 2048 cost units and 1024 workgroups remain)."""
+    from synth import configs as C_
+
+    d = C_.build("sage_rmat", scale=16, key=1603)
+    rp, col, n = d["row_ptr"], d["col_idx"], d["num_vertices"]
+    return rp, col, n, graph(rp, col, num_src=n, seg_len=64, block_cost=256, row_cost=4)
+
+
+@pytest.mark.parametrize("F", [64, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gather_merged_blocks(blocky, F, dtype):
+    S = lib()
+    rp, col, n, g = blocky
+    rng = np.random.default_rng(F + 1)
+    X = rng.standard_normal((n, F)).astype(np.float32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    if dtype == "bf16":
+        X = _bf16_round(X)
+    Xt = dev_padded(X, tdt)
+    tol = FP32_TOL if dtype == "f32" else BF16_TOL
+    bias = rng.standard_normal(F)
+    for red, msg, dn, b, act in [("sum", "copy", 0, None, "none"),
+                                 ("mean", "src_norm", 1, bias, "relu")]:
+        print(f"gather merged blocks F={F} {dtype} {red} {msg}", flush=True)
+        out = run_gather(g, Xt, dict(reduce={"sum": S.SAGA_RED_SUM, "mean": S.SAGA_RED_MEAN}[red],
+                                     msg={"copy": S.SAGA_MSG_COPY, "src_norm": S.SAGA_MSG_SRC_NORM}[msg],
+                                     dst_norm=dn, act=act), F, tdt, bias=b)
+        assert rel_err(to_np(out), _ref_simple(rp, col, X, red, msg, dn, b, act, n)) <= tol
+    print(f"gather merged blocks F={F} {dtype} max", flush=True)
+    out = run_gather(g, Xt, dict(reduce=S.SAGA_RED_MAX), F, tdt)
+    assert np.array_equal(to_np(out), O.gather(rp, col, X, "max"))
+
+
+def test_gather_attention_and_gated_merged_blocks(blocky):
+    S = lib()
+    rp, col, n, g = blocky
+    rng = np.random.default_rng(3)
+    heads, D = 8, 8
+    F = heads * D
+    Zx = rng.standard_normal((n, F + 2 * heads)).astype(np.float32)
+    zt = dev_padded(Zx, torch.float32)
+    print("gather attention merged blocks", flush=True)
+    out = run_gather(g, zt[:, :F], dict(msg=S.SAGA_MSG_GAT, reduce=S.SAGA_RED_SOFTMAX, heads=heads,
+                                        neg_slope=0.2), F, torch.float32,
+                     el=zt[:, F:F + heads], er=zt[:, F + heads:])
+    ref = O.attention_gather(rp, col, Zx[:, :F], Zx[:, F:F + heads], Zx[:, F + heads:], heads, 0.2)
+    assert rel_err(to_np(out), ref) <= FP32_TOL
+    E = len(col)
+    Fe = 16
+    H = rng.standard_normal((n, F)).astype(np.float32)
+    Ef = rng.standard_normal((E, Fe)).astype(np.float32)
+    W_e = (rng.standard_normal((2 * F + Fe, F)) * 0.1).astype(np.float32)
+    b_e = rng.standard_normal(F).astype(np.float32)
+    Gs = (H.astype(np.float64) @ W_e[:F]).astype(np.float32)
+    Gd = (H.astype(np.float64) @ W_e[F:2 * F]).astype(np.float32)
+    t = lambda a: dev_padded(a, torch.float32)  # noqa: E731
+    Ht, Gst, Gdt, Eft = t(H), t(Gs), t(Gd), t(Ef)
+    wt = torch.from_numpy(W_e[2 * F:].copy()).to(device())
+    bt = torch.from_numpy(b_e).to(device())
+    extra = dict(gate_src=S.cmat(Gst), gate_dst=S.cmat(Gdt), edge_feat=S.cmat(Eft),
+                 w_edge=wt.data_ptr(), gate_bias=bt.data_ptr())
+    print("gather gated merged blocks", flush=True)
+    out = run_gather(g, Ht, dict(msg=S.SAGA_MSG_GATED, reduce=S.SAGA_RED_SUM), F, torch.float32,
+                     extra=extra)
+    assert rel_err(to_np(out), O.gated_gather(rp, col, H, Ef, W_e, b_e)) <= FP32_TOL
+
+
 def test_gather_deterministic():
     S = lib()
     rp, col, n, g = _get_graph("rmat")
