@@ -474,13 +474,11 @@ __global__ __launch_bounds__(kThreads) void k_combine(GatherArgs a) {
       float A = red == kMax ? -INFINITY : 0.0f, M = -INFINITY, L = 0.0f;
       if (on) {
         const int hd = (red == kSoftmax && colc < F) ? colc / D : 0;
-        for (int j = f0 + sp; j < f1; j += spl) {
-          const float* p = a.partial + (int64_t)j * a.pstride;
-          const float v = p[colc];
+        // partial j merged into (A, M, L); the order of j is kept
+        auto merge = [&](float v, float mj, float lj) {
           if (red == kMax) {
             A = fmaxf(A, v);
           } else if (red == kSoftmax) {
-            const float mj = p[pc + hd], lj = p[pc + H + hd];
             const float mn = fmaxf(M, mj);
             const float fa = __expf(M - mn), fb = __expf(mj - mn);
             A = A * fa + v * fb;
@@ -489,6 +487,26 @@ __global__ __launch_bounds__(kThreads) void k_combine(GatherArgs a) {
           } else {
             A += v;
           }
+        };
+        // a hub row has hundreds of segments: UJ of its partials are read
+        // before any is merged, so their loads overlap
+        constexpr int UJ = 8;
+        int j = f0 + sp;
+        for (; j + (UJ - 1) * spl < f1; j += UJ * spl) {
+          float v[UJ], mj[UJ], lj[UJ];
+#pragma unroll
+          for (int u = 0; u < UJ; ++u) {
+            const float* p = a.partial + (int64_t)(j + u * spl) * a.pstride;
+            v[u] = p[colc];
+            mj[u] = red == kSoftmax ? p[pc + hd] : 0.0f;
+            lj[u] = red == kSoftmax ? p[pc + H + hd] : 0.0f;
+          }
+#pragma unroll
+          for (int u = 0; u < UJ; ++u) merge(v[u], mj[u], lj[u]);
+        }
+        for (; j < f1; j += spl) {
+          const float* p = a.partial + (int64_t)j * a.pstride;
+          merge(p[colc], red == kSoftmax ? p[pc + hd] : 0.0f, red == kSoftmax ? p[pc + H + hd] : 0.0f);
         }
       }
       sm_acc[t] = A;
