@@ -19,6 +19,7 @@
 //     partials, merged in segment order by k_combine (deterministic: no
 //     floating-point atomics anywhere).
 #include <algorithm>
+#include <utility>
 #include <cstdlib>
 
 #include "saga_device.h"
@@ -340,8 +341,24 @@ __global__ __launch_bounds__(kThreads) void k_gather_gat(GatherArgs a) {
 // Gated messages: sigmoid(gs[u] + gd[v] + b_e + e_uv W_ee) * h[u], SUM
 // (float32, F = 64, one 16-byte slice of 4 features per lane)
 // ------------------------------------------------------------------------
+// pre += sum_j e_j W[j][4 columns of this lane], e_j held by lane j of the
+// lane's 16-lane group: ds_swizzle in bit mode reads lane (lane & 16) | j of
+// each 32-lane half, i.e. lane j of the group (every lane takes part)
+template <int J>
+__device__ __forceinline__ void project_one(float ev, const float (&wr)[16][4], float (&pre)[4]) {
+  const float ej = __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(ev), 0x10 | (J << 5)));
+#pragma unroll
+  for (int q = 0; q < 4; ++q) pre[q] += ej * wr[J][q];
+}
+template <int... J>
+__device__ __forceinline__ void project_edge(float ev, const float (&wr)[16][4], float (&pre)[4],
+                                             std::integer_sequence<int, J...>) {
+  (project_one<J>(ev, wr, pre), ...);
+}
+
 template <int LPR, int U>
 __global__ __launch_bounds__(kThreads) void k_gather_gated(GatherArgs a) {
+  static_assert(LPR == 16, "the edge-feature broadcast works on 16-lane groups");
   constexpr int NG = kThreads / LPR;
   constexpr int FE_MAX = 16;
   const int32_t* __restrict__ counts = a.counts;
@@ -385,35 +402,26 @@ __global__ __launch_bounds__(kThreads) void k_gather_gated(GatherArgs a) {
         // U edges' loads (h_u, S_src[u], e_uv) in flight before the math;
         // a short last batch repeats its first edge and skips it
         for (int t = 0; t < n; t += U) {
-          float hs[U][4], gs[U][4], ev[U][FE_MAX];
+          // e_uv: lane j of the group holds feature j (one coalesced row
+          // load per edge), broadcast to the group inside the projection
+          float hs[U][4], gs[U][4], ev[U];
 #pragma unroll
           for (int k = 0; k < U; ++k) {
             const int tk = t + k < n ? t + k : t;
             const int u = __shfl(c, gbase + tk, 64);
+            ev[k] = gl < Fe ? a.efeat[(int64_t)(e + tk) * a.ld_efeat + gl] : 0.0f;
             if (active) {
               Vec16<float>::load(h + (int64_t)u * a.ld_src + gl * 4, hs[k]);
               Vec16<float>::load(a.gsrc + (int64_t)u * a.ld_gsrc + gl * 4, gs[k]);
-              const float* ef = a.efeat + (int64_t)(e + tk) * a.ld_efeat;
-#pragma unroll
-              for (int i4 = 0; i4 < FE_MAX / 4; ++i4) {
-                float v4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                if (i4 * 4 < Fe) Vec16<float>::load(ef + i4 * 4, v4);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) ev[k][i4 * 4 + j] = v4[j];
-              }
             }
           }
-          if (!active) continue;
 #pragma unroll
           for (int k = 0; k < U; ++k) {
-            if (t + k < n) {
-              float pre[4];
+            float pre[4];
 #pragma unroll
-              for (int q = 0; q < 4; ++q) pre[q] = gs[k][q] + gd[q];
-#pragma unroll
-              for (int j = 0; j < FE_MAX; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) pre[q] += ev[k][j] * wr[j][q];
+            for (int q = 0; q < 4; ++q) pre[q] = gs[k][q] + gd[q];
+            project_edge(ev[k], wr, pre, std::make_integer_sequence<int, FE_MAX>{});
+            if (active && t + k < n) {
 #pragma unroll
               for (int q = 0; q < 4; ++q) acc[q] += sigmoidf_(pre[q]) * hs[k][q];
             }
