@@ -633,18 +633,30 @@ __device__ __forceinline__ void store_staged(const GemmArgs& g, int64_t row0, in
   }
 }
 
-// staged stores need room in the ring for every wave's rows
+// staged stores need room in the ring for every wave's rows (kStaged), or
+// at least for 16 rows of every wave, staged one 16-row slab at a time
 template <typename T, int MT, int NT, typename R>
 constexpr bool kStaged =
     (size_t)(R::THREADS / 64) * 16 * MT * 16 * NT * sizeof(T) <= R::LDS_BYTES;
+template <typename T, int NT, typename R>
+constexpr bool kStagedSlab = (size_t)(R::THREADS / 64) * 16 * 16 * NT * sizeof(T) <= R::LDS_BYTES;
 
 template <typename T, int MT, int NT, typename R>
 __device__ __forceinline__ void store_tile(const GemmArgs& g, int64_t row0, int64_t n0,
                                            const f32x4 (&acc)[MT][NT], uint4* ring) {
+  const int wave = threadIdx.x >> 6;
   if constexpr (kStaged<T, MT, NT, R>) {
-    const int wave = threadIdx.x >> 6;
     store_staged<T, MT, NT>(g, row0, n0, acc,
                             reinterpret_cast<T*>(ring) + (size_t)wave * 16 * MT * 16 * NT);
+  } else if constexpr (kStagedSlab<T, NT, R>) {
+    T* region = reinterpret_cast<T*>(ring) + (size_t)wave * 16 * 16 * NT;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      // the previous slab's read-back stays ahead of this slab's writes
+      asm volatile("" ::: "memory");
+      store_staged<T, 1, NT>(g, row0 + mt * 16, n0,
+                             reinterpret_cast<const f32x4(&)[1][NT]>(acc[mt]), region);
+    }
   } else {
     store_direct<T, MT, NT>(g, row0, n0, acc);
   }
