@@ -905,13 +905,20 @@ hipError_t dispatch(const GemmArgs& g, hipStream_t st) {
   const Tiling t = choose(g.dtype, g.mode, g.N, g.mode == SAGA_GEMM_CONCAT ? g.K + g.K2 : g.K);
   if (g.mode == SAGA_GEMM_GRU) {
     dim3 grid((unsigned)((g.M + 63) / 64));
+    // two stages when both products have at most four k chunks (as for the
+    // narrow plain tiles)
+    const bool two = chunks(g.dtype, std::max(g.K, g.K2)) <= 4;
+#define SAGA_GRU(N3)                                                                     \
+  if (two) hipLaunchKernelGGL((k_gemm_gru<T, N3, 2>), grid, dim3(kThreads), 0, st, g);  \
+  else hipLaunchKernelGGL((k_gemm_gru<T, N3, 4>), grid, dim3(kThreads), 0, st, g)
     switch (t.nt) {
-      case 3: hipLaunchKernelGGL((k_gemm_gru<T, 1, 4>), grid, dim3(kThreads), 0, st, g); break;
-      case 6: hipLaunchKernelGGL((k_gemm_gru<T, 2, 4>), grid, dim3(kThreads), 0, st, g); break;
-      case 9: hipLaunchKernelGGL((k_gemm_gru<T, 3, 4>), grid, dim3(kThreads), 0, st, g); break;
-      case 12: hipLaunchKernelGGL((k_gemm_gru<T, 4, 4>), grid, dim3(kThreads), 0, st, g); break;
+      case 3: SAGA_GRU(1); break;
+      case 6: SAGA_GRU(2); break;
+      case 9: SAGA_GRU(3); break;
+      case 12: SAGA_GRU(4); break;
       default: return hipErrorInvalidValue;
     }
+#undef SAGA_GRU
     return hipGetLastError();
   }
   switch (t.nt) {
