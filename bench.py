@@ -22,6 +22,7 @@ import os
 import statistics
 import sys
 import time
+import types
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -251,6 +252,32 @@ def noreuse_bytes(step, stage):
     F = hid if stage == "gather1" else f_out
     row = (F * es + 15) // 16 * 16
     return E * (4 + row) + (V + 1) * 4 + V * F * es
+
+
+def stage_rooflines(V, E, dims, dtype, mean):
+    """Every stage of the step against its roofline: the GEMMs against the
+    dtype's dense MFMA peak (and HBM for their compulsory bytes), the
+    Gathers against 8 TB/s for their compulsory bytes, and, where the
+    counter record in profiles/ matches the kernel source, for the measured
+    FETCH_SIZE + WRITE_SIZE traffic."""
+    shim = types.SimpleNamespace(V=V, E=E, dims=dims, dtype=dtype)
+    out = {}
+    for n in ("gemm1", "gather1", "gemm2", "gather2"):
+        t = mean[n] * 1e-3
+        byts, flops = algorithmic(shim, n)
+        d = {"ms": round(mean[n], 4), "compulsory_GBps": byts / t / 1e9,
+             "compulsory_frac_of_8TBps": byts / t / PEAK_HBM}
+        if n.startswith("gemm"):
+            d["TFLOPs"] = flops / t / 1e12
+            d["mfma_frac"] = flops / t / PEAK_MFMA[dtype]
+        else:
+            d["noreuse_GBps"] = noreuse_bytes(shim, n) / t / 1e9
+        tr = load_traffic(n, dtype)
+        if tr:
+            d["counter_GBps"] = tr / t / 1e9
+            d["counter_frac_of_8TBps"] = tr / t / PEAK_HBM
+        out[n] = d
+    return out
 
 
 def time_step(step, steps, warmup):
@@ -715,6 +742,7 @@ def main():
         "plan": {"segments": r["counts"].num_segments, "blocks": r["counts"].num_blocks,
                  "split_rows": r["counts"].n_split, "max_in_degree": r["counts"].max_in_degree},
         "roofline": roof,
+        "stage_rooflines": stage_rooflines(V, E, step.dims, args.dtype, r["mean"]),
     }
     out["pipelining"] = {
         "what": "plan's row-order branch (in-degrees, validation, degree sort, segments, "
@@ -731,7 +759,8 @@ def main():
         out.setdefault("variants", {})[dt] = {
             "value": 2 * E / (rr["ms"] * 1e-3), "ms_per_step": rr["ms"],
             "stage_by_stage_ms": rr["ms_seq"], "pipelined_ms": rr["ms_pipe"],
-            "stage_ms": {n: round(rr["mean"][n], 4) for n in rr["mean"]}}
+            "stage_ms": {n: round(rr["mean"][n], 4) for n in rr["mean"]},
+            "stage_rooflines": stage_rooflines(V, E, step.dims, dt, rr["mean"])}
         if "unfused_ms" in rr:
             out["variants"][dt]["fusion"] = {"fused_ms": rr["mean"]["gather1"],
                                              "unfused_ms": rr["unfused_ms"],
