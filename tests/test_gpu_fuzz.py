@@ -1,0 +1,84 @@
+"""Seeded sweep over the corners of the layout and the Gather: random
+graphs (empty-heavy, uniform, power-law, one giant row; fewer or more
+source vertices than destinations), random plan options (segment lengths
+from 1, row costs, block costs down to the smallest allowed, which also
+makes the launcher hand several blocks to a workgroup), random widths
+(1 to 129 columns, fp32 and bf16) and every simple reduction.  The plan is
+compared with the oracle's bit for bit, the Gathers element by element."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import dev_padded, graph, lib, to_np
+from helpers import BF16_TOL, FP32_TOL, rel_err
+from oracle import saga_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+CASES = 200
+
+
+def _bf16_round(a):
+    from synth import tensors as T
+
+    return T.bf16_to_f32(T.bf16_bits(np.asarray(a, np.float32)))
+
+
+def _random_graph(rng):
+    V = int(rng.integers(1, 3000))
+    Vs = int(rng.choice([V, max(1, V // 3), V + int(rng.integers(1, 500))]))
+    kind = rng.choice(["empty", "uniform", "power", "giant"])
+    if kind == "empty":
+        d = np.where(rng.random(V) < 0.8, 0, rng.integers(1, 20, V))
+    elif kind == "uniform":
+        d = rng.integers(0, 12, V)
+    elif kind == "power":
+        d = np.minimum(rng.zipf(1.6, V) - 1, 5000)
+    else:
+        d = rng.integers(0, 4, V)
+        d[int(rng.integers(0, V))] = int(rng.integers(2000, 20000))
+    rp = np.zeros(V + 1, np.int64)
+    np.cumsum(d, out=rp[1:])
+    col = rng.integers(0, Vs, int(rp[-1])).astype(np.int32)
+    # CSR order within a row: by source id (ties keep order)
+    for v in np.flatnonzero(d > 1):
+        col[rp[v]:rp[v + 1]] = np.sort(col[rp[v]:rp[v + 1]], kind="stable")
+    return rp.astype(np.int32), col, V, Vs, kind
+
+
+@pytest.mark.parametrize("case", range(CASES))
+def test_fuzz_plan_and_gather(case):
+    S = lib()
+    rng = np.random.default_rng(9000 + case)
+    rp, col, V, Vs, kind = _random_graph(rng)
+    T = int(rng.choice([1, 2, 3, 5, 8, 16, 33, 64, 512]))
+    c = int(rng.integers(1, 9))
+    B = T + c + int(rng.choice([0, 1, 7, 100, 1000]))
+    F = int(rng.choice([1, 2, 3, 4, 5, 8, 17, 32, 33, 64, 100, 128, 129]))
+    dtype = str(rng.choice(["f32", "bf16"]))
+    print(f"fuzz case {case}: {kind} V={V} Vs={Vs} E={len(col)} seg_len={T} row_cost={c} "
+          f"block_cost={B} F={F} {dtype}", flush=True)
+    g = graph(rp, col, num_src=Vs, seg_len=T, block_cost=B, row_cost=c)
+    got = {k: v.cpu().numpy().astype(np.int64) for k, v in g.arrays().items()}
+    want = O.plan(rp, col, Vs, T, B, c)
+    for k in ("d_in", "d_out", "perm", "row_seg_first", "seg_row", "seg_beg", "seg_end",
+              "block_ptr"):
+        assert np.array_equal(got[k], want[k]), k
+    assert g.counts.n_split == want["n_split"]
+
+    X = rng.standard_normal((Vs, F)).astype(np.float32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    if dtype == "bf16":
+        X = _bf16_round(X)
+    Xt = dev_padded(X, tdt)
+    tol = FP32_TOL if dtype == "f32" else BF16_TOL
+    from test_gpu_ops import run_gather
+
+    for red in ("sum", "mean", "max"):
+        code = {"sum": S.SAGA_RED_SUM, "mean": S.SAGA_RED_MEAN, "max": S.SAGA_RED_MAX}[red]
+        out = to_np(run_gather(g, Xt, dict(reduce=code), F, tdt))
+        ref = O.gather(rp, col, X, red)
+        if red == "max":
+            assert np.array_equal(out, ref), red
+        else:
+            assert rel_err(out, ref) <= tol, red
