@@ -1,4 +1,6 @@
-"""Seeded sweep over the corners of the layout and the Gather: random
+"""Seeded sweeps over the corners of the layout, the Gather and the GEMM.
+
+Layout and Gather: random
 graphs (empty-heavy, uniform, power-law, one giant row; fewer or more
 source vertices than destinations), random plan options (segment lengths
 from 1, row costs, block costs down to the smallest allowed, which also
@@ -82,3 +84,44 @@ def test_fuzz_plan_and_gather(case):
             assert np.array_equal(out, ref), red
         else:
             assert rel_err(out, ref) <= tol, red
+
+
+GEMM_CASES = 120
+
+
+@pytest.mark.parametrize("case", range(GEMM_CASES))
+def test_fuzz_gemm(case):
+    """Random shapes across every tile path (narrow two- and four-stage
+    tiles, the LDS-ring and register-A wide tiles, concat), ragged M, K and
+    N, with a random epilogue (row scale, bias, activation)."""
+    from test_gpu_ops import run_gemm
+
+    rng = np.random.default_rng(7000 + case)
+    M = int(rng.integers(1, 3000))
+    K = int(rng.choice([1, 3, 16, 31, 32, 33, 64, 100, 128, 129, 255, 602, 700]))
+    N = int(rng.choice([1, 3, 8, 16, 17, 41, 64, 80, 81, 96, 128, 129, 200, 256, 300]))
+    dtype = str(rng.choice(["f32", "bf16"]))
+    act = str(rng.choice(["none", "relu", "elu", "sigmoid", "tanh"]))
+    concat = bool(rng.random() < 0.25)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((K, N)) / np.sqrt(K)).astype(np.float32)
+    A2 = W2 = None
+    if concat:
+        K2 = int(rng.choice([1, 32, 77, 128]))
+        A2 = rng.standard_normal((M, K2)).astype(np.float32)
+        W2 = (rng.standard_normal((K2, N)) / np.sqrt(K2)).astype(np.float32)
+    if dtype == "bf16":
+        A, W = _bf16_round(A), _bf16_round(W)
+        if concat:
+            A2, W2 = _bf16_round(A2), _bf16_round(W2)
+    bias = rng.standard_normal(N) if rng.random() < 0.5 else None
+    deg = rng.integers(0, 9, M) if rng.random() < 0.5 else None
+    print(f"fuzz gemm {case}: M={M} K={K} N={N} {dtype} {act} concat={concat} "
+          f"bias={bias is not None} deg={deg is not None}", flush=True)
+    out = run_gemm(A, W, dtype, bias=bias, act=act, deg=deg, A2=A2, W2=W2,
+                   mode="concat" if concat else "plain")
+    AA = np.concatenate([A, A2], 1) if concat else A
+    WW = np.concatenate([W, W2], 0) if concat else W
+    ref = O.dense(AA, WW, bias=bias, act=act,
+                  row_scale=None if deg is None else O.degree_scale(deg))
+    assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
