@@ -125,3 +125,97 @@ def test_fuzz_gemm(case):
     ref = O.dense(AA, WW, bias=bias, act=act,
                   row_scale=None if deg is None else O.degree_scale(deg))
     assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
+
+
+def _small_graph(rng, vmax, dmax, long_row=0):
+    V = int(rng.integers(1, vmax))
+    d = rng.integers(0, dmax, V)
+    d[rng.random(V) < 0.2] = 0
+    if long_row and V > 1:
+        d[int(rng.integers(0, V))] = long_row
+    rp = np.zeros(V + 1, np.int64)
+    np.cumsum(d, out=rp[1:])
+    col = rng.integers(0, V, int(rp[-1])).astype(np.int32)
+    for v in np.flatnonzero(d > 1):
+        col[rp[v]:rp[v + 1]] = np.sort(col[rp[v]:rp[v + 1]], kind="stable")
+    return rp.astype(np.int32), col, V
+
+
+@pytest.mark.parametrize("case", range(60))
+def test_fuzz_attention(case):
+    """Edge-softmax Gather over random graphs, head counts and widths."""
+    from test_gpu_ops import run_gather
+
+    S = lib()
+    rng = np.random.default_rng(5000 + case)
+    rp, col, V, Vs, kind = _random_graph(rng)
+    H = int(rng.choice([1, 2, 4, 8, 16]))
+    D = int(rng.choice([d for d in (4, 8, 12, 16, 32, 64) if H * d <= 256]))
+    F = H * D
+    head_mean = int(rng.random() < 0.4 and (F // 4) & (F // 4 - 1) == 0)
+    T = int(rng.choice([1, 4, 16, 64, 512]))
+    c = int(rng.integers(1, 9))
+    g = graph(rp, col, num_src=Vs, seg_len=T, block_cost=T + c + int(rng.choice([0, 50, 900])),
+              row_cost=c)
+    Z = rng.standard_normal((Vs, F + H)).astype(np.float32)
+    er = rng.standard_normal((V, H)).astype(np.float32)
+    zt, ert = dev_padded(Z), dev_padded(er)
+    bias = rng.standard_normal(D if head_mean else F)
+    print(f"fuzz attention {case}: {kind} V={V} Vs={Vs} E={len(col)} H={H} D={D} "
+          f"mean={head_mean} seg_len={T}", flush=True)
+    out = run_gather(g, zt[:, :F], dict(msg=S.SAGA_MSG_GAT, reduce=S.SAGA_RED_SOFTMAX, heads=H,
+                                        head_mean=head_mean, act="elu", neg_slope=0.2),
+                     D if head_mean else F, torch.float32, el=zt[:, F:], er=ert, bias=bias)
+    o = O.attention_gather(rp, col, Z[:, :F], Z[:, F:], er, H, 0.2)
+    if head_mean:
+        o = o.reshape(V, H, D).mean(axis=1)
+    assert rel_err(to_np(out), O.elu(o + bias[None, :])) <= FP32_TOL
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_fuzz_rgcn_layer(case):
+    """R-GCN layers over random graphs, relation counts, type skews and
+    widths (typed layout, grouped transform, typed Gather with self term)."""
+    from paper_2009_00804_amd import layers as LY
+
+    S = lib()
+    rng = np.random.default_rng(6000 + case)
+    rp, col, V = _small_graph(rng, 1200, int(rng.choice([3, 12, 40])),
+                              long_row=int(rng.choice([0, 0, 2500])))
+    R = int(rng.choice([1, 2, 3, 7, 32]))
+    p = 1.0 / (np.arange(R) + 1.0) ** float(rng.choice([0.0, 1.0, 2.0]))
+    et = rng.choice(R, size=len(col), p=p / p.sum()).astype(np.int32)
+    Fi = int(rng.choice([4, 20, 64, 128]))
+    Fo = int(rng.choice([8, 36, 64, 100]))
+    dtype = str(rng.choice(["f32", "bf16"]))
+    X = rng.standard_normal((V, Fi)).astype(np.float32)
+    W_rel = (rng.standard_normal((R, Fi, Fo)) / np.sqrt(Fi)).astype(np.float32)
+    W_self = (rng.standard_normal((Fi, Fo)) / np.sqrt(Fi)).astype(np.float32)
+    b = (rng.standard_normal(Fo) * 0.1).astype(np.float32)
+    if dtype == "bf16":
+        X, W_rel, W_self = _bf16_round(X), _bf16_round(W_rel), _bf16_round(W_self)
+    print(f"fuzz rgcn {case}: V={V} E={len(col)} R={R} {Fi}->{Fo} {dtype}", flush=True)
+    g = graph(rp, col)
+    rg = S.RelGraph(g, torch.from_numpy(et).to(g.row_ptr.device), R)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    model = LY.rgcn(g, rg, dict(W_rel=W_rel, W_self=W_self, b=b, act="relu"), dtype=tdt)
+    y = LY.run(model, dev_padded(X, dtype=tdt))
+    torch.cuda.synchronize()
+    want = O.rgcn_layer(rp, col, et, X, W_rel, W_self, b, act="relu")
+    assert rel_err(to_np(y), want) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_fuzz_lstm_gather(case):
+    """LSTM Gather over random graphs (empty rows, a long row) and H."""
+    from test_gpu_lstm import _ref, run_lstm
+
+    rng = np.random.default_rng(4000 + case)
+    rp, col, V = _small_graph(rng, 400, int(rng.choice([2, 10, 60])),
+                              long_row=int(rng.choice([0, 1100, 2100])))
+    H = int(rng.choice([32, 64, 128]))
+    P = (rng.standard_normal((V, 4 * H)) * 0.5).astype(np.float32)
+    W_hh = (rng.standard_normal((H, 4 * H)) / np.sqrt(H)).astype(np.float32)
+    print(f"fuzz lstm {case}: V={V} E={len(col)} H={H}", flush=True)
+    g = graph(rp, col)
+    assert rel_err(run_lstm(g, P, W_hh), _ref(rp, col, P, W_hh)) <= FP32_TOL
