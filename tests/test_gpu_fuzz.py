@@ -219,3 +219,54 @@ def test_fuzz_lstm_gather(case):
     print(f"fuzz lstm {case}: V={V} E={len(col)} H={H}", flush=True)
     g = graph(rp, col)
     assert rel_err(run_lstm(g, P, W_hh), _ref(rp, col, P, W_hh)) <= FP32_TOL
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_fuzz_gated_and_unfused(case):
+    """Gated-message Gather (edge features of 4 to 16 columns) and the
+    unfused baseline (edge tensor, then segment reduction) over random
+    graphs and plan options."""
+    from test_gpu_ops import run_gather
+    from test_gpu_unfused import run_unfused
+
+    S = lib()
+    rng = np.random.default_rng(3000 + case)
+    rp, col, V, Vs, kind = _random_graph(rng)
+    T = int(rng.choice([1, 4, 16, 64, 512]))
+    c = int(rng.integers(1, 9))
+    g = graph(rp, col, num_src=Vs, seg_len=T, block_cost=T + c + int(rng.choice([0, 50, 900])),
+              row_cost=c)
+    E = len(col)
+    print(f"fuzz gated/unfused {case}: {kind} V={V} Vs={Vs} E={E} seg_len={T}", flush=True)
+    if Vs == V:  # the gated layer's sources are its destinations
+        F, Fe = 64, int(rng.choice([4, 8, 12, 16]))
+        H = rng.standard_normal((V, F)).astype(np.float32)
+        Ef = rng.standard_normal((E, Fe)).astype(np.float32)
+        W_e = (rng.standard_normal((2 * F + Fe, F)) * 0.1).astype(np.float32)
+        b_e = rng.standard_normal(F).astype(np.float32)
+        Gs = (H.astype(np.float64) @ W_e[:F]).astype(np.float32)
+        Gd = (H.astype(np.float64) @ W_e[F:2 * F]).astype(np.float32)
+        t = lambda a: dev_padded(a, torch.float32)  # noqa: E731
+        Ht, Gst, Gdt = t(H), t(Gs), t(Gd)
+        Eft = t(Ef) if E else torch.zeros((0, Fe), device=Ht.device)
+        wt = torch.from_numpy(W_e[2 * F:].copy()).to(Ht.device)
+        bt = torch.from_numpy(b_e).to(Ht.device)
+        extra = dict(gate_src=S.cmat(Gst), gate_dst=S.cmat(Gdt), edge_feat=S.cmat(Eft),
+                     w_edge=wt.data_ptr(), gate_bias=bt.data_ptr())
+        out = run_gather(g, Ht, dict(msg=S.SAGA_MSG_GATED, reduce=S.SAGA_RED_SUM), F,
+                         torch.float32, extra=extra)
+        assert rel_err(to_np(out), O.gated_gather(rp, col, H, Ef, W_e, b_e)) <= FP32_TOL
+    dtype = str(rng.choice(["f32", "bf16"]))
+    Fu = int(rng.choice([1, 8, 41, 128]))
+    X = rng.standard_normal((Vs, Fu)).astype(np.float32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    if dtype == "bf16":
+        X = _bf16_round(X)
+    for red in ("sum", "max"):
+        code = S.SAGA_RED_SUM if red == "sum" else S.SAGA_RED_MAX
+        got = to_np(run_unfused(g, dev_padded(X, tdt), dict(reduce=code), Fu, tdt))
+        ref = O.gather(rp, col, X, red)
+        if red == "max":
+            assert np.array_equal(got, ref)
+        else:
+            assert rel_err(got, ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
