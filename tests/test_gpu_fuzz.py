@@ -270,3 +270,63 @@ def test_fuzz_gated_and_unfused(case):
             assert np.array_equal(got, ref)
         else:
             assert rel_err(got, ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_fuzz_layers(case):
+    """Whole layers through saga_layer over random graphs and widths: GCN
+    (fp32 / bf16, either association order, every activation), SAGE-pool
+    and GAT (concatenated or averaged heads)."""
+    from paper_2009_00804_amd import layers as LY
+
+    rng = np.random.default_rng(2000 + case)
+    rp, col, V = _small_graph(rng, 2500, int(rng.choice([3, 12, 40])),
+                              long_row=int(rng.choice([0, 0, 1500])))
+    g = graph(rp, col)
+    kind = str(rng.choice(["gcn", "sage_pool", "gat"]))
+    if kind == "gcn":
+        Fi = int(rng.choice([1, 8, 41, 64, 128, 300]))
+        Fo = int(rng.choice([1, 16, 41, 64, 128, 200]))
+        dtype = str(rng.choice(["f32", "bf16"]))
+        act = str(rng.choice(["none", "relu", "elu", "sigmoid", "tanh"]))
+        X = rng.standard_normal((V, Fi)).astype(np.float32)
+        W = (rng.standard_normal((Fi, Fo)) / np.sqrt(Fi)).astype(np.float32)
+        b = rng.standard_normal(Fo).astype(np.float32)
+        if dtype == "bf16":
+            X, W = _bf16_round(X), _bf16_round(W)
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        print(f"fuzz layer {case}: gcn V={V} E={len(col)} {Fi}->{Fo} {dtype} {act}", flush=True)
+        layer = LY.Layer(g, "gcn", Fi, Fo, {"w": W, "b": b}, dtype=tdt, act=act)
+        y = to_np(LY.run([layer], dev_padded(X, tdt)))
+        tol = FP32_TOL if dtype == "f32" else BF16_TOL
+        assert rel_err(y, O.gcn_layer(rp, col, X, W, b, act)) <= tol
+    elif kind == "sage_pool":
+        F = int(rng.choice([8, 32, 64, 100, 256]))
+        Fo = int(rng.choice([8, 64, 256]))
+        X = rng.standard_normal((V, F)).astype(np.float32)
+        gw = dict(W_pool=(rng.standard_normal((F, F)) / np.sqrt(F)).astype(np.float32),
+                  b_pool=rng.standard_normal(F).astype(np.float32),
+                  W=(rng.standard_normal((2 * F, Fo)) / np.sqrt(2 * F)).astype(np.float32),
+                  b=rng.standard_normal(Fo).astype(np.float32))
+        print(f"fuzz layer {case}: sage_pool V={V} E={len(col)} {F}->{Fo}", flush=True)
+        y = to_np(LY.run(LY.sage_pool(g, gw), dev_padded(X)))
+        want = O.sage_pool_layer(rp, col, X, gw["W_pool"], gw["b_pool"], gw["W"], gw["b"])
+        assert rel_err(y, want) <= FP32_TOL
+    else:
+        H = int(rng.choice([1, 2, 4, 8]))
+        D = int(rng.choice([4, 8, 16]))
+        Fi = int(rng.choice([16, 64, 512]))
+        mean = bool(rng.random() < 0.5)
+        X = rng.standard_normal((V, Fi)).astype(np.float32)
+        W = (rng.standard_normal((Fi, H * D)) / np.sqrt(Fi)).astype(np.float32)
+        al = rng.standard_normal((H, D)).astype(np.float32)
+        ar = rng.standard_normal((H, D)).astype(np.float32)
+        b = rng.standard_normal(D if mean else H * D).astype(np.float32)
+        act = "none" if mean else "elu"
+        print(f"fuzz layer {case}: gat V={V} E={len(col)} {Fi}->{H}x{D} mean={mean}", flush=True)
+        layer = LY.Layer(g, "gat", Fi, D if mean else H * D,
+                         {"w": W, "b": b, "attn_l": al, "attn_r": ar}, heads=H, head_mean=mean,
+                         act=act)
+        y = to_np(LY.run([layer], dev_padded(X)))
+        want = O.gat_layer(rp, col, X, W, al, ar, b, H, "mean" if mean else "concat", act)
+        assert rel_err(y, want) <= FP32_TOL
