@@ -27,6 +27,7 @@
 // zeros past column K and past row M; every later chunk is a whole 128-byte
 // row segment and needs no masking in k.
 #include <algorithm>
+#include <type_traits>
 #include <cstdlib>
 #include <cstring>
 
@@ -566,6 +567,81 @@ __device__ __forceinline__ void store_direct(const GemmArgs& g, int64_t row0, in
     }
 }
 
+// bfloat16, 128 columns from column 0, through registers: three lane
+// exchanges (partners lr ^ 1 and lr ^ 2 by DPP, lr ^ 4 by swizzle; lr =
+// lane % 16 with bits b0..b3, lg = lane / 16) turn the accumulator layout
+// (rows 4 lg + r of column 16 t + lr) into whole 16-byte row pieces: the
+// lane then holds, for q = 0..3, row 4 lg + 2 b0 + b1 at columns
+// 16 (2 q + b2) + 8 b3 .. + 7, and stores each with one 16-byte store
+// (element by element where the piece is not whole, as for the staged
+// stores).  For callers whose LDS is taken.
+__device__ __forceinline__ uint32_t pack_bf2(uint32_t lo, uint32_t hi) {
+  return (lo & 0xffffu) | (hi << 16);
+}
+template <int MT>
+__device__ __forceinline__ void store_shuffled(const GemmArgs& g, int64_t row0,
+                                               const f32x4 (&acc)[MT][8]) {
+  typedef uint16_t T;
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const bool b0 = lr & 1, b1 = (lr >> 1) & 1, b2 = (lr >> 2) & 1, b3 = (lr >> 3) & 1;
+  const bool vec = (reinterpret_cast<uintptr_t>(g.out) & 15) == 0 && (g.ldo * 2) % 16 == 0 &&
+                   (g.split <= 0 || ((reinterpret_cast<uintptr_t>(g.out2) & 15) == 0 &&
+                                     (g.ldo2 * 2) % 16 == 0));
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    uint32_t z[8][2];  // row 4 lg + 2 b0 + b1, columns 16 t + 4 (lr / 4) .. + 3
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) {
+      uint32_t x[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x[r] = Mma<T>::from_f(acc[mt][nt][r]);
+      // lanes with b0 = 0 keep rows 0, 1 and those with b0 = 1 rows 2, 3,
+      // now for the column pair (lr & ~1, + 1)
+      const uint32_t r1 = (uint32_t)__builtin_amdgcn_mov_dpp(
+          (int)(b0 ? pack_bf2(x[0], x[1]) : pack_bf2(x[2], x[3])), 0xB1, 0xF, 0xF, true);
+      const uint32_t y0 = b0 ? pack_bf2(r1, x[2]) : pack_bf2(x[0], r1);
+      const uint32_t y1 = b0 ? pack_bf2(r1 >> 16, x[3]) : pack_bf2(x[1], r1 >> 16);
+      // lanes with b1 = 0 keep the first of the two rows, b1 = 1 the second,
+      // now for four columns from lr & ~3
+      const uint32_t r2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)(b1 ? y0 : y1), 0x4E, 0xF, 0xF, true);
+      z[nt][0] = b1 ? r2 : y0;
+      z[nt][1] = b1 ? y1 : r2;
+    }
+    const int64_t row = row0 + mt * 16 + 4 * lg + 2 * b0 + b1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      // lanes with b2 = 0 keep tile 2 q and those with b2 = 1 tile 2 q + 1,
+      // now for eight columns from 8 b3
+      const uint32_t s0 = b2 ? z[2 * q][0] : z[2 * q + 1][0];
+      const uint32_t s1 = b2 ? z[2 * q][1] : z[2 * q + 1][1];
+      const uint32_t r0 = (uint32_t)__builtin_amdgcn_ds_swizzle((int)s0, 0x101F);
+      const uint32_t r3 = (uint32_t)__builtin_amdgcn_ds_swizzle((int)s1, 0x101F);
+      const uint4 w = b2 ? uint4{r0, r3, z[2 * q + 1][0], z[2 * q + 1][1]}
+                         : uint4{z[2 * q][0], z[2 * q][1], r0, r3};
+      const int64_t c = 16 * (2 * q + (int)b2) + 8 * (int)b3;
+      if (row >= g.M) continue;
+      const bool whole = c + 8 <= g.N && (g.split <= 0 || c + 8 <= g.split || c >= g.split);
+      if (vec && whole) {
+        T* dst = g.split > 0 && c >= g.split
+                     ? static_cast<T*>(g.out2) + row * g.ldo2 + (c - g.split)
+                     : static_cast<T*>(g.out) + row * g.ldo + c;
+        *reinterpret_cast<uint4*>(dst) = w;
+      } else {
+        T e[8];
+        __builtin_memcpy(e, &w, 16);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (c + j < g.N) {
+            if (g.split > 0 && c + j >= g.split)
+              static_cast<T*>(g.out2)[row * g.ldo2 + (c + j - g.split)] = e[j];
+            else
+              static_cast<T*>(g.out)[row * g.ldo + c + j] = e[j];
+          }
+      }
+    }
+  }
+}
+
 // Through LDS: the wave writes its 16 MT rows x 16 NT columns (already in
 // the output type) to its own region, then each lane reads back whole
 // 16-byte pieces of rows, so one store instruction covers 1 KB of whole
@@ -682,6 +758,153 @@ __global__ __launch_bounds__(R::THREADS) void k_gemm(GemmArgs g) {
   const int64_t row0 = tile0 + wave * MT * 16;
   finish_tile(g, row0, n0, acc);
   store_tile<T, MT, NT, R>(g, row0, n0, acc, ring);
+}
+
+// bfloat16 PLAIN with the weights resident: one workgroup per CU holds
+// all of W^T for its 128 output columns in LDS (k in half chunks of 32,
+// column n = 16 t + r: piece p of 8 k at slot ((h * 8 + t) * 4 + p) * 16 + r,
+// so the 16 lanes that read one piece of 16 columns read 256 contiguous
+// bytes, free of bank conflicts), loaded once.  Each wave
+// then streams its own 16 MT-row tiles (tile q = wave id, wave id + all
+// waves, ...) through D register slots of A chunks; the stream runs on
+// across tiles, so the next tile's first chunks are in flight during the
+// last chunks and the epilogue of the current one.  No workgroup barrier
+// after the weights land, and only A loads on the vmcnt counter, so a wait
+// for one chunk never drains the chunks behind it.  The LDS being taken,
+// the epilogue stores through lane exchanges (store_shuffled).
+constexpr int kResHalfChunks = 19;  // half chunks of 32 k: K <= 608, 152 KB of LDS
+
+template <int MT, int NW, int D>
+__global__ __launch_bounds__(64 * NW) void k_gemm_bres(GemmArgs g) {
+  typedef uint16_t T;
+  typedef RegA<T, MT, 8, 2, NW> R;
+  typedef typename Mma<T>::Frag Frag;
+  constexpr int NT = 8, KC = Mma<T>::KC;
+  static_assert(D >= 2 && D <= 8, "A slots");
+  __shared__ uint4 wres[kResHalfChunks * 128 * 4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const T* A = static_cast<const T*>(g.a);
+  const T* Wt = static_cast<const T*>(g.wt);
+  const int hc = (int)((g.K + 31) / 32);  // half chunks held (<= kResHalfChunks, checked by the host)
+  // weights: slot s of half chunk h, column n, piece p
+  {
+    const int slots = hc * 128 * 4;
+    for (int s0 = wave * 64; s0 < slots; s0 += NW * 64) {
+      const int s = s0 + lane, h = s / 512, p = (s / 16) % 4;
+      // columns past N (not packed when N < 128) repeat column N - 1; their
+      // outputs are never stored
+      const int n = min((s / 64) % 8 * 16 + s % 16, (int)g.N - 1);
+      __builtin_amdgcn_global_load_lds(Wt + (int64_t)n * g.kp + h * 32 + p * 8, (lds_ptr)(wres + s0),
+                                       16, 0, 0);
+    }
+    wait_vm<0>();
+    ring_barrier();
+  }
+  const int nch = (int)((g.K + KC - 1) / KC);
+  const int64_t ntile = (g.M + 16 * MT - 1) / (16 * MT);
+  const int64_t gw = (int64_t)blockIdx.x * NW + wave, stride = (int64_t)gridDim.x * NW;
+  if (gw >= ntile) return;
+  const int64_t mytiles = (ntile - gw + stride - 1) / stride;
+  const int64_t total = mytiles * nch;  // chunks in this wave's stream
+  // the stream's read position (tile q_pf, chunk c_pf) and compute position
+  // (tile q_cur, chunk c_cur), advanced one chunk at a time
+  int64_t q_pf = gw, q_cur = gw;
+  int c_pf = 0, c_cur = 0;
+  int64_t off_pf[MT];
+  R::row_offsets(nullptr, g.lda, g.M, q_pf * 16 * MT, off_pf);
+  auto issue_next = [&](Frag (&a)[2][MT]) {
+    R::load_a(A, off_pf, g.K, (int64_t)c_pf * KC, a);
+    if (++c_pf == nch) {  // rows of tiles past the last are clamped to row M - 1
+      c_pf = 0;
+      q_pf += stride;
+      R::row_offsets(nullptr, g.lda, g.M, q_pf * 16 * MT, off_pf);
+    }
+  };
+  Frag a[D][2][MT];
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // chunk i of the stream from register slot U; FULL: the read of chunk
+  // i + D - 1 exists (the steady state: no conditional loads, so the
+  // compiler's waits count exactly the D - 1 chunks in flight)
+  auto step = [&](auto u_c, auto full_c, int64_t i) {
+    constexpr int U = decltype(u_c)::value;
+    constexpr bool FULL = decltype(full_c)::value;
+    if constexpr (FULL) {
+      issue_next(a[(U + D - 1) % D]);
+    } else {
+      if (i >= total) return;
+      if (i + D - 1 < total) issue_next(a[(U + D - 1) % D]);
+    }
+    const int c = c_cur;
+    if (c == nch - 1) R::mask(g.K, (int64_t)c * KC, a[U]);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int hh = 2 * c + h;
+      if (hh >= hc) break;  // past K: the A values there are zero, the weights not held
+      Frag b[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const uint4 v = wres[((hh * 8 + nt) * 4 + lg) * 16 + lr];
+        __builtin_memcpy(&b[nt], &v, 16);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // every fragment read ahead of the MFMAs
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[U][h][mt], b[nt], acc[mt][nt], 0, 0, 0);
+    }
+    if (++c_cur == nch) {
+      const int64_t row0 = q_cur * 16 * MT;
+      finish_tile(g, row0, 0, acc);
+      store_shuffled<MT>(g, row0, acc);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      c_cur = 0;
+      q_cur += stride;
+    }
+  };
+  using T1 = std::true_type;
+  using T0 = std::false_type;
+  int64_t i0 = 0;
+  if (total >= 2 * D - 1) {
+    // the first D - 1 chunks, unconditionally: the steady loop below is
+    // entered only from here, with exactly D - 1 chunks in flight
+#pragma unroll
+    for (int j = 0; j < D - 1; ++j) issue_next(a[j]);
+    // steady state: every step's read exists (i + D - 1 < total)
+    for (; i0 + 2 * D - 1 <= total; i0 += D) {
+      step(std::integral_constant<int, 0>{}, T1{}, i0);
+      step(std::integral_constant<int, 1>{}, T1{}, i0 + 1);
+      if constexpr (D > 2) step(std::integral_constant<int, 2>{}, T1{}, i0 + 2);
+      if constexpr (D > 3) step(std::integral_constant<int, 3>{}, T1{}, i0 + 3);
+      if constexpr (D > 4) step(std::integral_constant<int, 4>{}, T1{}, i0 + 4);
+      if constexpr (D > 5) step(std::integral_constant<int, 5>{}, T1{}, i0 + 5);
+      if constexpr (D > 6) step(std::integral_constant<int, 6>{}, T1{}, i0 + 6);
+      if constexpr (D > 7) step(std::integral_constant<int, 7>{}, T1{}, i0 + 7);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < D - 1; ++j)
+      if (j < total) issue_next(a[j]);
+  }
+  // the last chunks, fewer or no reads
+  for (; i0 < total; i0 += D) {
+    step(std::integral_constant<int, 0>{}, T0{}, i0);
+    step(std::integral_constant<int, 1>{}, T0{}, i0 + 1);
+    if constexpr (D > 2) step(std::integral_constant<int, 2>{}, T0{}, i0 + 2);
+    if constexpr (D > 3) step(std::integral_constant<int, 3>{}, T0{}, i0 + 3);
+    if constexpr (D > 4) step(std::integral_constant<int, 4>{}, T0{}, i0 + 4);
+    if constexpr (D > 5) step(std::integral_constant<int, 5>{}, T0{}, i0 + 5);
+    if constexpr (D > 6) step(std::integral_constant<int, 6>{}, T0{}, i0 + 6);
+    if constexpr (D > 7) step(std::integral_constant<int, 7>{}, T0{}, i0 + 7);
+  }
 }
 
 // GRU: acc1 = a w (input gates), acc2 = a2 w2 (hidden gates), column blocks
@@ -900,8 +1123,52 @@ hipError_t launch_nt(const GemmArgs& g, const Tiling& t, hipStream_t st) {
   return launch_plain<T, 2, NT, RegA<T, 2, NT, 4>>(g, st);
 }
 
+// weight-resident bfloat16 kernel: one workgroup per CU (its LDS holds the
+// weights), or fewer when there are fewer tiles than waves
+template <int MT, int NW, int D>
+hipError_t launch_bres(const GemmArgs& g, hipStream_t st) {
+  static int cus = [] {
+    int dev = 0, n = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+      (void)hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    return n > 0 ? n : 256;
+  }();
+  const int64_t tiles = (g.M + 16 * MT - 1) / (16 * MT);
+  const int64_t wgs = std::max<int64_t>(1, std::min<int64_t>(cus, (tiles + NW - 1) / NW));
+  hipLaunchKernelGGL((k_gemm_bres<MT, NW, D>), dim3((unsigned)wgs), dim3(64 * NW), 0, st, g);
+  return hipGetLastError();
+}
+
+// The weight-resident kernel takes bfloat16 PLAIN products with 80 < N <=
+// 128 (narrower outputs use the narrow tiles) and 192 <= K <= 608.  On
+// 2^21 rows x 128 columns against the streamed tiles: 0.32 / 0.35 ms at
+// K = 192 (one 16-row tile per wave), 0.37 / 0.42 ms at K = 256, 0.49 /
+// 0.55 at 384 and 0.69 / 0.80 at 602 (two tiles per wave); at K = 128 the
+// streamed tiles are as fast.  SAGA_GEMM_BRES overrides the shape for
+// tuning ("MxWxD": M x 16 rows per wave, W waves, D A chunks in
+// registers; "off": the streamed tiles).
+hipError_t maybe_bres(const GemmArgs& g, hipStream_t st, bool* used) {
+  *used = false;
+  if (g.dtype != SAGA_BF16 || g.mode != SAGA_GEMM_PLAIN || g.N > 128 || g.K > 32 * kResHalfChunks)
+    return hipSuccess;
+  static const char* e = getenv("SAGA_GEMM_BRES");
+  const char* cfg = e ? e : g.N <= 80 || g.K < 192 ? "off" : g.K < 256 ? "1x8x4" : "2x8x4";
+  *used = true;
+  if (!strcmp(cfg, "1x8x4")) return launch_bres<1, 8, 4>(g, st);
+  if (!strcmp(cfg, "2x8x4")) return launch_bres<2, 8, 4>(g, st);
+  if (!strcmp(cfg, "1x16x3")) return launch_bres<1, 16, 3>(g, st);
+  if (!strcmp(cfg, "1x8x6")) return launch_bres<1, 8, 6>(g, st);
+  *used = false;
+  return hipSuccess;
+}
+
 template <typename T>
 hipError_t dispatch(const GemmArgs& g, hipStream_t st) {
+  if constexpr (sizeof(T) == 2) {
+    bool used = false;
+    const hipError_t e = maybe_bres(g, st, &used);
+    if (used || e != hipSuccess) return e;
+  }
   const Tiling t = choose(g.dtype, g.mode, g.N, g.mode == SAGA_GEMM_CONCAT ? g.K + g.K2 : g.K);
   if (g.mode == SAGA_GEMM_GRU) {
     dim3 grid((unsigned)((g.M + 63) / 64));

@@ -6,7 +6,9 @@ source vertices than destinations), random plan options (segment lengths
 from 1, row costs, block costs down to the smallest allowed, which also
 makes the launcher hand several blocks to a workgroup), random widths
 (1 to 129 columns, fp32 and bf16) and every simple reduction.  The plan is
-compared with the oracle's bit for bit, the Gathers element by element."""
+compared with the oracle's bit for bit, the Gathers element by element.
+GEMM: random shapes over every tile path and epilogue, and a sweep over
+the shapes the bfloat16 weight-resident kernel takes."""
 import numpy as np
 import pytest
 import torch
@@ -125,6 +127,32 @@ def test_fuzz_gemm(case):
     ref = O.dense(AA, WW, bias=bias, act=act,
                   row_scale=None if deg is None else O.degree_scale(deg))
     assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
+
+
+RESIDENT_CASES = 24
+
+
+@pytest.mark.parametrize("case", range(RESIDENT_CASES))
+def test_fuzz_gemm_bf16_resident(case):
+    """bfloat16 PLAIN shapes the weight-resident kernel takes (80 < N <= 128,
+    192 <= K <= 608): random M from one row to several tiles per wave,
+    ragged K and N, random epilogue."""
+    from test_gpu_ops import run_gemm
+
+    rng = np.random.default_rng(9100 + case)
+    M = int(rng.choice([1, 15, 16, 17, int(rng.integers(18, 5000)), int(rng.integers(30000, 70000))]))
+    K = int(rng.integers(192, 609))
+    N = int(rng.integers(81, 129))
+    act = str(rng.choice(["none", "relu", "elu", "sigmoid", "tanh"]))
+    A = _bf16_round(rng.standard_normal((M, K)).astype(np.float32))
+    W = _bf16_round((rng.standard_normal((K, N)) / np.sqrt(K)).astype(np.float32))
+    bias = rng.standard_normal(N) if rng.random() < 0.5 else None
+    deg = rng.integers(0, 9, M) if rng.random() < 0.5 else None
+    print(f"fuzz gemm resident {case}: M={M} K={K} N={N} {act} bias={bias is not None} "
+          f"deg={deg is not None}", flush=True)
+    out = run_gemm(A, W, "bf16", bias=bias, act=act, deg=deg)
+    ref = O.dense(A, W, bias=bias, act=act, row_scale=None if deg is None else O.degree_scale(deg))
+    assert rel_err(to_np(out), ref) <= BF16_TOL
 
 
 def _small_graph(rng, vmax, dmax, long_row=0):

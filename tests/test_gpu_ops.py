@@ -345,6 +345,28 @@ def test_gemm_plain_many_tiles(dtype):
     assert rel_err(to_np(out), ref) <= (FP32_TOL if dtype == "f32" else BF16_TOL)
 
 
+@pytest.mark.parametrize("M,K,N,act", [(4099, 602, 128, "relu"), (1000, 608, 100, "elu"),
+                                       (3001, 300, 81, "none"), (2050, 256, 128, "tanh"),
+                                       (17, 512, 96, "sigmoid"), (100_003, 602, 128, "relu"),
+                                       (5000, 192, 128, "relu"), (33, 255, 90, "elu")])
+def test_gemm_bf16_resident_weights(M, K, N, act):
+    """bfloat16 products with 80 < N <= 128 and 192 <= K <= 608 (the
+    weights held in LDS for the whole run, rows streamed per wave, stores
+    through lane exchanges): ragged M, K and N, fewer rows than one wave's
+    tile, and more tiles than waves, with the full epilogue."""
+    rng = np.random.default_rng(M + K + N)
+    A = _bf16_round(rng.standard_normal((M, K)).astype(np.float32))
+    W = _bf16_round((rng.standard_normal((K, N)) / np.sqrt(K)).astype(np.float32))
+    bias = rng.standard_normal(N)
+    deg = rng.integers(0, 9, M)
+    print(f"gemm bf16 resident M={M} K={K} N={N} {act}", flush=True)
+    out = run_gemm(A, W, "bf16", bias=bias, act=act, deg=deg)
+    ref = O.dense(A, W, bias=bias, act=act, row_scale=O.degree_scale(deg))
+    assert rel_err(to_np(out), ref) <= BF16_TOL
+    out = run_gemm(A, W, "bf16")
+    assert rel_err(to_np(out), O.dense(A, W)) <= BF16_TOL
+
+
 def test_gemm_small_integers_exact():
     rng = np.random.default_rng(1)
     A = rng.integers(-8, 9, (333, 64)).astype(np.float32)
@@ -389,14 +411,16 @@ def test_gemm_gru(F):
     assert rel_err(to_np(out), ref) <= FP32_TOL
 
 
-@pytest.mark.parametrize("dtype,N,split", [("f32", 41, 32), ("f32", 100, 64), ("bf16", 100, 64)])
-def test_gemm_split_output_equals_single_output(dtype, N, split):
+@pytest.mark.parametrize("dtype,N,split,K", [("f32", 41, 32, 150), ("f32", 100, 64, 150),
+                                             ("bf16", 100, 64, 150), ("bf16", 128, 64, 602),
+                                             ("bf16", 100, 41, 300)])
+def test_gemm_split_output_equals_single_output(dtype, N, split, K):
     """split_col writes columns [0, s) to out and [s, N) to the tail matrix:
     the same values, bit for bit, as one output matrix (row scale, bias and
     activation included)."""
     S = lib()
     rng = np.random.default_rng(N)
-    M, K = 777, 150
+    M = 777
     A = rng.standard_normal((M, K)).astype(np.float32)
     W = rng.standard_normal((K, N)).astype(np.float32) / np.sqrt(K)
     b = rng.standard_normal(N).astype(np.float32)
