@@ -1143,8 +1143,9 @@ hipError_t launch_bres(const GemmArgs& g, hipStream_t st) {
 // 128 (narrower outputs use the narrow tiles) and 192 <= K <= 608.  On
 // 2^21 rows x 128 columns against the streamed tiles: 0.32 / 0.35 ms at
 // K = 192 (one 16-row tile per wave), 0.37 / 0.42 ms at K = 256, 0.49 /
-// 0.55 at 384 and 0.69 / 0.80 at 602 (two tiles per wave); at K = 128 the
-// streamed tiles are as fast.  SAGA_GEMM_BRES overrides the shape for
+// 0.55 at 384 and 0.69 / 0.80 at 602 (two tiles per wave, three A slots:
+// as fast as four, which spill registers); at K = 128 the streamed tiles
+// are as fast.  SAGA_GEMM_BRES overrides the shape for
 // tuning ("MxWxD": M x 16 rows per wave, W waves, D A chunks in
 // registers; "off": the streamed tiles).
 hipError_t maybe_bres(const GemmArgs& g, hipStream_t st, bool* used) {
@@ -1152,10 +1153,11 @@ hipError_t maybe_bres(const GemmArgs& g, hipStream_t st, bool* used) {
   if (g.dtype != SAGA_BF16 || g.mode != SAGA_GEMM_PLAIN || g.N > 128 || g.K > 32 * kResHalfChunks)
     return hipSuccess;
   static const char* e = getenv("SAGA_GEMM_BRES");
-  const char* cfg = e ? e : g.N <= 80 || g.K < 192 ? "off" : g.K < 256 ? "1x8x4" : "2x8x4";
+  const char* cfg = e ? e : g.N <= 80 || g.K < 192 ? "off" : g.K < 256 ? "1x8x4" : "2x8x3";
   *used = true;
   if (!strcmp(cfg, "1x8x4")) return launch_bres<1, 8, 4>(g, st);
   if (!strcmp(cfg, "2x8x4")) return launch_bres<2, 8, 4>(g, st);
+  if (!strcmp(cfg, "2x8x3")) return launch_bres<2, 8, 3>(g, st);
   if (!strcmp(cfg, "1x16x3")) return launch_bres<1, 16, 3>(g, st);
   if (!strcmp(cfg, "1x8x6")) return launch_bres<1, 8, 6>(g, st);
   *used = false;

@@ -39,7 +39,7 @@ STAGES = {
                          ("k_gather_simple<float, 4, 1, 4, 8, false, 0, false", 1)],
                  "bf16": [("k_gather_simple<unsigned short, 8, 1, 8, 4, false, 0, false", 1)]},
                 "gather.hip"),
-    "gemm1": ({"f32": [("k_gemm<float, 2, 8,", 1)], "bf16": [("k_gemm_bres<2, 8, 4>", 1)]},
+    "gemm1": ({"f32": [("k_gemm<float, 2, 8,", 1)], "bf16": [("k_gemm_bres<2, 8, 3>", 1)]},
               "gemm.hip"),
     "gemm2": ({"f32": [("k_gemm<float, 2, 3,", 1)], "bf16": [("k_gemm<unsigned short, 2, 3,", 1)]},
               "gemm.hip"),
