@@ -294,7 +294,7 @@ __global__ __launch_bounds__(kThreads) void k_outdeg_scatter(const int32_t* __re
   }
 #pragma unroll
   for (int j = 0; j < kEdgeItems; ++j) {
-    if (j * kThreads + threadIdx.x < n) {
+    if (j * kThreads + (int)threadIdx.x < n) {
       const int b = c[j] >> kBucketBits;
       const int32_t p = atomicAdd(&cur[b], 1);
       if (p >= 0 && p < n) {
