@@ -22,6 +22,21 @@ def S():
     return S
 
 
+def test_missing_library_raises_no_fallback(tmp_path):
+    """Without libsaga.so the binding raises at the first call: no op has a
+    CPU or PyTorch fallback."""
+    import paper_2009_00804_amd.saga as S
+
+    saved_path, saved_lib = S.LIB_PATH, S._lib
+    try:
+        S.LIB_PATH = str(tmp_path / "libsaga.so")
+        S._lib = None
+        with pytest.raises(RuntimeError, match="not built"):
+            S.lib()
+    finally:
+        S.LIB_PATH, S._lib = saved_path, saved_lib
+
+
 def _declared():
     src = open(os.path.join(ROOT, "include", "saga.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
