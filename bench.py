@@ -636,8 +636,8 @@ def main():
                          "(a known-size kernel for calibrating memory counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(sharding is a design note); use --gpus 1", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(how it would shard is documented, not built); use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
