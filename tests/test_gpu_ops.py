@@ -411,10 +411,11 @@ def test_gemm_gru(F):
     assert rel_err(to_np(out), ref) <= FP32_TOL
 
 
-@pytest.mark.parametrize("dtype,N,split,K", [("f32", 41, 32, 150), ("f32", 100, 64, 150),
-                                             ("bf16", 100, 64, 150), ("bf16", 128, 64, 602),
-                                             ("bf16", 100, 41, 300)])
-def test_gemm_split_output_equals_single_output(dtype, N, split, K):
+@pytest.mark.parametrize("dtype,N,split,K,aligned", [
+    ("f32", 41, 32, 150, False), ("f32", 100, 64, 150, False), ("bf16", 100, 64, 150, False),
+    ("bf16", 128, 64, 602, False), ("bf16", 100, 41, 300, False), ("bf16", 128, 64, 602, True),
+    ("bf16", 100, 41, 300, True), ("f32", 100, 64, 150, True)])
+def test_gemm_split_output_equals_single_output(dtype, N, split, K, aligned):
     """split_col writes columns [0, s) to out and [s, N) to the tail matrix:
     the same values, bit for bit, as one output matrix (row scale, bias and
     activation included)."""
@@ -432,12 +433,17 @@ def test_gemm_split_output_equals_single_output(dtype, N, split, K):
     op = S.saga_gemm_op(S.dtype_code(tdt), S.SAGA_GEMM_PLAIN, S.SAGA_ACT_ELU, deg.data_ptr())
     ws = S.workspace(S.saga_apply_vertex_workspace_size(op, K, 0, N), device())
     none = S.saga_cmat(None, 0, 0, 0)
-    print(f"gemm split {dtype} N={N} s={split}", flush=True)
+    print(f"gemm split {dtype} N={N} s={split} K={K} aligned={aligned}", flush=True)
     one = torch.full((M, N), 7.0, dtype=tdt, device=device())
     S.saga_apply_vertex(op, S.cmat(a), S.cmat(w), none, none, bias.data_ptr(), None, S.mat(one),
                         C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
-    head = torch.full((M, split), 7.0, dtype=tdt, device=device())
-    tail = torch.full((M, N - split + 3), 7.0, dtype=tdt, device=device())[:, :N - split]
+    # head and tail rows padded to 16 bytes (whole-piece stores) or the tail
+    # by 3 elements (element stores)
+    per16 = 16 // (4 if dtype == "f32" else 2)
+    ld_head = -(-split // per16) * per16 if aligned else split
+    ld_tail = -(-(N - split) // per16) * per16 if aligned else N - split + 3
+    head = torch.full((M, ld_head), 7.0, dtype=tdt, device=device())[:, :split]
+    tail = torch.full((M, ld_tail), 7.0, dtype=tdt, device=device())[:, :N - split]
     op.split_col = split
     op.tail = S.mat(tail)
     S.saga_apply_vertex(op, S.cmat(a), S.cmat(w), none, none, bias.data_ptr(), None, S.mat(head),
