@@ -39,23 +39,60 @@ __device__ __forceinline__ float load_elem(const void* p, int64_t i) {
     return bf16_to_f32(static_cast<const uint16_t*>(p)[i]);
 }
 
+// Activations other than ReLU / none, four columns per call: kept out of
+// line so the transcendental code does not set the register budget of the
+// gather loops that share an epilogue with it.
+__device__ __noinline__ f32x4 act_slow4(int act, f32x4 v) {
+  return f32x4{apply_act(act, v.x), apply_act(act, v.y), apply_act(act, v.z), apply_act(act, v.w)};
+}
+
+template <int N>
+__device__ __forceinline__ void apply_act_vec(int act, float (&x)[N]) {
+  if (act == SAGA_ACT_RELU) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] = x[i] > 0.0f ? x[i] : 0.0f;
+  } else if (act != SAGA_ACT_NONE) {
+#pragma unroll
+    for (int i = 0; i < N; i += 4) {
+      const f32x4 r = act_slow4(act, f32x4{x[i], x[i + 1], x[i + 2], x[i + 3]});
+      x[i] = r.x; x[i + 1] = r.y; x[i + 2] = r.z; x[i + 3] = r.w;
+    }
+  }
+}
+
+// out[row, col0 .. col0 + EPV) = act(x + self + bias), clipped to out_cols
 template <typename T>
 __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int col0,
                                           float (&x)[Vec16<T>::N]) {
   constexpr int EPV = Vec16<T>::N;
-#pragma unroll
-  for (int k = 0; k < EPV; ++k) {
-    const int c = col0 + k;
-    float v = x[k];
-    if (a.self && c < a.out_cols) v += load_elem<T>(a.self, row * a.ld_self + c);
-    if (a.bias && c < a.out_cols) v += a.bias[c];
-    x[k] = apply_act(a.act, v);
-  }
   T* o = static_cast<T*>(a.out) + row * a.ld_out + col0;
-  if (col0 + EPV <= a.out_cols)
+  if (col0 + EPV <= a.out_cols) {
+    // a whole 16-byte vector: self as one vector load (its rows are 16-byte
+    // aligned), bias as EPV scalars
+    if (a.self) {
+      float sv[EPV];
+      Vec16<T>::widen(*reinterpret_cast<const uint4*>(static_cast<const T*>(a.self) + row * a.ld_self + col0), sv);
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) x[k] += sv[k];
+    }
+    if (a.bias) {
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) x[k] += a.bias[col0 + k];
+    }
+    apply_act_vec(a.act, x);
     Vec16<T>::store(o, x);
-  else if (col0 < a.out_cols)
+  } else if (col0 < a.out_cols) {
+#pragma unroll
+    for (int k = 0; k < EPV; ++k) {
+      const int c = col0 + k;
+      float v = x[k];
+      if (a.self && c < a.out_cols) v += load_elem<T>(a.self, row * a.ld_self + c);
+      if (a.bias && c < a.out_cols) v += a.bias[c];
+      x[k] = v;
+    }
+    apply_act_vec(a.act, x);
     Vec16<T>::store_n(o, x, a.out_cols - col0);
+  }
 }
 
 // ------------------------------------------------------------------------
@@ -71,15 +108,15 @@ __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int 
 // non-temporal loads (they are streamed once) and broadcast by cross-lane
 // permute; U source-row loads are kept in flight per lane.
 // ------------------------------------------------------------------------
-// SLICED only distinguishes the sliced instance (rows wider than one slice)
-// in profiles.
+// FULL: every lane's 16-byte vector lies inside the row (the row's vectors
+// are a whole number of slices), so the per-vector range checks drop out.
 // IDENT: the source row of edge e is row e itself (the segment reduction of
 // an edge tensor already laid out in CSR order; the unfused path).
 // WM: message weight -- kWNone (1), kWSrcNorm (d_out(u)^-1/2, GCN) or
 // kWEdge (edge_scale[e], R-GCN's 1 / c(v, r); col_idx then holds the
 // edge's pair row).
 enum { kWNone = 0, kWSrcNorm = 1, kWEdge = 2 };
-template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, int WM, bool SLICED,
+template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, int WM, bool FULL,
           bool IDENT = false>
 __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int nslices, int slice0) {
   constexpr int EPV = Vec16<T>::N;
@@ -145,7 +182,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
 #pragma unroll
             for (int q = 0; q < VPL; ++q) {
               const int vi = v0 + gl + q * LPR;
-              if (vi < nv && t + k < nq) raw[k][q] = src[(int64_t)u * ld16 + vi];
+              if ((FULL || vi < nv) && t + k < nq) raw[k][q] = src[(int64_t)u * ld16 + vi];
             }
           }
 #pragma unroll
@@ -168,13 +205,16 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
     }
 
     if (s < s_split) {
+      // float32 partials; pstride and vi * EPV are multiples of 4 floats
       float* p = a.partial + (int64_t)s * a.pstride;
 #pragma unroll
       for (int q = 0; q < VPL; ++q) {
         const int vi = v0 + gl + q * LPR;
-        if (vi < nv)
+        if (FULL || vi < nv)
 #pragma unroll
-          for (int i = 0; i < EPV; ++i) p[vi * EPV + i] = acc[q][i];
+          for (int i = 0; i < EPV; i += 4)
+            *reinterpret_cast<f32x4*>(p + vi * EPV + i) =
+                f32x4{acc[q][i], acc[q][i + 1], acc[q][i + 2], acc[q][i + 3]};
       }
     } else {
       const int d = end - beg;  // a whole row
@@ -184,7 +224,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
 #pragma unroll
       for (int q = 0; q < VPL; ++q) {
         const int vi = v0 + gl + q * LPR;
-        if (vi < nv) {
+        if (FULL || vi < nv) {
           float x[EPV];
 #pragma unroll
           for (int i = 0; i < EPV; ++i) {
@@ -634,30 +674,37 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
   if (conc <= 0 || conc > nslices || nslices % conc != 0) conc = nslices;
   const dim3 grid(blocks * conc);
   const bool srcnorm = a.msg == SAGA_MSG_SRC_NORM;
+  const int nv = (int)((a.feat * (int64_t)sizeof(T) + 15) / 16);
+  const bool full = nv == nslices * LPR * VPL;
   for (int s0 = 0; s0 < nslices; s0 += conc) {
-#define SAGA_LAUNCH(MX, WM, SL)                                                              \
-  hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, WM, SL>), grid, dim3(kThreads), \
+#define SAGA_LAUNCH(MX, WM, FL)                                                              \
+  hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, WM, FL>), grid, dim3(kThreads), \
                      0, st, a, conc, s0)
+#define SAGA_LAUNCH_FULL(MX, WM)   \
+  do {                             \
+    if (full)                      \
+      SAGA_LAUNCH(MX, WM, true);   \
+    else                           \
+      SAGA_LAUNCH(MX, WM, false);  \
+  } while (0)
 #define SAGA_LAUNCH_IDENT(MX)                                                                  \
   hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, kWNone, false, true>), grid,    \
                      dim3(kThreads), 0, st, a, conc, s0)
-    const bool sl = nslices > 1;
     if (a.identity) {
       if (a.reduce == kMax) SAGA_LAUNCH_IDENT(true);
       else SAGA_LAUNCH_IDENT(false);
     } else if (a.msg == SAGA_MSG_TYPED) {
-      SAGA_LAUNCH(false, kWEdge, false);
+      SAGA_LAUNCH_FULL(false, kWEdge);
     } else if (a.reduce == kMax) {
-      if (srcnorm) SAGA_LAUNCH(true, kWSrcNorm, false);
-      else SAGA_LAUNCH(true, kWNone, false);
+      if (srcnorm) SAGA_LAUNCH_FULL(true, kWSrcNorm);
+      else SAGA_LAUNCH_FULL(true, kWNone);
     } else if (srcnorm) {
-      SAGA_LAUNCH(false, kWSrcNorm, false);
-    } else if (sl) {
-      SAGA_LAUNCH(false, kWNone, true);
+      SAGA_LAUNCH_FULL(false, kWSrcNorm);
     } else {
-      SAGA_LAUNCH(false, kWNone, false);
+      SAGA_LAUNCH_FULL(false, kWNone);
     }
 #undef SAGA_LAUNCH
+#undef SAGA_LAUNCH_FULL
 #undef SAGA_LAUNCH_IDENT
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
