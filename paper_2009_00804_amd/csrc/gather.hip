@@ -110,6 +110,9 @@ __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int 
 // ------------------------------------------------------------------------
 // FULL: every lane's 16-byte vector lies inside the row (the row's vectors
 // are a whole number of slices), so the per-vector range checks drop out.
+// O32: the source matrix spans less than 4 GiB, so a row vector's address is
+// the uniform base plus a 32-bit byte offset (one register per load in
+// flight instead of a 64-bit address pair).
 // IDENT: the source row of edge e is row e itself (the segment reduction of
 // an edge tensor already laid out in CSR order; the unfused path).
 // WM: message weight -- kWNone (1), kWSrcNorm (d_out(u)^-1/2, GCN) or
@@ -117,8 +120,8 @@ __device__ __forceinline__ void store_out(const GatherArgs& a, int64_t row, int 
 // edge's pair row).
 enum { kWNone = 0, kWSrcNorm = 1, kWEdge = 2 };
 template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, int WM, bool FULL,
-          bool IDENT = false>
-__global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int nslices, int slice0) {
+          bool IDENT, bool O32>
+__device__ __forceinline__ void gather_simple_body(const GatherArgs& a, int nslices, int slice0) {
   constexpr int EPV = Vec16<T>::N;
   constexpr int NG = kThreads / LPR;
   const int32_t* __restrict__ counts = a.counts;
@@ -138,6 +141,8 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
   // this lane's 16-byte vectors of every source row
   const uint4* __restrict__ src = reinterpret_cast<const uint4*>(static_cast<const T*>(a.src));
   const int64_t ld16 = a.ld_src * (int64_t)sizeof(T) / 16;
+  const char* __restrict__ srcb = static_cast<const char*>(a.src);
+  const uint32_t ldb = (uint32_t)(a.ld_src * (int64_t)sizeof(T));
   const int32_t* __restrict__ col = a.col_idx;
   const float init = MAXRED ? -INFINITY : 0.0f;
 
@@ -182,7 +187,13 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
 #pragma unroll
             for (int q = 0; q < VPL; ++q) {
               const int vi = v0 + gl + q * LPR;
-              if ((FULL || vi < nv) && t + k < nq) raw[k][q] = src[(int64_t)u * ld16 + vi];
+              if ((FULL || vi < nv) && t + k < nq) {
+                if constexpr (O32)
+                  raw[k][q] = *reinterpret_cast<const uint4*>(
+                      srcb + ((uint32_t)u * ldb + (uint32_t)vi * 16u));
+                else
+                  raw[k][q] = src[(int64_t)u * ld16 + vi];
+              }
             }
           }
 #pragma unroll
@@ -237,6 +248,21 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
       }
     }
   }
+}
+
+template <typename T, int LPR, int VPL, int U, int CPL, bool MAXRED, int WM, bool FULL,
+          bool IDENT = false>
+__global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int nslices, int slice0) {
+  gather_simple_body<T, LPR, VPL, U, CPL, MAXRED, WM, FULL, IDENT, false>(a, nslices, slice0);
+}
+
+// The plain sum over whole slices of a source below 4 GiB (the GCN Gather):
+// built for seven waves per SIMD, which its registers allow without spills
+// (bfloat16 rows otherwise take 74 registers, six waves).
+template <typename T, int LPR, int VPL, int U, int CPL>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(7))) void k_gather_sum(
+    GatherArgs a, int nslices, int slice0) {
+  gather_simple_body<T, LPR, VPL, U, CPL, false, kWNone, true, false, true>(a, nslices, slice0);
 }
 
 // ------------------------------------------------------------------------
@@ -646,16 +672,19 @@ inline int next_pow2(int x) {
 // 2^21-row source one 128-byte slice per launch (268 MB) measured fastest,
 // while a source of 131,072 rows has all eight 128-byte slices of its
 // 1 KB rows in one launch (134 MB), which also spares the launches their
-// ramp and tail.  SAGA_GATHER_CONCURRENT_SLICES overrides the choice
-// (0 = all in one launch).
+// ramp and tail.  A sweep build (SAGA_SWEEP_BUILD) reads an override from
+// SAGA_GATHER_CONCURRENT_SLICES (0 = all in one launch); the library itself
+// reads no environment.
 constexpr int64_t kSliceBudget = int64_t(192) << 20;
 
 int concurrent_slices(const GatherArgs& a, int nslices, int slice_bytes_) {
+#ifdef SAGA_SWEEP_BUILD
   static int env = [] {
     const char* e = getenv("SAGA_GATHER_CONCURRENT_SLICES");
     return e ? atoi(e) : -1;
   }();
   if (env >= 0) return env;
+#endif
   const int64_t per = std::max<int64_t>(1, a.src_rows) * slice_bytes_;
   int c = 1;
   for (int k = nslices; k >= 1; --k)
@@ -668,7 +697,7 @@ int concurrent_slices(const GatherArgs& a, int nslices, int slice_bytes_) {
 
 template <typename T, int LPR, int VPL>
 hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, hipStream_t st) {
-  constexpr int U = LPR >= 8 ? (VPL == 1 ? 8 : 4) : LPR;
+  constexpr int U = LPR >= 8 ? (VPL == 1 && sizeof(T) == 2 ? 8 : 4) : LPR;
   constexpr int CPL = LPR >= 32 ? 1 : (LPR >= 8 ? 4 : 8);
   int conc = concurrent_slices(a, nslices, LPR * VPL * 16);
   if (conc <= 0 || conc > nslices || nslices % conc != 0) conc = nslices;
@@ -676,6 +705,8 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
   const bool srcnorm = a.msg == SAGA_MSG_SRC_NORM;
   const int nv = (int)((a.feat * (int64_t)sizeof(T) + 15) / 16);
   const bool full = nv == nslices * LPR * VPL;
+  // every row a valid column index can name lies within 4 GiB of the base
+  const bool o32 = a.src_rows * a.ld_src * (int64_t)sizeof(T) <= (int64_t(1) << 32);
   for (int s0 = 0; s0 < nslices; s0 += conc) {
 #define SAGA_LAUNCH(MX, WM, FL)                                                              \
   hipLaunchKernelGGL((k_gather_simple<T, LPR, VPL, U, CPL, MX, WM, FL>), grid, dim3(kThreads), \
@@ -700,6 +731,12 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
       else SAGA_LAUNCH_FULL(true, kWNone);
     } else if (srcnorm) {
       SAGA_LAUNCH_FULL(false, kWSrcNorm);
+    } else if (LPR <= 8 && full && o32) {
+      // (whole slices of at most 128 bytes: wider lane groups never take
+      // this path with 128-byte slices, and are not built)
+      if constexpr (LPR <= 8)
+        hipLaunchKernelGGL((k_gather_sum<T, LPR, VPL, U, CPL>), grid, dim3(kThreads), 0, st, a,
+                           conc, s0);
     } else {
       SAGA_LAUNCH_FULL(false, kWNone);
     }
@@ -718,21 +755,24 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
 // slices in one launch) runs 23 % faster two blocks to a workgroup, the
 // gated layer 3 % faster; 2048- and 4096-cost blocks (R-GCN, the 2^21 GCN)
 // run fastest alone, and the GAT graph's 1185 blocks would leave CUs idle.
-// SAGA_GATHER_BLOCKS_PER_WG overrides the choice.
+// A sweep build reads an override from SAGA_GATHER_BLOCKS_PER_WG.
 int blocks_per_wg(const GatherArgs& a) {
+#ifdef SAGA_SWEEP_BUILD
   static int env = [] {
     const char* e = getenv("SAGA_GATHER_BLOCKS_PER_WG");
     int x = e ? atoi(e) : 0;
     return x >= 1 && x <= 64 ? x : 0;
   }();
   if (env) return env;
+#endif
   int k = 1;
   while (2 * k * (int64_t)a.block_cost <= 2048 && a.max_blocks / (2 * k) >= 1024) k *= 2;
   return k;
 }
 
-// bytes of each source row one slice covers (128 = one cache line); the
-// SAGA_GATHER_SLICE_BYTES environment variable overrides it for tuning
+// bytes of each source row one slice covers: 128, one L2 line (a sweep
+// build reads other widths from SAGA_GATHER_SLICE_BYTES)
+#ifdef SAGA_SWEEP_BUILD
 int slice_bytes() {
   static int v = [] {
     const char* e = getenv("SAGA_GATHER_SLICE_BYTES");
@@ -741,12 +781,18 @@ int slice_bytes() {
   }();
   return v;
 }
+#else
+constexpr int slice_bytes() { return 128; }
+#endif
 
 template <typename T>
 hipError_t launch_simple(const GatherArgs& a, int nv, unsigned blocks, hipStream_t st) {
   const int sv = slice_bytes() / 16;
   if (sv >= 1 && nv > sv && nv % sv == 0 && (sv & (sv - 1)) == 0 && sv <= 64) {
     const int ns = nv / sv;
+#ifndef SAGA_SWEEP_BUILD
+    return launch_simple_lpr<T, 8, 1>(a, blocks, ns, st);
+#else
     switch (sv) {
       case 1: return launch_simple_lpr<T, 1, 1>(a, blocks, ns, st);
       case 2: return launch_simple_lpr<T, 2, 1>(a, blocks, ns, st);
@@ -756,6 +802,7 @@ hipError_t launch_simple(const GatherArgs& a, int nv, unsigned blocks, hipStream
       case 32: return launch_simple_lpr<T, 32, 1>(a, blocks, ns, st);
       default: return launch_simple_lpr<T, 64, 1>(a, blocks, ns, st);
     }
+#endif
   }
   if (nv > 64) return launch_simple_lpr<T, 64, 2>(a, blocks, 1, st);
   switch (next_pow2(nv)) {

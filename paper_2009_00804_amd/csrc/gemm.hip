@@ -1030,7 +1030,8 @@ struct Tiling {
   int nw = 4;   // waves per workgroup (RegA)
 };
 
-// SAGA_GEMM_CFG overrides the tile shape of the N <= 128 kernels for tuning:
+#ifdef SAGA_SWEEP_BUILD
+// A sweep build reads SAGA_GEMM_CFG to override the tile shape of the N <= 128 kernels for tuning:
 // "aMxS" = A through registers, M = rows per wave / 16, S stages;
 // "rMxS" = A through the LDS ring
 Tiling cfg_override(Tiling t) {
@@ -1047,6 +1048,9 @@ Tiling cfg_override(Tiling t) {
     if (!strcmp(e, x.name)) return x.t;
   return t;
 }
+#else
+Tiling cfg_override(Tiling t) { return t; }
+#endif
 
 // k chunks of a K-long operand
 int64_t chunks(int dtype, int64_t K) {
@@ -1145,13 +1149,14 @@ hipError_t launch_bres(const GemmArgs& g, hipStream_t st) {
 // K = 192 (one 16-row tile per wave), 0.37 / 0.42 ms at K = 256, 0.49 /
 // 0.55 at 384 and 0.69 / 0.80 at 602 (two tiles per wave, three A slots:
 // as fast as four, which spill registers); at K = 128 the streamed tiles
-// are as fast.  SAGA_GEMM_BRES overrides the shape for
-// tuning ("MxWxD": M x 16 rows per wave, W waves, D A chunks in
-// registers; "off": the streamed tiles).
+// are as fast.  A sweep build reads SAGA_GEMM_BRES to override the shape
+// ("MxWxD": M x 16 rows per wave, W waves, D A chunks in registers; "off":
+// the streamed tiles).
 hipError_t maybe_bres(const GemmArgs& g, hipStream_t st, bool* used) {
   *used = false;
   if (g.dtype != SAGA_BF16 || g.mode != SAGA_GEMM_PLAIN || g.N > 128 || g.K > 32 * kResHalfChunks)
     return hipSuccess;
+#ifdef SAGA_SWEEP_BUILD
   static const char* e = getenv("SAGA_GEMM_BRES");
   const char* cfg = e ? e : g.N <= 80 || g.K < 192 ? "off" : g.K < 256 ? "1x8x4" : "2x8x3";
   *used = true;
@@ -1162,6 +1167,11 @@ hipError_t maybe_bres(const GemmArgs& g, hipStream_t st, bool* used) {
   if (!strcmp(cfg, "1x8x6")) return launch_bres<1, 8, 6>(g, st);
   *used = false;
   return hipSuccess;
+#else
+  if (g.N <= 80 || g.K < 192) return hipSuccess;
+  *used = true;
+  return g.K < 256 ? launch_bres<1, 8, 4>(g, st) : launch_bres<2, 8, 3>(g, st);
+#endif
 }
 
 template <typename T>
