@@ -6,7 +6,6 @@ cases that reduce to textbook operations.  CPU only."""
 import json
 import math
 import os
-from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -66,6 +65,50 @@ def test_gat_hand_worked():
     want = np.array([[0.75 * ln3, 5.0], [-2.0, 1.0],
                      [w0 * -2.0 + w1 * ln3, w0 * 1.0 + w1 * 4.0], [0.0, 0.0]])
     np.testing.assert_allclose(out, want, rtol=1e-14, atol=1e-15)
+
+
+def test_gat_head_mean_hand_worked():
+    """Two heads averaged (the second GAT layer's merge), worked by hand in
+    tests/golden/gat_mean_hand.json."""
+    g = _load("gat_mean_hand.json")
+    src = [e[0] for e in g["edges_src_to_dst"]]
+    dst = [e[1] for e in g["edges_src_to_dst"]]
+    rp, col, _ = _graph(g["n"], src, dst)
+    ln3 = math.log(3.0)
+    H = np.array([[ln3 if x == "ln3" else float(x) for x in row] for row in g["H"]])
+    out = O.gat_layer(rp, col, H, np.eye(4), np.array(g["a_l"], dtype=np.float64),
+                      np.array(g["a_r"], dtype=np.float64), np.array(g["b"], dtype=np.float64),
+                      g["heads"], "mean", "none", g["neg_slope"])
+    e = math.e
+    w1, w2 = 1.0 / (1.0 + e), e / (1.0 + e)
+    want = np.array([[(0.75 * ln3 + 6 * w1 + 10 * w2) / 2 + 0.5, (2.5 - 5 * w1) / 2 - 1.0],
+                     [3.5, 4.0], [0.5, -1.0]])
+    np.testing.assert_allclose(out, want, rtol=1e-14, atol=1e-15)
+
+
+def test_gru_cell_equals_torch_grucell():
+    """The GRU ApplyVertex (Fig. 2, GGNN) against torch.nn.GRUCell in float64
+    with non-zero input and hidden weights and biases: gate order (r, z, n),
+    the reset gate applied to h W_hn + b_hn, h' = (1 - z) n + z h."""
+    import torch
+
+    rng = np.random.default_rng(21)
+    F, M = 5, 9
+    a = rng.standard_normal((M, F))
+    h = rng.standard_normal((M, F))
+    W_ih = rng.standard_normal((F, 3 * F))
+    W_hh = rng.standard_normal((F, 3 * F))
+    b_ih = rng.standard_normal(3 * F)
+    b_hh = rng.standard_normal(3 * F)
+    cell = torch.nn.GRUCell(F, F, bias=True, dtype=torch.float64)
+    with torch.no_grad():
+        cell.weight_ih.copy_(torch.from_numpy(W_ih.T.copy()))
+        cell.weight_hh.copy_(torch.from_numpy(W_hh.T.copy()))
+        cell.bias_ih.copy_(torch.from_numpy(b_ih))
+        cell.bias_hh.copy_(torch.from_numpy(b_hh))
+        want = cell(torch.from_numpy(a), torch.from_numpy(h)).numpy()
+    got = O.gru_cell(a, h, W_ih, b_ih, W_hh, b_hh)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
 
 
 # --------------------------------------------------------------------------
@@ -445,6 +488,8 @@ def _pins_pass():
             test_gather_max_equals_masked_max(case)
         test_closed_forms_of_sum_mean_and_gcn()
         test_gru_closed_forms()
+        test_gat_head_mean_hand_worked()
+        test_gru_cell_equals_torch_grucell()
     except AssertionError:
         return False
     return True
@@ -454,17 +499,54 @@ def test_pins_pass_unmutated():
     assert _pins_pass()
 
 
+def _gat_mean_over_dims(orig):
+    """GAT head merge averaging each head's dims instead of the heads (same
+    output shape when heads == head dims)."""
+    def f(row_ptr, col_idx, H, W, a_l, a_r, b, heads, merge, act, neg_slope=0.2, rows=None):
+        if merge != "mean":
+            return orig(row_ptr, col_idx, H, W, a_l, a_r, b, heads, merge, act, neg_slope, rows)
+        F = W.shape[1]
+        o = orig(row_ptr, col_idx, H, W, a_l, a_r, np.zeros(F), heads, "concat", "none",
+                 neg_slope, rows)
+        return O.ACTS[act](o.reshape(-1, heads, F // heads).mean(axis=2)
+                           + np.asarray(b, dtype=np.float64)[None, :])
+    return f
+
+
+def _gru_mutant(kind):
+    """GRU cells with a misplaced reset gate or hidden bias."""
+    def f(a, h, W_ih, b_ih, W_hh, b_hh):
+        F = h.shape[1]
+        gi = a @ W_ih + b_ih[None, :]
+        gh_w = h @ W_hh
+        gh = gh_w + b_hh[None, :]
+        r = 1.0 / (1.0 + np.exp(-(gi[:, :F] + gh[:, :F])))
+        z = 1.0 / (1.0 + np.exp(-(gi[:, F:2 * F] + gh[:, F:2 * F])))
+        if kind == "reset_on_input":      # r gates the input side instead
+            n = np.tanh(r * gi[:, 2 * F:] + gh[:, 2 * F:])
+        else:                             # b_hn added outside the reset gate
+            n = np.tanh(gi[:, 2 * F:] + r * gh_w[:, 2 * F:] + b_hh[None, 2 * F:])
+        return (1.0 - z) * n + z * h
+    return f
+
+
 MUTANTS = {
+    # GAT layer 2 averaging over each head's dims instead of over the heads
+    "gat_mean_over_dims": lambda O_: setattr(O_, "gat_layer", _gat_mean_over_dims(O_.gat_layer)),
+    # GRU reset gate applied to the input side
+    "gru_reset_on_input": lambda O_: setattr(O_, "gru_cell", _gru_mutant("reset_on_input")),
+    # GRU hidden bias b_hn outside the reset gate
+    "gru_bhn_outside_reset": lambda O_: setattr(O_, "gru_cell", _gru_mutant("bhn_outside")),
     # dropped destination scaling in GCN
     "gcn_no_din": lambda O_: setattr(O_, "in_degrees", lambda rp: np.ones(len(rp) - 1, np.int64)),
     # wrong sign in LeakyReLU
     "leaky_sign": lambda O_: setattr(O_, "leaky_relu", lambda x, s: np.where(x > 0, x, -s * x)),
-    # softmax without max subtraction is still exact; use a wrong normaliser
+    # wrong sign inside the sigmoid (the gated edge MPNN's gate)
     "sigmoid_sign": lambda O_: setattr(O_, "sigmoid", lambda x: 1.0 / (1.0 + np.exp(x))),
     # transposed operand in the dense transform
     "dense_transpose": lambda O_: setattr(
         O_, "dense", (lambda orig: (lambda A, W, **k: orig(A, W.T if W.shape[0] == W.shape[1] else W, **k)))(O_.dense)),
-    # reductions: max replaced by sum
+    # degree scaling d^-1 instead of d^-1/2 (GCN normalisation)
     "degree_scale_sq": lambda O_: setattr(O_, "degree_scale", lambda d: np.where(np.asarray(d) > 0, 1.0 / np.maximum(np.asarray(d, float), 1), 0.0)),
 }
 
@@ -473,7 +555,8 @@ MUTANTS = {
 def test_planted_mistake_is_caught(mutant, monkeypatch):
     import oracle.saga_oracle as mod
 
-    saved = {k: getattr(mod, k) for k in ("in_degrees", "leaky_relu", "sigmoid", "dense", "degree_scale")}
+    saved = {k: getattr(mod, k) for k in ("in_degrees", "leaky_relu", "sigmoid", "dense", "degree_scale",
+                                           "gat_layer", "gru_cell")}
     try:
         MUTANTS[mutant](mod)
         assert not _pins_pass(), f"mutant {mutant} survived the pins"
@@ -488,5 +571,3 @@ def test_rel_err_metric():
     rms = math.sqrt((1 + 4 + 1e-18) / 4)
     # element 0: |r| = 1 < rms, so the floor applies; element 1 is exact
     assert abs(rel_err(y, r) - max(1e-5 / rms, 1e-6 / rms)) < 1e-15
-    # an exact rational check of the floor rule
-    assert Fraction(1, 2) / Fraction(2) == Fraction(1, 4)
