@@ -390,6 +390,23 @@ saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edg
                                            void* workspace, size_t workspace_bytes,
                                            void* stream);
 
+/* The same Gather for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): no workspace argument.  The split-row partials go to a fixed
+ * 64 MiB device array inside the library; each GPU the library runs on
+ * holds its own copy from the first call on that GPU until the process
+ * ends.  The call allocates nothing and reads the device of `stream` (the
+ * current device for the null stream).  Same arguments, validation,
+ * results (bit for bit) and errors as saga_scatter_apply_edge_gather, plus
+ * SAGA_EUNSUPPORTED when the partials could exceed 64 MiB (bound:
+ * saga_gather_workspace_size's value for this plan and op).  The array is
+ * shared by every call on one GPU and keeps the last call's contents (no
+ * call reads what an earlier call left): calls that overlap on one GPU
+ * (different streams without ordering) race and must not be issued. */
+saga_status saga_scatter_apply_edge_gather_noalloc(const saga_plan* plan, const saga_edge_op* op,
+                                                   const saga_edge_inputs* in, saga_mat out,
+                                                   void* stream);
+
 /* ----------------------------------------------------------------------
  * Unfused baseline (Sec. 3.2 "Gather", Fig. 7a): the same operation as
  * saga_scatter_apply_edge_gather, computed the way a framework without a

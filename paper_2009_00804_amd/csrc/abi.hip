@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <exception>
+#include <mutex>
 
 #include "saga.h"
 #include "saga_internal.h"
@@ -963,6 +964,44 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
   return fail(SAGA_EINVAL, "bad layer kind");
 }
 
+// ---------------------------------------------------------------------------
+// Fixed device scratch of saga_scatter_apply_edge_gather_noalloc: the
+// split-row partials live here instead of in a caller workspace.  Each GPU
+// the library runs on holds its own copy until the process ends.  In host
+// code the name `scratch` is a host-side stand-in, not a device address:
+// kernels get the address noalloc_scratch() looked up for their device.
+// ---------------------------------------------------------------------------
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of `scratch` on device `dev`, looked up on first use with
+// that device current and kept for the process.
+hipError_t noalloc_scratch(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1133,6 +1172,35 @@ saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edg
     if (!op || !in) return fail(SAGA_EINVAL, "null argument");
     return run_gather(*plan, *op, *in, out, workspace, workspace_bytes,
                       static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_scatter_apply_edge_gather_noalloc(const saga_plan* plan, const saga_edge_op* op,
+                                                   const saga_edge_inputs* in, saga_mat out,
+                                                   void* stream) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!op || !in) return fail(SAGA_EINVAL, "null argument");
+    s = validate_edge_op(*plan, *op, *in, out);
+    if (s) return s;
+    size_t need = 0;
+    gather_ws_bytes(*plan, *op, in->src.cols, &need);
+    if (plan->max_split_segments > 0 && need > kNoAllocScratchBytes)
+      return fail(SAGA_EUNSUPPORTED,
+                  "noalloc gather: the split-row partials may need %zu bytes, the fixed scratch "
+                  "holds %zu; use saga_scatter_apply_edge_gather with a workspace",
+                  need, kNoAllocScratchBytes);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    int dev = -1;
+    hipError_t e = st ? hipStreamGetDevice(st, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return dev_fail(e, "noalloc gather: device of the stream");
+    void* ws = nullptr;
+    e = noalloc_scratch(dev, &ws);
+    if (e != hipSuccess) return dev_fail(e, "noalloc gather: scratch address");
+    return run_gather(*plan, *op, *in, out, ws, kNoAllocScratchBytes, st);
   } catch (...) {
     return fail(SAGA_EINTERNAL, "exception");
   }

@@ -36,6 +36,7 @@ ACT = {"none": 0, "relu": 1, "elu": 2, "sigmoid": 3, "tanh": 4}
 EXPORTS = [
     "saga_plan_workspace_size", "saga_plan_build", "saga_plan_build_split", "saga_plan_check",
     "saga_gather_workspace_size", "saga_scatter_apply_edge_gather",
+    "saga_scatter_apply_edge_gather_noalloc",
     "saga_unfused_workspace_size", "saga_scatter_gather_unfused",
     "saga_lstm_gather_workspace_size", "saga_lstm_gather", "saga_lstm_gather_rows",
     "saga_rel_plan_workspace_size", "saga_rel_plan_build", "saga_rel_plan_check",
@@ -145,6 +146,8 @@ def lib():
         "saga_gather_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64, P(C.c_size_t)]),
         "saga_scatter_apply_edge_gather": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs), saga_mat,
                                                C.c_void_p, C.c_size_t, C.c_void_p]),
+        "saga_scatter_apply_edge_gather_noalloc": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs),
+                                                       saga_mat, C.c_void_p]),
         "saga_unfused_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64, P(C.c_size_t)]),
         "saga_scatter_gather_unfused": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs), saga_mat,
                                             C.c_void_p, C.c_size_t, C.c_void_p]),
@@ -240,6 +243,12 @@ def saga_scatter_apply_edge_gather(plan, op, inputs, out, workspace, ws_bytes, s
     return _check(lib().saga_scatter_apply_edge_gather(C.byref(plan), C.byref(op), C.byref(inputs), out,
                                                        workspace, ws_bytes, stream),
                   "saga_scatter_apply_edge_gather")
+
+
+def saga_scatter_apply_edge_gather_noalloc(plan, op, inputs, out, stream):
+    return _check(lib().saga_scatter_apply_edge_gather_noalloc(C.byref(plan), C.byref(op), C.byref(inputs),
+                                                               out, stream),
+                  "saga_scatter_apply_edge_gather_noalloc")
 
 
 def saga_unfused_workspace_size(plan, op, feat):
