@@ -19,6 +19,23 @@ def rel_err(y, r):
     return float(np.max(np.abs(y - r) / den))
 
 
+def rel_err_terms(y, r, mag):
+    """max_i |y_i - r_i| / max(|r_i|, mag_i), where mag_i is the magnitude of
+    the terms summed into r_i (the same computation on absolute values).  A
+    floating-point sum of n terms errs by about n * eps * mag_i at most, so
+    this bounds every element by its own conditioning rather than by the
+    rms of the whole tensor (rel_err's floor)."""
+    y = np.asarray(y, dtype=np.float64)
+    r = np.asarray(r, dtype=np.float64)
+    mag = np.asarray(mag, dtype=np.float64)
+    assert y.shape == r.shape == mag.shape, (y.shape, r.shape, mag.shape)
+    if r.size == 0:
+        return 0.0
+    den = np.maximum(np.abs(r), mag)
+    den = np.where(den > 0, den, 1.0)
+    return float(np.max(np.abs(y - r) / den))
+
+
 def edges_to_csr(n, src, dst):
     """Destination-major CSR via plain Python (rows by dst, then src, then
     edge order) -- independent of synth.graphs.to_in_csr."""

@@ -9,7 +9,7 @@ import pytest
 import torch
 
 from gpu_util import dev_padded, device, graph, lib, to_np
-from helpers import BF16_TOL, FP32_TOL, edges_to_csr, rel_err, tiny_graphs
+from helpers import BF16_TOL, FP32_TOL, edges_to_csr, rel_err, rel_err_terms, tiny_graphs
 from oracle import saga_oracle as O
 
 pytestmark = pytest.mark.gpu
@@ -110,8 +110,13 @@ def test_gather_sum_mean(gname, F, dtype):
                                      msg={"copy": S.SAGA_MSG_COPY, "src_norm": S.SAGA_MSG_SRC_NORM}[msg],
                                      dst_norm=dn, act=act), F, tdt, bias=b)
         ref = _ref_simple(rp, col, X, red, msg, dn, b, act, n)
-        err = rel_err(to_np(out), ref)
+        got = to_np(out)
+        err = rel_err(got, ref)
         assert err <= tol, (red, msg, err)
+        # element by element, against the magnitude of each output's own terms
+        mag = _ref_simple(rp, col, np.abs(X), red, msg, dn, None if b is None else np.abs(b), "none", n)
+        err_t = rel_err_terms(got, ref, mag)
+        assert err_t <= tol, (red, msg, err_t)
 
 
 @pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_star"])

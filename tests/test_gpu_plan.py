@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 from gpu_util import graph, lib
-from helpers import edges_to_csr, tiny_graphs
+from helpers import FP32_TOL, edges_to_csr, rel_err, tiny_graphs
 from oracle import saga_oracle as O
 
 pytestmark = pytest.mark.gpu
@@ -83,9 +83,10 @@ def test_plan_rejects_invalid_csr():
 
 def test_split_plan_equals_single_stream_plan_and_overlaps_the_transform():
     """saga_plan_build_split (out-degree branch on the stream, row order on a
-    second stream) gives the arrays of saga_plan_build bit for bit, and a
-    2-layer GCN whose transform is enqueued between the branches gives the
-    same output as the sequential order."""
+    second stream) gives the oracle's plan bit for bit (and so the arrays of
+    saga_plan_build), and the GCN layer whose transform is enqueued between
+    the branches matches the oracle's layer (and the sequential order's
+    bytes)."""
     import ctypes as C
 
     import torch
@@ -101,6 +102,8 @@ def test_split_plan_equals_single_stream_plan_and_overlaps_the_transform():
     rp, col = dev_int(g["row_ptr"]), dev_int(g["col_idx"])
     ref = S.Graph(rp, col)
     want = {k: v.cpu().numpy() for k, v in ref.arrays().items()}
+    p0 = ref.plan
+    oracle = O.plan(g["row_ptr"], g["col_idx"], V, p0.seg_len, p0.block_cost, p0.row_cost)
     main = torch.cuda.current_stream()
     side = torch.cuda.Stream()
     fork, join = torch.cuda.Event(), torch.cuda.Event()
@@ -120,7 +123,9 @@ def test_split_plan_equals_single_stream_plan_and_overlaps_the_transform():
         gr.plan, gr.ws, gr.counts = plan, ws, counts
         got = {k: v.cpu().numpy() for k, v in gr.arrays().items()}
         for k in want:
+            assert np.array_equal(got[k].astype(np.int64), oracle[k].astype(np.int64)), k
             assert np.array_equal(got[k], want[k]), k
+        assert counts.n_split == oracle["n_split"]
     # layer 1 of the GCN with its transform enqueued between the branches
     X = torch.from_numpy(np.ascontiguousarray(g["X"][:, :g["dims"][0]])).to(device())
     X = torch.nn.functional.pad(X, (0, (-X.shape[1]) % 4))[:, :g["dims"][0]]
@@ -154,7 +159,10 @@ def test_split_plan_equals_single_stream_plan_and_overlaps_the_transform():
                                     ref.opts, C.c_void_p(ws2.data_ptr()), ws2.numel(),
                                     S.stream_handle(main), S.stream_handle(side),
                                     C.c_void_p(fork.cuda_event), C.c_void_p(join.cuda_event))
-    assert np.array_equal(layer1(plan2, wait=join), seq)
+    piped = layer1(plan2, wait=join)
+    ref1 = O.gcn_layer(g["row_ptr"], g["col_idx"], g["X"][:, :g["dims"][0]], g["W1"], g["b1"], "relu")
+    assert rel_err(piped, ref1) <= FP32_TOL
+    assert np.array_equal(piped, seq)
     with pytest.raises(S.SagaError):
         S.saga_plan_build_split(V, V, E, C.c_void_p(rp.data_ptr()), C.c_void_p(col.data_ptr()),
                                 ref.opts, C.c_void_p(ws.data_ptr()), ws.numel(),
