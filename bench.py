@@ -357,11 +357,127 @@ def _oracle_model(name, g, rows=None):
     return O.gated_layer_of(g)
 
 
-def suite(dev, reps=10, oracle=True):
+def _gemm_work(M, K, N, es=4):
+    """(compulsory bytes, flops) of an M x K by K x N product: A, W and the
+    output once; 2 M K N."""
+    return (M * K + K * N + M * N) * es, 2 * M * K * N
+
+
+def _gather_work(V, E, F_src, F_out, src_rows=None, per_edge_bytes=0, per_row_bytes=0,
+                 flops_per_edge=None):
+    """(compulsory bytes, flops) of a Gather: 4 B per CSR index, row_ptr, each
+    source row once, the output once, plus the kernel's other inputs."""
+    src_rows = V if src_rows is None else src_rows
+    byts = (E * 4 + (V + 1) * 4 + src_rows * F_src * 4 + V * F_out * 4 + E * per_edge_bytes
+            + V * per_row_bytes)
+    return byts, E * (F_src if flops_per_edge is None else flops_per_edge)
+
+
+def suite_stages(name, g, rel_counts=None):
+    """The stages saga_layer runs for each layer of a workload (the order
+    saga_trace_stages reports them in), with the algorithmic work of each:
+    [[(stage, kind, bytes, flops), ...] per layer]; kind "mfma" for the
+    dense transforms (priced against the float32 MFMA peak), "hbm" for the
+    Gathers."""
+    V, E = g["num_vertices"], g["num_edges"]
+    G = lambda st, w: (st, "mfma", *w)  # noqa: E731
+    A = lambda st, w: (st, "hbm", *w)   # noqa: E731
+    if name == "gcn_er":
+        f_in, hid, f_out = g["dims"]
+        return [[G("transform", _gemm_work(V, f_in, hid)), A("gather", _gather_work(V, E, hid, hid))],
+                [G("transform", _gemm_work(V, hid, f_out)), A("gather", _gather_work(V, E, f_out, f_out))]]
+    if name == "gat_ba":
+        K = g["heads"]
+        f_in, F1 = g["W1"].shape
+        F2 = g["W2"].shape[1]
+        return [[G("transform", _gemm_work(V, f_in, F1 + 2 * K)),
+                 A("gather", _gather_work(V, E, F1, F1, per_row_bytes=2 * K * 4,
+                                          flops_per_edge=2 * F1 + 8 * K))],
+                [G("transform", _gemm_work(V, F1, F2 + 2 * K)),
+                 A("gather", _gather_work(V, E, F2, F2 // K, per_row_bytes=2 * K * 4,
+                                          flops_per_edge=2 * F2 + 8 * K))]]
+    if name == "sage_rmat":
+        F, Fo = g["W_pool"].shape[0], g["W"].shape[1]
+        return [[G("pool transform", _gemm_work(V, F, F)), A("max gather", _gather_work(V, E, F, F)),
+                 G("concat transform", _gemm_work(V, 2 * F, Fo))]]
+    if name == "gated_rgg":
+        F, Fe = g["H"].shape[1], g["E_feat"].shape[1]
+        gru_b = (2 * V * F + 2 * F * 3 * F + V * F) * 4
+        return [[G("source-gate transform", _gemm_work(V, F, F)),
+                 G("destination-gate transform", _gemm_work(V, F, F)),
+                 A("gated gather", _gather_work(V, E, F, F, per_edge_bytes=Fe * 4,
+                                                per_row_bytes=2 * F * 4,
+                                                flops_per_edge=2 * Fe * F + 8 * F)),
+                 G("GRU transform", (gru_b, 2 * 2 * V * F * 3 * F))]]
+    if name == "sage_lstm":
+        F, G4 = g["W_ih"].shape
+        H, Fo = G4 // 4, g["W"].shape[1]
+        return [[G("input transform", _gemm_work(V, F, G4)),
+                 A("LSTM gather", _gather_work(V, E, G4, H, flops_per_edge=2 * H * G4 + 10 * H)),
+                 G("concat transform", _gemm_work(V, F + H, Fo))]]
+    if name == "rgcn_rmat":
+        R, Fi, Fo = g["W_rel"].shape
+        pairs, rows = int(rel_counts.pairs), int(rel_counts.pair_rows)
+        srcs = min(V, pairs)
+        return [[G("relation transform", ((srcs * Fi + R * Fi * Fo + rows * Fo) * 4,
+                                          2 * rows * Fi * Fo)),
+                 G("self transform", _gemm_work(V, Fi, Fo)),
+                 A("typed gather", _gather_work(V, E, Fo, Fo, src_rows=pairs, per_edge_bytes=4,
+                                                per_row_bytes=Fo * 4, flops_per_edge=2 * Fo))]]
+    raise ValueError(name)
+
+
+def time_stages(S, torch, model, x, ef, stages, reps, markers=False):
+    """Mean ms of every stage of every layer: events recorded by the library
+    after each stage (saga_trace_stages), one more before each layer."""
+    st = torch.cuda.current_stream()
+    evs = []
+    for _ in range(reps):
+        h = x
+        row = []
+        for layer, names in zip(model, stages):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+            S.saga_trace_stages(ev[1:], markers)
+            ev[0].record(st)
+            h = layer(h, edge_feat=ef)
+            row.append(ev)
+        evs.append(row)
+    S.saga_trace_stages([])
+    torch.cuda.synchronize()
+    return [[statistics.fmean(evs[r][i][k].elapsed_time(evs[r][i][k + 1]) for r in range(reps))
+             for k in range(len(names))] for i, names in enumerate(stages)]
+
+
+def suite_rooflines(name, stages, ms):
+    """Each stage against its roofline: compulsory bytes against 8 TB/s, the
+    transforms' flops against the float32 MFMA peak, and, where a counter
+    record in profiles/ matches the kernel sources, the measured HBM bytes."""
+    out = []
+    for li, (layer, tl) in enumerate(zip(stages, ms)):
+        for (st, kind, byts, flops), t_ms in zip(layer, tl):
+            t = t_ms * 1e-3
+            d = {"layer": li + 1, "stage": st, "bound": kind, "ms": round(t_ms, 5),
+                 "compulsory_bytes": byts, "compulsory_GBps": byts / t / 1e9,
+                 "compulsory_frac_of_8TBps": byts / t / PEAK_HBM}
+            if kind == "mfma":
+                d["TFLOPs"] = flops / t / 1e12
+                d["mfma_frac"] = flops / t / PEAK_MFMA["f32"]
+            tr = load_traffic(f"suite:{name}:L{li + 1}:{st}", "f32")
+            if tr:
+                d["counter_GBps"] = tr / t / 1e9
+                d["counter_frac_of_8TBps"] = tr / t / PEAK_HBM
+            out.append(d)
+    return out
+
+
+def suite(dev, reps=10, oracle=True, schedule=None):
     """Per-workload, per-layer timing of the other six workloads through
-    saga_layer (plan built once per graph and timed separately); with
-    `oracle`, the oracle's whole model on the same inputs (or a bounded row
-    sample of it), one thread."""
+    saga_layer (plan built once per graph and timed separately), each layer
+    also stage by stage against its roofline; with `oracle`, the oracle's
+    whole model on the same inputs (or a bounded row sample of it), one
+    thread.  With `schedule` (a list), the stage loop runs with the
+    library's stage markers on and the calls are appended to it (for
+    attributing a counter profile's dispatches to stages)."""
     import numpy as np
     import torch
 
@@ -398,6 +514,11 @@ def suite(dev, reps=10, oracle=True):
         for _ in range(3):
             LY.run(model, x, edge_feat=ef)
         torch.cuda.synchronize()
+        stages = suite_stages(name, g, relg.check() if name == "rgcn_rmat" else None)
+        names = [[st_[0] for st_ in layer] for layer in stages]
+        stage_ms = time_stages(S, torch, model, x, ef, names, reps, markers=schedule is not None)
+        if schedule is not None:
+            schedule.append({"workload": name, "layers": names, "calls": reps})
         per = [0.0] * len(model)
         for _ in range(reps):
             h = x
@@ -422,7 +543,8 @@ def suite(dev, reps=10, oracle=True):
             "workload": desc, "vertices": V, "edges": E,
             "plan_ms": e0.elapsed_time(e1) / reps,
             "layers": [{"ms": round(ms, 5), "gteps": E / (ms * 1e-3) / 1e9,
-                        "vertices_per_s": V / (ms * 1e-3)} for ms in per]}
+                        "vertices_per_s": V / (ms * 1e-3)} for ms in per],
+            "stage_rooflines": suite_rooflines(name, stages, stage_ms)}
         log(f"suite {name}: V={V} E={E} plan {out[name]['plan_ms']:.3f} ms, layers "
             + ", ".join(f"{ms:.3f} ms" for ms in per))
         if name == "rgcn_rmat":
@@ -451,7 +573,7 @@ def suite(dev, reps=10, oracle=True):
                 _oracle_model(name, g, rows=rows)
                 t = time.perf_counter() - t0
             out[name]["cpu_oracle"] = {"ms": t * 1e3, "edges_per_s": len(per) * e_s / t, "cores": 1,
-                                       "kind": "oracle", "sample": sample}
+                                       "kind": "oracle", "sample": sample, "cpu_model": _cpu_model()}
             log(f"suite {name}: oracle {t:.2f} s")
         del model, graph
         torch.cuda.empty_cache()
@@ -577,40 +699,89 @@ def rgcn_detail(S, torch, graph, relg, layer, x, g, dev, reps):
             "flops_vs_all_relations": pairs / (V * R)}
 
 
-def cpu_baseline(g, budget_s=12.0):
-    """The oracle's layer-1 GCN (aggregate-first, float64) on a bounded random
-    sample of destination rows of the same workload, one thread."""
-    import numpy as np
-    from threadpoolctl import threadpool_limits
+_CPU_G = None  # the workload, shared with forked baseline workers
 
+
+def _oracle_rows(g, rows):
+    """The oracle's layer-1 GCN (aggregate-first, float64) on some
+    destination rows; the degree scalings are computed once, outside."""
     from oracle import saga_oracle as O
 
     f_in = g["dims"][0]
-    X = g["X"][:, :f_in]
+    rp = g["row_ptr"]
+    agg = O.gather(rp, g["col_idx"], g["X"][:, :f_in], "sum", rows=rows, src_scale=g["_s_out"])
+    agg = agg * g["_s_in"][rows][:, None]
+    O.dense(agg, g["W1"], bias=g["b1"], act="relu")
+
+
+def _cpu_worker(args):
+    seed, budget_s = args
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    g = _CPU_G
     rp = g["row_ptr"].astype(np.int64)
-    rng = np.random.default_rng(7)
-    V = g["num_vertices"]
-    # degrees once, outside the timed region (the oracle recomputes them per
-    # call otherwise); the per-row Gather and the transform are timed
-    d_out = O.out_degrees(g["col_idx"], V)
-    s_out = O.degree_scale(d_out)
-    s_in = O.degree_scale(np.diff(rp))
-    edges = 0
-    rows_done = 0
-    t = 0.0
+    rng = np.random.default_rng(seed)
+    edges, t, n = 0, 0.0, 0
     with threadpool_limits(1):
-        while t < budget_s and rows_done < 400000:
-            rows = rng.integers(0, V, 2000)
+        while t < budget_s:
+            rows = rng.integers(0, g["num_vertices"], 500)
             t0 = time.perf_counter()
-            agg = O.gather(rp, g["col_idx"], X, "sum", rows=rows, src_scale=s_out)
-            agg = agg * s_in[rows][:, None]
-            O.dense(agg, g["W1"], bias=g["b1"], act="relu")
+            _oracle_rows(g, rows)
             t += time.perf_counter() - t0
             edges += int((rp[rows + 1] - rp[rows]).sum())
-            rows_done += len(rows)
-    return dict(value=edges / t, unit="edges/s", cores=1, kind="oracle",
-                sample=f"layer-1 GCN (602->128, aggregate-first, float64) on {rows_done} random "
-                       f"destination rows ({edges} in-edges) of the same graph; {t:.1f} s")
+            n += len(rows)
+    return edges, n
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(g, budget_s=12.0):
+    """The oracle's layer-1 GCN (aggregate-first, float64) on bounded random
+    samples of destination rows of the same workload: once on one thread,
+    and once on every core of the affinity mask (at most 16), each worker
+    process one thread on its own sample.  Runs before the GPU is touched
+    (its workers are forked)."""
+    import multiprocessing as mp
+
+    import numpy as np
+
+    from oracle import saga_oracle as O
+
+    global _CPU_G
+    V = g["num_vertices"]
+    g["_s_out"] = O.degree_scale(O.out_degrees(g["col_idx"], V))
+    g["_s_in"] = O.degree_scale(np.diff(g["row_ptr"].astype(np.int64)))
+    _CPU_G = g
+    t0 = time.perf_counter()
+    e1, n1 = _cpu_worker((7, budget_s / 2))
+    t1 = time.perf_counter() - t0
+    cores = max(1, min(len(os.sched_getaffinity(0)), 16))
+    en, nn, tn = e1, n1, t1
+    if cores > 1:
+        t0 = time.perf_counter()
+        with mp.get_context("fork").Pool(cores) as pool:
+            res = pool.map(_cpu_worker, [(100 + k, budget_s / 2) for k in range(cores)])
+        tn = time.perf_counter() - t0
+        en, nn = sum(r[0] for r in res), sum(r[1] for r in res)
+    _CPU_G = None
+    for k in ("_s_out", "_s_in"):
+        g.pop(k)
+    return dict(value=en / tn, unit="edges/s", cores=cores, kind="oracle", cpu_model=_cpu_model(),
+                sample=f"layer-1 GCN (602->128, aggregate-first, float64) on {nn} random destination "
+                       f"rows ({en} in-edges) of the same graph, {cores} worker processes of one "
+                       f"thread each, {tn:.1f} s wall",
+                single_thread={"value": e1 / t1, "unit": "edges/s", "cores": 1,
+                               "sample": f"{n1} random destination rows ({e1} in-edges), {t1:.1f} s"})
 
 
 def main():
@@ -631,6 +802,9 @@ def main():
                     help="time the step with the plan's row-order branch on a second stream, "
                          "overlapping the first transform (on), or stage by stage (off); both "
                          "are measured and reported")
+    ap.add_argument("--suite-schedule", default="",
+                    help="run the suite's stage loop with the library's stage markers on and "
+                         "write its call schedule here (for attributing a counter profile)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before timing, run one device-to-device copy of this many MiB "
                          "(a known-size kernel for calibrating memory counters)")
@@ -644,14 +818,21 @@ def main():
 
     from synth import configs as Cfg
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    dev = torch.device("cuda:0")
     t0 = time.time()
     g = Cfg.build("gcn_rmat", scale=args.scale)
+    log(f"inputs: V={g['num_vertices']} E={g['num_edges']} in {time.time() - t0:.1f}s")
+    cpu = None
+    if not args.no_cpu_baseline:
+        # before any GPU call: the all-cores leg forks worker processes
+        log("cpu baseline (oracle) ...")
+        cpu = cpu_baseline(g, args.cpu_budget)
+        log(f"cpu baseline: {cpu['value']:.3e} edges/s on {cpu['cores']} cores, "
+            f"{cpu['single_thread']['value']:.3e} on one")
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
     dtypes = [args.dtype] + [d for d in args.variants.split(",") if d and d != args.dtype]
     if "bf16" in dtypes:
         Cfg.add_bf16_variant(g)
-    log(f"inputs: V={g['num_vertices']} E={g['num_edges']} in {time.time() - t0:.1f}s")
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 18
@@ -699,8 +880,9 @@ def main():
     dom = max(stages, key=lambda n: r["mean"][n])
     byts, flops = algorithmic(step, dom)
     dur = r["mean"][dom] * 1e-3
-    kernel_name = {"gather1": "k_gather_simple", "gather2": "k_gather_simple",
-                   "gemm1": "k_gemm", "gemm2": "k_gemm"}[dom]
+    kernel_name = {"gather1": "k_gather_sum", "gather2": "k_gather_sum + k_gather_simple",
+                   "gemm1": "k_gemm_bres" if args.dtype == "bf16" else "k_gemm",
+                   "gemm2": "k_gemm"}[dom]
     if dom.startswith("gemm") and args.dtype == "f32":
         roof = dict(bound="mfma", achieved=flops / dur / 1e12, peak=PEAK_MFMA["f32"] / 1e12,
                     unit="TFLOP/s")
@@ -766,10 +948,13 @@ def main():
                                              "unfused_ms": rr["unfused_ms"],
                                              "speedup": rr["unfused_ms"] / rr["mean"]["gather1"]}
     if not args.no_suite:
-        out["suite"] = suite(dev, oracle=not args.no_cpu_baseline)
-    if not args.no_cpu_baseline:
-        log("cpu baseline (oracle) ...")
-        out["cpu_baseline"] = cpu_baseline(g, args.cpu_budget)
+        schedule = [] if args.suite_schedule else None
+        out["suite"] = suite(dev, oracle=not args.no_cpu_baseline, schedule=schedule)
+        if schedule is not None:
+            with open(args.suite_schedule, "w") as f:
+                json.dump(schedule, f)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
 
 

@@ -576,6 +576,30 @@ saga_status saga_layer(const saga_plan* plan, const saga_layer_desc* desc, saga_
                        saga_cmat edge_feat, saga_mat out, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/* Stage tracing, for timing and profiling the stages inside saga_layer.
+ * After each of its stages, saga_layer records the next of these caller-
+ * created hipEvent_t on its stream (events[0] after the first stage, ...;
+ * stages past n_events record nothing), and with markers != 0 launches an
+ * empty kernel named k_stage_mark there (and k_stage_begin before the first
+ * stage), which delimit the stages in a counter profile's list of
+ * dispatches.  The stages, in order:
+ *   GCN (transform first)   transform, gather (a split output: transform,
+ *                           gather of the whole-line columns, gather of the
+ *                           rest)
+ *   GCN (aggregate first)   gather, transform
+ *   GAT                     transform (with the folded attention columns),
+ *                           gather
+ *   SAGE_POOL               pool transform, max gather, concat transform
+ *   SAGE_LSTM               input transform, LSTM gather, concat transform
+ *   GATED_GRU               source-gate transform, destination-gate
+ *                           transform, gated gather, GRU transform
+ *   RGCN                    relation transform, self transform, typed gather
+ * Each saga_layer call starts again from events[0].  The setting is
+ * thread-local and copied (the array may be freed after the call); pass
+ * NULL, 0, 0 to stop.  Errors: SAGA_EINVAL (n_events < 0, a null array or
+ * event). */
+saga_status saga_trace_stages(void* const* events, int32_t n_events, int32_t markers);
+
 /* ====================================================================== */
 const char* saga_status_str(saga_status s);
 const char* saga_last_error(void);

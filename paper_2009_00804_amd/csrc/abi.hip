@@ -8,6 +8,7 @@
 #include <cstring>
 #include <exception>
 #include <mutex>
+#include <vector>
 
 #include "saga.h"
 #include "saga_internal.h"
@@ -784,6 +785,34 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
   return c.used;
 }
 
+// ---------------------------------------------------------------------------
+// Stage tracing (saga_trace_stages): after each stage of saga_layer, record
+// the next of the caller's events on the layer's stream and, with markers,
+// launch k_stage_mark, an empty kernel that delimits the stages in a
+// counter profile's dispatch list (k_stage_begin opens each traced layer
+// call).  Thread-local; off unless set.
+// ---------------------------------------------------------------------------
+__global__ void k_stage_begin() {}
+__global__ void k_stage_mark() {}
+
+thread_local std::vector<hipEvent_t> g_stage_events;
+thread_local int g_stage_next = 0;
+thread_local int g_stage_markers = 0;
+
+saga_status stage_done(hipStream_t st) {
+  if (g_stage_next < (int)g_stage_events.size()) {
+    const hipError_t e = hipEventRecord(g_stage_events[g_stage_next], st);
+    if (e != hipSuccess) return dev_fail(e, "stage event");
+  }
+  ++g_stage_next;
+  if (g_stage_markers) {
+    hipLaunchKernelGGL(k_stage_mark, dim3(1), dim3(64), 0, st);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return dev_fail(e, "stage marker");
+  }
+  return SAGA_OK;
+}
+
 saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_cmat& x,
                       const saga_cmat& ef, const saga_mat& out, void* ws, size_t ws_bytes,
                       hipStream_t st) {
@@ -796,6 +825,12 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
   if ((uintptr_t)ws % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
   b = LayerBufs();
   layer_carve(p, d, ws, &b);
+  g_stage_next = 0;
+  if (g_stage_markers) {
+    hipLaunchKernelGGL(k_stage_begin, dim3(1), dim3(64), 0, st);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return dev_fail(e, "stage marker");
+  }
   const size_t es = esize(d.dtype);
   const int64_t V = p.num_dst, Fi = d.in_feat, Fo = d.out_feat;
   s = check_mat(x.ptr, x.rows, x.cols, x.ld, V, Fi, es, true, "x");
@@ -829,6 +864,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
         s = run_gemm(g, x, saga_cmat{d.w, Fi, Fo, Fo}, none, none, nullptr, nullptr,
                      saga_mat{b.z, V, sp > 0 ? sp : Fo, b.ldz}, b.gws, b.gws_bytes, st);
         if (s) return s;
+        if ((s = stage_done(st))) return s;
         op.msg = SAGA_MSG_COPY;
         op.reduce = SAGA_RED_SUM;
         op.dst_norm = 1;
@@ -836,18 +872,23 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
         if (sp == 0) {
           in.src = saga_cmat{b.z, V, Fo, b.ldz};
           in.bias = d.b;
-          return run_gather(p, op, in, out, b.part, b.part_bytes, st);
+          s = run_gather(p, op, in, out, b.part, b.part_bytes, st);
+          if (s) return s;
+          return stage_done(st);
         }
         // the whole-line columns, then the rest, into the two column ranges of out
         in.src = saga_cmat{b.z, V, sp, b.ldz};
         in.bias = d.b;
         s = run_gather(p, op, in, saga_mat{out.ptr, out.rows, sp, out.ld}, b.part, b.part_bytes, st);
         if (s) return s;
+        if ((s = stage_done(st))) return s;
         in.src = saga_cmat{b.z3, V, Fo - sp, b.ldz3};
         in.bias = d.b ? d.b + sp : nullptr;
-        return run_gather(p, op, in,
-                          saga_mat{static_cast<char*>(out.ptr) + sp * es, out.rows, Fo - sp, out.ld},
-                          b.part, b.part_bytes, st);
+        s = run_gather(p, op, in,
+                       saga_mat{static_cast<char*>(out.ptr) + sp * es, out.rows, Fo - sp, out.ld},
+                       b.part, b.part_bytes, st);
+        if (s) return s;
+        return stage_done(st);
       }
       // aggregate first: agg = d_in^-1/2 sum_u d_out(u)^-1/2 X_u; out = act(agg W + b)
       op.msg = SAGA_MSG_SRC_NORM;
@@ -856,10 +897,13 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       in.src = x;
       s = run_gather(p, op, in, saga_mat{b.z2, V, Fi, b.ldz2}, b.part, b.part_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       g.mode = SAGA_GEMM_PLAIN;
       g.act = d.act;
-      return run_gemm(g, saga_cmat{b.z2, V, Fi, b.ldz2}, saga_cmat{d.w, Fi, Fo, Fo}, none, none,
-                      d.b, nullptr, out, b.gws, b.gws_bytes, st);
+      s = run_gemm(g, saga_cmat{b.z2, V, Fi, b.ldz2}, saga_cmat{d.w, Fi, Fo, Fo}, none, none,
+                   d.b, nullptr, out, b.gws, b.gws_bytes, st);
+      if (s) return s;
+      return stage_done(st);
     }
     case SAGA_LAYER_GAT: {
       const int64_t H = d.heads;
@@ -872,6 +916,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       s = run_gemm(g, x, saga_cmat{b.wext, Fi, cols, b.ldw}, none, none, nullptr, nullptr,
                    saga_mat{b.z, V, cols, b.ldz}, b.gws, b.gws_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       const float* z = static_cast<const float*>(b.z);
       op.msg = SAGA_MSG_GAT;
       op.reduce = SAGA_RED_SOFTMAX;
@@ -883,7 +928,9 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       in.el = saga_cmat{z + F, V, H, b.ldz};
       in.er = saga_cmat{z + F + H, V, H, b.ldz};
       in.bias = d.b;
-      return run_gather(p, op, in, out, b.part, b.part_bytes, st);
+      s = run_gather(p, op, in, out, b.part, b.part_bytes, st);
+      if (s) return s;
+      return stage_done(st);
     }
     case SAGA_LAYER_SAGE_POOL: {
       g.mode = SAGA_GEMM_PLAIN;
@@ -891,16 +938,20 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       s = run_gemm(g, x, saga_cmat{d.w_pool, Fi, Fi, Fi}, none, none, d.b_pool, nullptr,
                    saga_mat{b.z, V, Fi, b.ldz}, b.gws, b.gws_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       op.msg = SAGA_MSG_COPY;
       op.reduce = SAGA_RED_MAX;
       in.src = saga_cmat{b.z, V, Fi, b.ldz};
       s = run_gather(p, op, in, saga_mat{b.z2, V, Fi, b.ldz2}, b.part, b.part_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       const char* w = static_cast<const char*>(d.w);
       g.mode = SAGA_GEMM_CONCAT;
       g.act = SAGA_ACT_NONE;
-      return run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, Fi, b.ldz2},
-                      saga_cmat{w + (size_t)Fi * Fo * es, Fi, Fo, Fo}, d.b, nullptr, out, b.gws, b.gws_bytes, st);
+      s = run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, Fi, b.ldz2},
+                   saga_cmat{w + (size_t)Fi * Fo * es, Fi, Fo, Fo}, d.b, nullptr, out, b.gws, b.gws_bytes, st);
+      if (s) return s;
+      return stage_done(st);
     }
     case SAGA_LAYER_SAGE_LSTM: {
       // P = X W_ih + b_ih + b_hh; A = LSTM Gather; out = [X | A] W + b
@@ -909,14 +960,18 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       s = run_gemm(g, x, saga_cmat{d.w_ih, Fi, 4 * H, 4 * H}, none, none, d.b_ih, d.b_hh,
                    saga_mat{b.z, V, 4 * H, b.ldz}, b.gws, b.gws_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       s = run_lstm(p, saga_cmat{b.z, V, 4 * H, b.ldz}, saga_cmat{d.w_hh, H, 4 * H, 4 * H},
                    saga_mat{b.z2, V, H, b.ldz2}, b.lstm_q, kLstmWs, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       const char* w = static_cast<const char*>(d.w);
       g.mode = SAGA_GEMM_CONCAT;
-      return run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, H, b.ldz2},
-                      saga_cmat{w + (size_t)Fi * Fo * 4, H, Fo, Fo}, d.b, nullptr, out, b.gws,
-                      b.gws_bytes, st);
+      s = run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, H, b.ldz2},
+                   saga_cmat{w + (size_t)Fi * Fo * 4, H, Fo, Fo}, d.b, nullptr, out, b.gws,
+                   b.gws_bytes, st);
+      if (s) return s;
+      return stage_done(st);
     }
     case SAGA_LAYER_RGCN: {
       // T = pair rows x_u W_r; S = X W_self + b; out = act(S_v + sum_e norm_e T[pair_e])
@@ -924,17 +979,21 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       s = run_rel_transform(r, d.dtype, x, saga_cmat{d.w, r.num_rel * Fi, Fo, Fo},
                             saga_mat{b.z, r.max_pairs, Fo, b.ldz}, b.gws, b.gws_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       g.mode = SAGA_GEMM_PLAIN;
       s = run_gemm(g, x, saga_cmat{d.w_self, Fi, Fo, Fo}, none, none, d.b, nullptr,
                    saga_mat{b.z2, V, Fo, b.ldz2}, b.gws, b.gws_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       op.msg = SAGA_MSG_TYPED;
       op.reduce = SAGA_RED_SUM;
       op.act = d.act;
       in.src = saga_cmat{b.z, r.max_pairs, Fo, b.ldz};
       in.rel = &r;
       in.self = saga_cmat{b.z2, V, Fo, b.ldz2};
-      return run_gather(p, op, in, out, b.part, b.part_bytes, st);
+      s = run_gather(p, op, in, out, b.part, b.part_bytes, st);
+      if (s) return s;
+      return stage_done(st);
     }
     case SAGA_LAYER_GATED_GRU: {
       const int64_t F = Fi, Fe = d.edge_feat;
@@ -942,9 +1001,11 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       s = run_gemm(g, x, saga_cmat{d.w_e, F, F, F}, none, none, nullptr, nullptr,
                    saga_mat{b.z, V, F, b.ldz}, b.gws, b.gws_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       s = run_gemm(g, x, saga_cmat{d.w_e + F * F, F, F, F}, none, none, nullptr, nullptr,
                    saga_mat{b.z2, V, F, b.ldz2}, b.gws, b.gws_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       op.msg = SAGA_MSG_GATED;
       op.reduce = SAGA_RED_SUM;
       in.src = x;
@@ -956,9 +1017,12 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       in.gate_bias = d.b_e;
       s = run_gather(p, op, in, saga_mat{b.z3, V, F, b.ldz3}, b.part, b.part_bytes, st);
       if (s) return s;
+      if ((s = stage_done(st))) return s;
       g.mode = SAGA_GEMM_GRU;
-      return run_gemm(g, saga_cmat{b.z3, V, F, b.ldz3}, saga_cmat{d.w_ih, F, 3 * F, 3 * F}, x,
-                      saga_cmat{d.w_hh, F, 3 * F, 3 * F}, d.b_ih, d.b_hh, out, b.gws, b.gws_bytes, st);
+      s = run_gemm(g, saga_cmat{b.z3, V, F, b.ldz3}, saga_cmat{d.w_ih, F, 3 * F, 3 * F}, x,
+                   saga_cmat{d.w_hh, F, 3 * F, 3 * F}, d.b_ih, d.b_hh, out, b.gws, b.gws_bytes, st);
+      if (s) return s;
+      return stage_done(st);
     }
   }
   return fail(SAGA_EINVAL, "bad layer kind");
@@ -1422,6 +1486,22 @@ saga_status saga_layer_workspace_size(const saga_plan* plan, const saga_layer_de
     if (s) return s;
     LayerBufs b;
     *bytes = layer_carve(*plan, *desc, nullptr, &b);
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_trace_stages(void* const* events, int32_t n_events, int32_t markers) {
+  try {
+    if (n_events < 0 || (n_events > 0 && !events))
+      return fail(SAGA_EINVAL, "trace: %d events at %p", n_events, (const void*)events);
+    for (int32_t i = 0; i < n_events; ++i)
+      if (!events[i]) return fail(SAGA_EINVAL, "trace: event %d is null", i);
+    g_stage_events.assign(reinterpret_cast<const hipEvent_t*>(events),
+                          reinterpret_cast<const hipEvent_t*>(events) + n_events);
+    g_stage_markers = markers ? 1 : 0;
+    g_stage_next = 0;
     return ok();
   } catch (...) {
     return fail(SAGA_EINTERNAL, "exception");

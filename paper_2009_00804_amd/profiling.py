@@ -14,6 +14,15 @@ factor is true bytes / counted bytes.
 Usage:
   python -m paper_2009_00804_amd.profiling --trace DIR --fetch DIR --write DIR \\
       --copy-mib 1024 --dtype f32 --command "..." --out profiles
+
+Suite mode (the other workloads, stage by stage): bench.py run with
+``--suite-schedule FILE`` launches the library's stage markers
+(k_stage_begin, k_stage_mark) around every stage of its traced layer calls
+and writes the order of those calls to FILE; ``--suite FILE`` then
+attributes every dispatch of the FETCH_SIZE and WRITE_SIZE runs to its
+workload, layer and stage:
+  python -m paper_2009_00804_amd.profiling --suite FILE --fetch DIR --write DIR \\
+      --copy-mib 1024 --command "..." --out profiles
 """
 from __future__ import annotations
 
@@ -28,20 +37,31 @@ import re
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 
-# stage -> ({dtype: [(kernel-name prefix, dispatches per launch), ...]}, source file).
-# gather1 runs one dispatch per 128-byte column slice; the float32 gather2
-# runs two kernels (the 32 whole-line columns and the 9-column rest).
+# stage -> ({dtype: [(kernel-name prefix, dispatches per launch, cycle,
+# slots), ...]}, source file).  A kernel that several stages of one step
+# launch (the same instance serves the layer-1 slices and the layer-2
+# whole-line pass) is split by position: of every `cycle` consecutive
+# dispatches of it, the stage takes those at `slots`.  gather1 runs one
+# dispatch per 128-byte column slice; the float32 gather2 runs the 32
+# whole-line columns and the 9-column rest; each Gather with split rows ends
+# with a combine.
 STAGES = {
-    "gather1": ({"f32": [("k_gather_simple<float, 8, 1, 8, 4, false, 0, true", 4)],
-                 "bf16": [("k_gather_simple<unsigned short, 8, 1, 8, 4, false, 0, true", 2)]},
+    "gather1": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4>", 4, 5, (0, 1, 2, 3)),
+                         ("k_combine<float>", 1, 3, (0,))],
+                 "bf16": [("k_gather_sum<unsigned short, 8, 1, 8, 4>", 2, 2, (0, 1)),
+                          ("k_combine<unsigned short>", 1, 2, (0,))]},
                 "gather.hip"),
-    "gather2": ({"f32": [("k_gather_simple<float, 8, 1, 8, 4, false, 0, false", 1),
-                         ("k_gather_simple<float, 4, 1, 4, 8, false, 0, false", 1)],
-                 "bf16": [("k_gather_simple<unsigned short, 8, 1, 8, 4, false, 0, false", 1)]},
+    "gather2": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4>", 1, 5, (4,)),
+                         ("k_gather_simple<float, 4, 1, 4, 8, false, 0, false", 1, 1, (0,)),
+                         ("k_combine<float>", 2, 3, (1, 2))],
+                 "bf16": [("k_gather_simple<unsigned short, 8, 1, 8, 4, false, 0, false", 1, 1, (0,)),
+                          ("k_combine<unsigned short>", 1, 2, (1,))]},
                 "gather.hip"),
-    "gemm1": ({"f32": [("k_gemm<float, 2, 8,", 1)], "bf16": [("k_gemm_bres<2, 8, 3>", 1)]},
+    "gemm1": ({"f32": [("k_gemm<float, 2, 8,", 1, 1, (0,))],
+               "bf16": [("k_gemm_bres<2, 8, 3>", 1, 1, (0,))]},
               "gemm.hip"),
-    "gemm2": ({"f32": [("k_gemm<float, 2, 3,", 1)], "bf16": [("k_gemm<unsigned short, 2, 3,", 1)]},
+    "gemm2": ({"f32": [("k_gemm<float, 2, 3,", 1, 1, (0,))],
+               "bf16": [("k_gemm<unsigned short, 2, 3,", 1, 1, (0,))]},
               "gemm.hip"),
 }
 
@@ -74,8 +94,19 @@ def kernel_stats(trace_dir):
     return {k: (len(v), sum(v) / len(v), sum(v), min(v), max(v)) for k, v in acc.items()}
 
 
+def trace_lists(trace_dir):
+    """{short kernel name: [duration us, ...]} in dispatch order."""
+    rows = list(csv.DictReader(open(_csv(trace_dir, "kernel_trace.csv"))))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    acc = collections.defaultdict(list)
+    for r in rows:
+        acc[_short(r["Kernel_Name"])].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    return acc
+
+
 def counter_avgs(counter_dir, counter):
     rows = list(csv.DictReader(open(_csv(counter_dir, "counter_collection.csv"))))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
     acc = collections.defaultdict(list)
     for r in rows:
         if r["Counter_Name"] == counter:
@@ -93,9 +124,95 @@ def calibration(acc, copy_mib):
     return (copy_mib * 1024.0) / counted_kib if counted_kib > 0 else None
 
 
+# main kernel source of each suite stage (the traffic record is valid while
+# its hash matches)
+def _stage_source(stage):
+    if stage == "LSTM gather":
+        return "lstm.hip"
+    return "gather.hip" if "gather" in stage else "gemm.hip"
+
+
+def dispatches(counter_dir, counter):
+    """[(kernel name, value)] in dispatch order."""
+    rows = [r for r in csv.DictReader(open(_csv(counter_dir, "counter_collection.csv")))
+            if r["Counter_Name"] == counter]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return [(_short(r["Kernel_Name"]), float(r["Counter_Value"])) for r in rows]
+
+
+def attribute(disp, schedule):
+    """Sum of each (workload, layer, stage)'s counter values over the traced
+    calls, and the kernels seen in each, walking the dispatches between the
+    stage markers in the order the schedule lists the calls."""
+    calls = []
+    for w in schedule:
+        for _ in range(w["calls"]):
+            for li, stages in enumerate(w["layers"]):
+                calls.append((w["workload"], li + 1, stages))
+    acc, kern = collections.defaultdict(float), collections.defaultdict(set)
+    ci, stage, inside = 0, 0, False
+    for name, val in disp:
+        if name.startswith("k_stage_begin"):
+            if ci >= len(calls):
+                raise ValueError("more traced calls in the profile than in the schedule")
+            inside, stage = True, 0
+            continue
+        if not inside:
+            continue
+        wl, li, stages = calls[ci]
+        if name.startswith("k_stage_mark"):
+            stage += 1
+            if stage == len(stages):
+                inside = False
+                ci += 1
+            continue
+        acc[(wl, li, stages[stage])] += val
+        kern[(wl, li, stages[stage])].add(name)
+    if ci != len(calls):
+        raise ValueError(f"profile holds {ci} traced calls, the schedule {len(calls)}")
+    return acc, kern
+
+
+def suite_main(a):
+    schedule = json.load(open(a.suite))
+    fe, wr = dispatches(a.fetch, "FETCH_SIZE"), dispatches(a.write, "WRITE_SIZE")
+    cf = calibration({"__amd_rocclr_copyBuffer": [v for n, v in fe if n == "__amd_rocclr_copyBuffer"]},
+                     a.copy_mib)
+    cw = calibration({"__amd_rocclr_copyBuffer": [v for n, v in wr if n == "__amd_rocclr_copyBuffer"]},
+                     a.copy_mib)
+    fa, fk = attribute(fe, schedule)
+    wa, _ = attribute(wr, schedule)
+    ncalls = {w["workload"]: w["calls"] for w in schedule}
+    lines = ["# HBM traffic per stage: the suite workloads (float32)", "",
+             f"command (FETCH_SIZE pass): {a.command} --pmc FETCH_SIZE",
+             f"command (WRITE_SIZE pass): {a.command} --pmc WRITE_SIZE", "",
+             f"calibration copy: {a.copy_mib:.0f} MiB device-to-device; FETCH_SIZE scale "
+             f"{cf:.3f}, WRITE_SIZE scale {cw:.3f} (true bytes / counted bytes)", "",
+             f"{'workload':10s} {'layer':>5s} {'stage':28s} {'FETCH MB':>10s} {'WRITE MB':>10s}  kernels"]
+    rec_path = os.path.join(a.out, "traffic.json")
+    rec = json.load(open(rec_path)) if os.path.exists(rec_path) else {}
+    for key in sorted(fa, key=lambda k: (k[0], k[1])):
+        wl, li, stage = key
+        n = ncalls[wl]
+        fb = fa[key] * cf * 1024 / n
+        wb = wa.get(key, 0.0) * cw * 1024 / n
+        lines.append(f"{wl:10s} {li:5d} {stage:28s} {fb / 1e6:10.2f} {wb / 1e6:10.2f}  "
+                     + ", ".join(sorted(k[:48] for k in fk[key])))
+        src = _stage_source(stage)
+        rec[f"suite:{wl}:L{li}:{stage}:f32"] = {
+            "kernels": sorted(fk[key]), "source": src, "src_sha": src_sha(src),
+            "bytes_per_launch": fb + wb, "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+            "calibration": {"fetch": cf, "write": cw}}
+    with open(os.path.join(a.out, "hbm_traffic_suite_f32.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    with open(rec_path, "w") as f:
+        json.dump(rec, f, indent=1, sort_keys=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--trace", required=True)
+    ap.add_argument("--trace")
+    ap.add_argument("--suite", help="call schedule written by bench.py --suite-schedule")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
     ap.add_argument("--copy-mib", type=float, default=1024)
@@ -105,6 +222,8 @@ def main():
     ap.add_argument("--tag", default="gcn_rmat21")
     a = ap.parse_args()
     os.makedirs(a.out, exist_ok=True)
+    if a.suite:
+        return suite_main(a)
 
     st = kernel_stats(a.trace)
     tot = sum(v[2] for v in st.values())
@@ -138,21 +257,23 @@ def main():
 
     rec_path = os.path.join(a.out, "traffic.json")
     rec = json.load(open(rec_path)) if os.path.exists(rec_path) else {}
+    tr_us = trace_lists(a.trace)
     for stage, (pats, src) in STAGES.items():
         parts = []
-        for pat, per in pats[a.dtype]:
+        for pat, per, cycle, slots in pats[a.dtype]:
             keys = [k for k in set(fe) | set(wr) if k.startswith(pat)]
             if len(keys) != 1:
                 break
-            parts.append((keys[0], per))
+            parts.append((keys[0], per, cycle, slots))
         if len(parts) != len(pats[a.dtype]):
             continue
         entry = {"kernels": [], "source": src, "src_sha": src_sha(src), "bytes_per_launch": 0.0,
                  "trace_us_per_launch": 0.0, "calibration": {"fetch": cf, "write": cw}}
-        for k, per in parts:
-            f_ = sum(fe[k]) / len(fe[k])
-            w_ = sum(wr[k]) / len(wr[k])
-            n_avg = st.get(k, (0, 0.0, 0.0))[1]
+        for k, per, cycle, slots in parts:
+            pick = lambda v: [x for i, x in enumerate(v) if i % cycle in slots] or [0.0]  # noqa: E731
+            f_ = sum(pick(fe[k])) / len(pick(fe[k]))
+            w_ = sum(pick(wr[k])) / len(pick(wr[k]))
+            n_avg = sum(pick(tr_us.get(k, []))) / len(pick(tr_us.get(k, [])))
             entry["kernels"].append({
                 "kernel": k, "dispatches_per_launch": per,
                 "fetch_bytes_per_dispatch": f_ * cf * 1024,

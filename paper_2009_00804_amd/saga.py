@@ -42,7 +42,8 @@ EXPORTS = [
     "saga_rel_plan_workspace_size", "saga_rel_plan_build", "saga_rel_plan_check",
     "saga_rel_transform_workspace_size", "saga_rel_transform",
     "saga_apply_vertex_workspace_size", "saga_apply_vertex",
-    "saga_layer_workspace_size", "saga_layer", "saga_status_str", "saga_last_error",
+    "saga_layer_workspace_size", "saga_layer", "saga_trace_stages", "saga_status_str",
+    "saga_last_error",
     "saga_version",
 ]
 
@@ -171,6 +172,7 @@ def lib():
         "saga_layer_workspace_size": (S, [P(saga_plan), P(saga_layer_desc), P(C.c_size_t)]),
         "saga_layer": (S, [P(saga_plan), P(saga_layer_desc), saga_cmat, saga_cmat, saga_mat, C.c_void_p,
                            C.c_size_t, C.c_void_p]),
+        "saga_trace_stages": (S, [C.POINTER(C.c_void_p), C.c_int32, C.c_int32]),
         "saga_status_str": (C.c_char_p, [S]),
         "saga_last_error": (C.c_char_p, []),
         "saga_version": (C.c_char_p, []),
@@ -326,6 +328,18 @@ def saga_apply_vertex(op, a, w, a2, w2, bias, bias2, out, workspace, ws_bytes, s
     return _check(lib().saga_apply_vertex(C.byref(op), a, w, a2, w2, bias, bias2, out, workspace,
                                           ws_bytes, stream),
                   "saga_apply_vertex")
+
+
+def saga_trace_stages(events, markers=False):
+    """Record events[i] (torch.cuda.Event) after stage i of each saga_layer
+    call on this thread; saga_trace_stages([]) stops."""
+    for e in events:
+        if not e.cuda_event:      # torch creates the event at its first record
+            e.record()
+    handles = [e.cuda_event for e in events]
+    arr = (C.c_void_p * max(1, len(handles)))(*handles)
+    return _check(lib().saga_trace_stages(arr if handles else None, len(handles), int(markers)),
+                  "saga_trace_stages")
 
 
 def saga_layer_workspace_size(plan, desc):

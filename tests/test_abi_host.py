@@ -151,6 +151,15 @@ def test_gather_rejects_bad_arguments(S):
     assert b"F == 64" in L.saga_last_error()
 
 
+def test_trace_stages_rejects_bad_arguments(S):
+    L = S.lib()
+    assert L.saga_trace_stages(None, -1, 0) == S.SAGA_EINVAL
+    assert L.saga_trace_stages(None, 2, 0) == S.SAGA_EINVAL
+    arr = (C.c_void_p * 2)(None, None)
+    assert L.saga_trace_stages(arr, 2, 1) == S.SAGA_EINVAL     # null events
+    assert L.saga_trace_stages(None, 0, 0) == S.SAGA_OK         # tracing off
+
+
 def test_unfused_rejects_bad_arguments(S):
     """The unfused baseline: unsupported ops, workspace size, alignment and
     overlap are all rejected on the host before any launch."""

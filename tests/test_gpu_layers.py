@@ -183,3 +183,29 @@ def test_layer_repeatable_and_equivariant():
     y2 = LY.run(LY.sage_pool(graph2, g2), dev_padded(g2["X"]))
     torch.cuda.synchronize()
     assert rel_err(to_np(y2)[pi], to_np(a)) <= FP32_TOL
+
+
+def test_stage_tracing_records_every_stage_and_changes_nothing():
+    """saga_trace_stages: the layer records one event after each of its
+    stages, in order, and with the stage markers on its output bytes are
+    the same as untraced."""
+    from paper_2009_00804_amd import layers as LY
+
+    S = lib()
+    g = C.build("sage_rmat", small=True)
+    graph = _graph(g)
+    x = dev_padded(g["X"])
+    model = LY.sage_pool(graph, g)
+    want = model[0](x).clone()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    S.saga_trace_stages(ev[1:], markers=True)
+    ev[0].record(st)
+    got = model[0](x)
+    S.saga_trace_stages([])
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
+    t = [ev[k].elapsed_time(ev[k + 1]) for k in range(3)]   # pool transform, max gather, concat
+    print(f"sage-pool stages (ms): {t}", flush=True)
+    assert all(x_ >= 0.0 for x_ in t) and sum(t) > 0.0
