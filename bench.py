@@ -144,6 +144,16 @@ class Step:
         self.stream = torch.cuda.current_stream()
         self.sh = S.stream_handle(self.stream)
         self.names = ["plan", "gemm1", "gather1", "gemm2", "gather2"]
+        # cross-stage fusion: layer 1's Gather with layer 2's transform in its
+        # last slice pass writes Z2 directly (no H1, no separate gemm2)
+        self.fused = False
+        self.nx = S.saga_next_transform()
+        self.nx.w = S.cmat(self.W2)
+        self.nx.row_scale_deg = p.d_out
+        if self.split2:
+            self.nx.split_col = self.split2
+            self.nx.tail = S.mat(self.Z2t)
+        self.xws = S.workspace(S.saga_gather_transform_workspace_size(p, self.op1, hid), dev)
         self.ev = None
         self.uws = None
         # stage pipelining: the plan's row-order branch on a second stream
@@ -204,15 +214,23 @@ class Step:
             self.stream.wait_event(self.join)
         if ev:
             ev[2].record(self.stream)
-        S.saga_scatter_apply_edge_gather(p, self.op1, self.in1, S.mat(self.H1),
-                                         C.c_void_p(self.gws.data_ptr()), self.gws.numel(), self.sh)
-        if ev:
-            ev[3].record(self.stream)
-        S.saga_apply_vertex(self.gop2, S.cmat(self.H1), S.cmat(self.W2), self.none, self.none, None,
-                            None, S.mat(self.Z2), C.c_void_p(self.mws.data_ptr()), self.mws.numel(),
-                            self.sh)
-        if ev:
-            ev[4].record(self.stream)
+        if self.fused:
+            S.saga_scatter_apply_edge_gather_transform(p, self.op1, self.in1, self.nx, S.mat(self.Z2),
+                                                       C.c_void_p(self.xws.data_ptr()), self.xws.numel(),
+                                                       self.sh)
+            if ev:
+                ev[3].record(self.stream)
+                ev[4].record(self.stream)
+        else:
+            S.saga_scatter_apply_edge_gather(p, self.op1, self.in1, S.mat(self.H1),
+                                             C.c_void_p(self.gws.data_ptr()), self.gws.numel(), self.sh)
+            if ev:
+                ev[3].record(self.stream)
+            S.saga_apply_vertex(self.gop2, S.cmat(self.H1), S.cmat(self.W2), self.none, self.none,
+                                None, None, S.mat(self.Z2), C.c_void_p(self.mws.data_ptr()),
+                                self.mws.numel(), self.sh)
+            if ev:
+                ev[4].record(self.stream)
         S.saga_scatter_apply_edge_gather(p, self.op2, self.in2, self.out2,
                                          C.c_void_p(self.gws.data_ptr()), self.gws.numel(), self.sh)
         if self.split2:
@@ -802,6 +820,9 @@ def main():
                     help="time the step with the plan's row-order branch on a second stream, "
                          "overlapping the first transform (on), or stage by stage (off); both "
                          "are measured and reported")
+    ap.add_argument("--fused", choices=["on", "off"], default="off",
+                    help="time the step with layer 2's transform fused into layer 1's Gather "
+                         "(on) for the headline value; both are measured and reported")
     ap.add_argument("--suite-schedule", default="",
                     help="run the suite's stage loop with the library's stage markers on and "
                          "write its call schedule here (for attributing a counter profile)")
@@ -854,14 +875,23 @@ def main():
         mean = {n: statistics.fmean(v) for n, v in per.items()}
         step.split = True
         wall_p, _, _ = time_step(step, args.steps, args.warmup)
-        step.split = args.pipeline == "on"
         ms_pipe = wall_p * 1e3 / args.steps
-        ms = ms_pipe if step.split else ms_seq
+        # and with layer 2's transform fused into layer 1's Gather
+        step.fused = True
+        wall_f, per_f, _ = time_step(step, args.steps, args.warmup)
+        ms_fused = wall_f * 1e3 / args.steps
+        fused_gather1 = statistics.fmean(per_f["gather1"])
+        step.split = args.pipeline == "on"
+        step.fused = args.fused == "on"
+        ms = ms_fused if step.fused else (ms_pipe if step.split else ms_seq)
         results[dt] = dict(step=step, ms=ms, med=med, mean=mean, counts=counts,
-                           ev_ms=statistics.median(tot), ms_seq=ms_seq, ms_pipe=ms_pipe)
+                           ev_ms=statistics.median(tot), ms_seq=ms_seq, ms_pipe=ms_pipe,
+                           ms_fused=ms_fused, fused_gather1=fused_gather1)
         log(f"{dt}: {ms_seq:.3f} ms/step stage by stage (events {statistics.median(tot):.3f}); "
             + ", ".join(f"{n} {med[n]:.3f}" for n in step.names)
-            + f"; {ms_pipe:.3f} ms/step with the plan's row order overlapping gemm1")
+            + f"; {ms_pipe:.3f} ms/step with the plan's row order overlapping gemm1"
+            + f"; {ms_fused:.3f} ms/step with layer 2's transform fused into layer 1's Gather "
+              f"({fused_gather1:.3f} ms for the fused stage)")
         if not args.no_unfused:
             um = time_unfused(step)
             results[dt]["unfused_ms"] = um
@@ -931,6 +961,15 @@ def main():
                 "blocks) on a second stream, overlapping the d_out-scaled layer-1 transform",
         "stage_by_stage_ms": r["ms_seq"], "pipelined_ms": r["ms_pipe"],
         "speedup": r["ms_seq"] / r["ms_pipe"], "value_uses": args.pipeline}
+    out["cross_stage_fusion"] = {
+        "what": "layer 2's transform (d_out^-1/2 (h1 W2)) done inside layer 1's last Gather "
+                "pass, each wave multiplying the rows it has just finished on the matrix cores "
+                "(saga_scatter_apply_edge_gather_transform), instead of a separate GEMM over "
+                "all rows after the Gather; with the plan's row order overlapping gemm1",
+        "pipelined_ms": r["ms_pipe"], "fused_ms": r["ms_fused"],
+        "unfused_gather1_plus_gemm2_ms": r["mean"]["gather1"] + r["mean"]["gemm2"],
+        "fused_stage_ms": r["fused_gather1"], "speedup": r["ms_pipe"] / r["ms_fused"],
+        "value_uses": args.fused}
     if "unfused_ms" in r:
         out["fusion"] = {
             "stage": "layer-1 Scatter+ApplyEdge+Gather (Fig. 7a unfused vs Fig. 7b fused)",
@@ -941,6 +980,7 @@ def main():
         out.setdefault("variants", {})[dt] = {
             "value": 2 * E / (rr["ms"] * 1e-3), "ms_per_step": rr["ms"],
             "stage_by_stage_ms": rr["ms_seq"], "pipelined_ms": rr["ms_pipe"],
+            "fused_ms": rr["ms_fused"], "fused_stage_ms": rr["fused_gather1"],
             "stage_ms": {n: round(rr["mean"][n], 4) for n in rr["mean"]},
             "stage_rooflines": stage_rooflines(V, E, step.dims, dt, rr["mean"])}
         if "unfused_ms" in rr:

@@ -390,6 +390,48 @@ saga_status saga_scatter_apply_edge_gather(const saga_plan* plan, const saga_edg
                                            void* workspace, size_t workspace_bytes,
                                            void* stream);
 
+/* ----------------------------------------------------------------------
+ * Gather with the next layer's transform fused in (the paper's outlook of
+ * pipelining stages finely instead of running them one after another,
+ * Sec. 4 "Forward Looking"; here the next layer's ApplyVertex transform
+ * starts on a row block as soon as the Gather has finished it): with h_v
+ * the row that saga_scatter_apply_edge_gather would write for v,
+ *     out[v] = rs(v) * (h_v next->w)      rs(v) = next->row_scale_deg ?
+ *                                          deg[v]^-1/2 (0 for deg 0) : 1
+ * h lives in the workspace only: the Gather runs one 128-byte column slice
+ * of the source per pass, and in the last pass each workgroup, once its
+ * rows are whole, multiplies them by w on the matrix cores (16 rows at a
+ * time); rows split into segments are multiplied after their combine.  For
+ * bfloat16, h takes its bfloat16 storage rounding before the product, as
+ * when it is stored and transformed by saga_apply_vertex; the product
+ * accumulates in float32.
+ * Supported: COPY messages with SUM or MEAN (dst_norm, bias, act and self
+ * as in saga_scatter_apply_edge_gather); src 1 to 4 whole 128-byte lines
+ * wide (32..128 float32 or 64..256 bfloat16 columns) and under 4 GiB;
+ * w: F x N dense (ld == N), the op's dtype, 1 <= N <= 64; split_col (0, or
+ * a multiple of 16 bytes of columns in (0, N)) sends columns from split_col
+ * on to `tail`, as saga_apply_vertex's split output does.  out: num_dst x
+ * (split_col ? split_col : N), 16-byte rows.  Workspace:
+ * saga_gather_transform_workspace_size(plan, op, F) bytes, 256-byte aligned
+ * (the split-row partials, h and w packed for the matrix cores).  Errors as
+ * saga_scatter_apply_edge_gather,
+ * SAGA_EUNSUPPORTED outside the supported shapes. */
+typedef struct saga_next_transform {
+  saga_cmat w;                    /* F x N weights */
+  const int32_t* row_scale_deg;   /* nullable, int32[num_dst] */
+  int32_t split_col;              /* 0 = one output matrix */
+  saga_mat tail;                  /* num_dst x (N - split_col) when split_col > 0 */
+} saga_next_transform;
+
+saga_status saga_gather_transform_workspace_size(const saga_plan* plan, const saga_edge_op* op,
+                                                 int64_t feat, size_t* bytes);
+
+saga_status saga_scatter_apply_edge_gather_transform(const saga_plan* plan, const saga_edge_op* op,
+                                                     const saga_edge_inputs* in,
+                                                     const saga_next_transform* next,
+                                                     saga_mat out, void* workspace,
+                                                     size_t workspace_bytes, void* stream);
+
 /* The same Gather for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): no workspace argument.  The split-row partials go to a fixed

@@ -237,15 +237,9 @@ saga_status validate_edge_op(const saga_plan& p, const saga_edge_op& op,
   return SAGA_OK;
 }
 
-saga_status run_gather(const saga_plan& p, const saga_edge_op& op, const saga_edge_inputs& in,
-                       const saga_mat& out, void* ws, size_t ws_bytes, hipStream_t st) {
-  saga_status s = validate_edge_op(p, op, in, out);
-  if (s) return s;
-  size_t need;
-  gather_ws_bytes(p, op, in.src.cols, &need);
-  if (p.max_split_segments > 0 && (!ws || ws_bytes < need))
-    return fail(SAGA_EWORKSPACE, "gather workspace: need %zu bytes, got %zu", need, ws_bytes);
-  if (p.num_dst == 0) return ok();
+// GatherArgs of a validated call: plan, op, inputs, output, partials at ws
+saga::GatherArgs fill_gather_args(const saga_plan& p, const saga_edge_op& op,
+                                  const saga_edge_inputs& in, const saga_mat& out, void* ws) {
   saga::GatherArgs a = gather_args_from_plan(p);
   a.msg = op.msg;
   a.reduce = op.reduce;
@@ -286,8 +280,104 @@ saga_status run_gather(const saga_plan& p, const saga_edge_op& op, const saga_ed
   a.partial = static_cast<float*>(ws);
   a.pstride = (int64_t)saga::gather_partial_stride(op, in.src.cols);
   a.pcols = saga::gather_partial_cols(in.src.cols);
+  return a;
+}
+
+saga_status run_gather(const saga_plan& p, const saga_edge_op& op, const saga_edge_inputs& in,
+                       const saga_mat& out, void* ws, size_t ws_bytes, hipStream_t st) {
+  saga_status s = validate_edge_op(p, op, in, out);
+  if (s) return s;
+  size_t need;
+  gather_ws_bytes(p, op, in.src.cols, &need);
+  if (p.max_split_segments > 0 && (!ws || ws_bytes < need))
+    return fail(SAGA_EWORKSPACE, "gather workspace: need %zu bytes, got %zu", need, ws_bytes);
+  if (p.num_dst == 0) return ok();
+  const saga::GatherArgs a = fill_gather_args(p, op, in, out, ws);
   hipError_t e = saga::launch_gather(a, st);
   if (e != hipSuccess) return dev_fail(e, "gather launch");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Gather with the next transform fused in (saga_scatter_apply_edge_gather_
+// transform): workspace = the split-row partials, then the Gather output h
+// (num_dst x F, the op's dtype; the earlier slices pass through it)
+// ---------------------------------------------------------------------------
+saga_status gather_xf_ws_bytes(const saga_plan& p, const saga_edge_op& op, int64_t feat,
+                               size_t* part, size_t* total) {
+  gather_ws_bytes(p, op, feat, part);
+  // h, then W^T packed for the matrix cores (sized for 64 output columns)
+  *total = *part + align256((size_t)p.num_dst * feat * esize(op.dtype)) +
+           align256((size_t)saga::xf_pack_bytes(feat, (int)esize(op.dtype), 64));
+  return SAGA_OK;
+}
+
+saga_status run_gather_transform(const saga_plan& p, const saga_edge_op& op,
+                                 const saga_edge_inputs& in, const saga_next_transform& nx,
+                                 const saga_mat& out, void* ws, size_t ws_bytes, hipStream_t st) {
+  const size_t es = esize(op.dtype);
+  const int64_t F = in.src.cols, N = nx.w.cols, V = p.num_dst;
+  if (op.msg != SAGA_MSG_COPY || (op.reduce != SAGA_RED_SUM && op.reduce != SAGA_RED_MEAN))
+    return fail(SAGA_EUNSUPPORTED, "gather + transform: COPY messages with SUM or MEAN only");
+  if (F <= 0 || (F * (int64_t)es) % 128 != 0 || F * (int64_t)es > 4 * 128)
+    return fail(SAGA_EUNSUPPORTED, "gather + transform: src must be 1 to 4 whole 128-byte lines "
+                                   "wide (32..128 float32 or 64..256 bfloat16 columns)");
+  if (in.src.rows * in.src.ld * (int64_t)es > (int64_t(1) << 32))
+    return fail(SAGA_EUNSUPPORTED, "gather + transform: source matrix of 4 GiB or more");
+  if (N < 1 || N > 64) return fail(SAGA_EUNSUPPORTED, "gather + transform: 1 to 64 output columns");
+  saga_status s = check_mat(nx.w.ptr, nx.w.rows, nx.w.cols, nx.w.ld, F, N, es, false, "next.w");
+  if (s) return s;
+  if (nx.w.ld != N) return fail(SAGA_EINVAL, "next.w must be dense (ld == cols)");
+  const int64_t epv = 16 / (int64_t)es;
+  if (nx.split_col < 0 || (nx.split_col > 0 && (nx.split_col >= N || nx.split_col % epv != 0)))
+    return fail(SAGA_EINVAL, "next.split_col must be 0, or in (0, N) and a multiple of %lld",
+                (long long)epv);
+  const int64_t head = nx.split_col > 0 ? nx.split_col : N;
+  s = check_mat(out.ptr, out.rows, out.cols, out.ld, V, head, es, true, "out");
+  if (s) return s;
+  const saga_mat& t = nx.tail;
+  if (nx.split_col > 0) {
+    s = check_mat(t.ptr, t.rows, t.cols, t.ld, V, N - nx.split_col, es, true, "next.tail");
+    if (s) return s;
+  }
+  size_t part, need;
+  gather_xf_ws_bytes(p, op, F, &part, &need);
+  if (!ws || ws_bytes < need)
+    return fail(SAGA_EWORKSPACE, "gather + transform workspace: need %zu bytes, got %zu", need,
+                ws_bytes);
+  if ((uintptr_t)ws % 256 != 0) return fail(SAGA_EINVAL, "workspace must be 256-byte aligned");
+  // h lives in the workspace; its shape is what the Gather's output check wants
+  const saga_mat h = {static_cast<char*>(ws) + part, V, F, F};
+  s = validate_edge_op(p, op, in, h);
+  if (s) return s;
+  const size_t ob = mat_bytes(out.rows, out.cols, out.ld, es);
+  const size_t tb = nx.split_col > 0 ? mat_bytes(t.rows, t.cols, t.ld, es) : 0;
+  const void* outs[2] = {out.ptr, nx.split_col > 0 ? t.ptr : nullptr};
+  const size_t outb[2] = {ob, tb};
+  const void* ins[5] = {in.src.ptr, nx.w.ptr, p.row_ptr, p.col_idx, ws};
+  const size_t inb[5] = {mat_bytes(in.src.rows, in.src.cols, in.src.ld, es),
+                         mat_bytes(nx.w.rows, nx.w.cols, nx.w.ld, es), (size_t)(V + 1) * 4,
+                         (size_t)p.num_edges * 4, need};
+  for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 5; ++j)
+      if (range_overlap(outs[i], outb[i], ins[j], inb[j]))
+        return fail(SAGA_EINVAL, "gather + transform: an output overlaps an input or the workspace");
+  if (nx.split_col > 0 && range_overlap(out.ptr, ob, t.ptr, tb))
+    return fail(SAGA_EINVAL, "next.tail overlaps out");
+  if (V == 0) return ok();
+  saga::GatherArgs a = fill_gather_args(p, op, in, h, ws);
+  a.xw = nx.w.ptr;
+  a.xwt = reinterpret_cast<uint4*>(static_cast<char*>(ws) + part +
+                                   align256((size_t)V * F * es));
+  a.xn = (int)N;
+  a.xsplit = nx.split_col;
+  a.xout = out.ptr;
+  a.ld_xout = out.ld;
+  a.xtail = t.ptr;
+  a.ld_xtail = t.ld;
+  a.xrs = nx.row_scale_deg;
+  hipError_t e = saga::launch_gather_transform(a, st);
+  if (e != hipSuccess) return dev_fail(e, "gather + transform launch");
   return ok();
 }
 
@@ -1265,6 +1355,37 @@ saga_status saga_scatter_apply_edge_gather_noalloc(const saga_plan* plan, const 
     e = noalloc_scratch(dev, &ws);
     if (e != hipSuccess) return dev_fail(e, "noalloc gather: scratch address");
     return run_gather(*plan, *op, *in, out, ws, kNoAllocScratchBytes, st);
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_gather_transform_workspace_size(const saga_plan* plan, const saga_edge_op* op,
+                                                 int64_t feat, size_t* bytes) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!op || !bytes) return fail(SAGA_EINVAL, "null argument");
+    if (feat <= 0) return fail(SAGA_EINVAL, "feat must be > 0");
+    size_t part;
+    gather_xf_ws_bytes(*plan, *op, feat, &part, bytes);
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
+saga_status saga_scatter_apply_edge_gather_transform(const saga_plan* plan, const saga_edge_op* op,
+                                                     const saga_edge_inputs* in,
+                                                     const saga_next_transform* next,
+                                                     saga_mat out, void* workspace,
+                                                     size_t workspace_bytes, void* stream) {
+  try {
+    saga_status s = check_plan(plan);
+    if (s) return s;
+    if (!op || !in || !next) return fail(SAGA_EINVAL, "null argument");
+    return run_gather_transform(*plan, *op, *in, *next, out, workspace, workspace_bytes,
+                                static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(SAGA_EINTERNAL, "exception");
   }

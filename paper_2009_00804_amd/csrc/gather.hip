@@ -266,6 +266,173 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(7))) v
 }
 
 // ------------------------------------------------------------------------
+// The next layer's transform fused into this Gather (cross-stage
+// pipelining, Sec. 4): y[v] = xrs(v) * (h_v W) for W F x xn (xn <= 64),
+// h_v the finished Gather row, taken as soon as a workgroup has finished
+// its rows rather than after the whole Gather.  Sixteen rows at a time go
+// onto the matrix cores with the output columns as the M side (A = W^T,
+// staged in LDS with k contiguous) and the rows as the N side (B = the h
+// rows, read from memory with k contiguous): the k order inside a chunk is
+// the same permutation on both sides, so the contraction is unchanged, and
+// a lane's four accumulators are four adjacent outputs of one row.
+// ------------------------------------------------------------------------
+template <typename T> struct XfMma;
+template <> struct XfMma<float> {
+  __device__ __forceinline__ static f32x4 mma(const uint4& w, const uint4& h, f32x4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.x), __uint_as_float(h.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.y), __uint_as_float(h.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.z), __uint_as_float(h.z), c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.w), __uint_as_float(h.w), c, 0, 0, 0);
+  }
+};
+template <> struct XfMma<uint16_t> {
+  __device__ __forceinline__ static f32x4 mma(const uint4& w, const uint4& h, f32x4 c) {
+    bf16x8 wa, hb;
+    __builtin_memcpy(&wa, &w, 16);
+    __builtin_memcpy(&hb, &h, 16);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, hb, c, 0, 0, 0);
+  }
+};
+
+// one 16-row tile: lane (lr, lg) = (lane % 16, lane / 16) brings row `row`
+// (-1: a padding lane of a short tile) and stores outputs 16 nt + 4 lg ..
+// + 3 of it.  The rows' 64-byte chunks (at most eight: F is at most 512
+// bytes) are loaded four at a time ahead of their MFMAs.
+template <typename T, int NT>
+__device__ __forceinline__ void xf_tile(const GatherArgs& a, int row, const uint4* wt) {
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int nk = (int)(a.feat * (int64_t)sizeof(T) / 64);
+  const uint4* hp = reinterpret_cast<const uint4*>(static_cast<const T*>(a.out) +
+                                                   (int64_t)(row >= 0 ? row : 0) * a.ld_out);
+  f32x4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int j0 = 0; j0 < nk; j0 += 4) {
+    uint4 hv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      hv[j] = (row >= 0 && j0 + j < nk) ? hp[(j0 + j) * 4 + lg] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (j0 + j < nk) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          acc[nt] = XfMma<T>::mma(wt[(nt * 16 + lr) * a.xldwt + (j0 + j) * 4 + lg], hv[j], acc[nt]);
+      }
+    }
+  }
+  if (row < 0) return;
+  const float rs = a.xrs ? rsqrt_deg(a.xrs[row]) : 1.0f;
+  const int head = a.xsplit > 0 ? a.xsplit : a.xn;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n0 = nt * 16 + lg * 4;
+    if (n0 >= a.xn) continue;
+    float y[4] = {acc[nt].x * rs, acc[nt].y * rs, acc[nt].z * rs, acc[nt].w * rs};
+    T* o;
+    int lim;  // outputs of the four that exist (xsplit is a multiple of 4)
+    if (n0 >= head) {
+      o = static_cast<T*>(a.xtail) + (int64_t)row * a.ld_xtail + (n0 - head);
+      lim = a.xn - n0;
+    } else {
+      o = static_cast<T*>(a.xout) + (int64_t)row * a.ld_xout + n0;
+      lim = head - n0;
+    }
+    if (lim >= 4 && ((uintptr_t)o & (4 * sizeof(T) - 1)) == 0) {
+      if constexpr (sizeof(T) == 4) {
+        *reinterpret_cast<f32x4*>(o) = f32x4{y[0], y[1], y[2], y[3]};
+      } else {
+        const uint32_t lo = (uint32_t)f32_to_bf16(y[0]) | ((uint32_t)f32_to_bf16(y[1]) << 16);
+        const uint32_t hi = (uint32_t)f32_to_bf16(y[2]) | ((uint32_t)f32_to_bf16(y[3]) << 16);
+        *reinterpret_cast<uint2*>(o) = make_uint2(lo, hi);
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if (t < lim) {
+          if constexpr (sizeof(T) == 4)
+            o[t] = y[t];
+          else
+            o[t] = f32_to_bf16(y[t]);
+        }
+      }
+    }
+  }
+}
+
+// W (F x xn, row-major) -> the packed W^T of GatherArgs::xwt
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_xf_pack(GatherArgs a, int nrows) {
+  constexpr int EPV = Vec16<T>::N;
+  const int F = a.feat;
+  const int per = a.xldwt * EPV;  // elements per packed row, pad included
+  T* wt = reinterpret_cast<T*>(a.xwt);
+  for (int i = blockIdx.x * kThreads + threadIdx.x; i < nrows * per; i += gridDim.x * kThreads) {
+    const int n = i / per, k = i - n * per;
+    T v = 0;
+    if (n < a.xn && k < F) v = static_cast<const T*>(a.xw)[(int64_t)k * a.xn + n];
+    wt[i] = v;
+  }
+}
+
+// The last slice pass of the sum Gather with the next transform fused in:
+// the slice is gathered as in k_gather_sum (its part of h goes to `out`),
+// then each wave multiplies the whole rows its own lane groups finished
+// (lane group g of the wave takes segments s0 + 8 wave + g + 32 k; a tile
+// is k = 2t, 2t + 1), whose earlier slices earlier passes wrote.  No
+// workgroup barrier after the Gather: a wave whose lane groups are done
+// goes on to its tiles while the others still gather.  A workgroup takes
+// kXfBpw row blocks, which fills the waves' tiles better (a block averages
+// about 74 rows at 2^21 vertices, 18 per wave).  Dynamic LDS: the packed
+// W^T (25 KB for 128 x 41 float32, which caps the kernel at six workgroups
+// per CU).
+constexpr int kXfBpw = 2;
+template <typename T, int U, int NT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_gather_sum_xf(
+    GatherArgs a, int slice0) {
+  extern __shared__ uint4 xf_wt[];
+  const int32_t* __restrict__ counts = a.counts;
+  if (counts[kErrFlags]) return;
+  const int nb = counts[kNumBlocks];
+  const int b = blockIdx.x * a.bpw;
+  if (b >= nb) return;
+  for (int i = threadIdx.x; i < NT * 16 * a.xldwt; i += kThreads) xf_wt[i] = a.xwt[i];
+  __syncthreads();
+  gather_simple_body<T, 8, 1, U, 4, false, kWNone, true, false, true>(a, 1, slice0);
+  // the lanes of this wave read rows other lanes of it stored
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  const int s_split = counts[kSSplit];
+  const int s0 = a.block_ptr[b], s1 = a.block_ptr[b + a.bpw < nb ? b + a.bpw : nb];
+  const int wave = threadIdx.x >> 6, lr = threadIdx.x & 15;
+  constexpr int NG = kThreads / 8;  // lane groups of the workgroup
+  for (int t0 = s0 + wave * 8; t0 < s1; t0 += 2 * NG) {
+    const int s = t0 + (lr & 7) + (lr >> 3) * NG;
+    xf_tile<T, NT>(a, s < s1 && s >= s_split ? a.seg_row[s] : -1, xf_wt);
+  }
+}
+
+// The transform of the split rows (perm positions 0 .. n_split - 1), whose
+// h rows k_combine has just finished.
+template <typename T, int NT>
+__global__ __launch_bounds__(kThreads) void k_xf_rows(GatherArgs a) {
+  extern __shared__ uint4 xf_wt[];
+  const int32_t* __restrict__ counts = a.counts;
+  if (counts[kErrFlags]) return;
+  const int n_split = counts[kNSplit];
+  if (blockIdx.x * (kThreads / 4) >= n_split) return;
+  for (int i = threadIdx.x; i < NT * 16 * a.xldwt; i += kThreads) xf_wt[i] = a.xwt[i];
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lr = threadIdx.x & 15;
+  for (int t0 = (blockIdx.x * (kThreads / 64) + wave) * 16; t0 < n_split;
+       t0 += gridDim.x * (kThreads / 4)) {
+    const int i = t0 + lr;
+    xf_tile<T, NT>(a, i < n_split ? a.perm[i] : -1, xf_wt);
+  }
+}
+
+// ------------------------------------------------------------------------
 // Unfused Scatter + ApplyEdge (the baseline of Fig. 7a): materialise the
 // edge tensor msg[e] = w(u) * src[u] for every edge e = (u -> v) in CSR
 // order, w(u) = d_out(u)^-1/2 for the GCN source norm, else 1.  One thread
@@ -863,6 +1030,66 @@ hipError_t launch_gather(const GatherArgs& a0, hipStream_t st) {
     err = hipGetLastError();
   }
   return err;
+}
+
+int64_t xf_pack_bytes(int64_t feat, int esize, int xn) {
+  return (int64_t)(xn + 15) / 16 * 16 * (feat * esize / 16 + 1) * 16;
+}
+
+namespace {
+
+template <typename T, int NT>
+hipError_t launch_xf(const GatherArgs& a, unsigned grid, int nslices, hipStream_t st) {
+  const size_t lds = (size_t)NT * 16 * a.xldwt * 16;
+  const unsigned pb = (unsigned)((NT * 16 * a.xldwt * Vec16<T>::N + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL((k_xf_pack<T>), dim3(pb), dim3(kThreads), 0, st, a, NT * 16);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // the earlier slices, one launch each; U as in the plain sliced Gather
+  constexpr int U = sizeof(T) == 2 ? 8 : 4;
+  for (int s0 = 0; s0 < nslices - 1; ++s0) {
+    hipLaunchKernelGGL((k_gather_sum<T, 8, 1, U, 4>), dim3(grid), dim3(kThreads), 0, st, a, 1, s0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  GatherArgs ax = a;
+  ax.bpw = a.bpw * kXfBpw;
+  const unsigned gx = (unsigned)(a.max_blocks > 0 ? (a.max_blocks + ax.bpw - 1) / ax.bpw : 1);
+  hipLaunchKernelGGL((k_gather_sum_xf<T, U, NT>), dim3(gx), dim3(kThreads), lds, st, ax,
+                     nslices - 1);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (a.max_split > 0) {
+    const unsigned cg = (unsigned)(a.max_split < 4096 ? a.max_split : 4096);
+    hipLaunchKernelGGL(k_combine<T>, dim3(cg), dim3(kThreads), 0, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int64_t tiles = (a.max_split + kThreads / 4 - 1) / (kThreads / 4);
+    hipLaunchKernelGGL((k_xf_rows<T, NT>), dim3((unsigned)(tiles < 1024 ? tiles : 1024)),
+                       dim3(kThreads), lds, st, a);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+template <typename T>
+hipError_t launch_xf_nt(const GatherArgs& a, unsigned grid, int nslices, hipStream_t st) {
+  switch ((a.xn + 15) / 16) {
+    case 1: return launch_xf<T, 1>(a, grid, nslices, st);
+    case 2: return launch_xf<T, 2>(a, grid, nslices, st);
+    case 3: return launch_xf<T, 3>(a, grid, nslices, st);
+    default: return launch_xf<T, 4>(a, grid, nslices, st);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gather_transform(const GatherArgs& a0, hipStream_t st) {
+  GatherArgs a = a0;
+  a.bpw = blocks_per_wg(a);
+  const unsigned grid = (unsigned)(a.max_blocks > 0 ? (a.max_blocks + a.bpw - 1) / a.bpw : 1);
+  const int esz = a.dtype == SAGA_BF16 ? 2 : 4;
+  const int nslices = (int)(a.feat * (int64_t)esz / 128);
+  a.xldwt = (int)(a.feat * esz / 16 + 1);
+  return a.dtype == SAGA_BF16 ? launch_xf_nt<uint16_t>(a, grid, nslices, st)
+                              : launch_xf_nt<float>(a, grid, nslices, st);
 }
 
 namespace {

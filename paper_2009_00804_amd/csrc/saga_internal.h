@@ -87,11 +87,26 @@ struct GatherArgs {
   const int32_t* err2;
   // added to every output row before the bias (nullable; dtype of out)
   const void* self; int64_t ld_self;
+  // fused next transform (xn > 0): the Gather's output h (in `out`, a
+  // workspace) is multiplied as rows finish: xout[v] = xrs(v) * (h_v xw),
+  // xw F x xn (dtype), columns from xsplit on (xsplit > 0) going to xtail
+  const void* xw; int xn; int xsplit;
+  // xw packed as W^T for the matrix cores (workspace): 16 * ceil(xn / 16)
+  // rows of xldwt 16-byte vectors (F columns, zero rows past xn, a 16-byte
+  // pad per row)
+  uint4* xwt; int xldwt;
+  void* xout; int64_t ld_xout;
+  void* xtail; int64_t ld_xtail;
+  const int32_t* xrs;
 };
 
 int gather_partial_cols(int64_t feat);
 size_t gather_partial_stride(const saga_edge_op& op, int64_t feat);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t st);
+// the fused Gather + next transform (COPY with SUM or MEAN, whole 128-byte
+// slices, at most four of them, xn <= 64); xf_pack_bytes: the packed W^T
+int64_t xf_pack_bytes(int64_t feat, int esize, int xn);
+hipError_t launch_gather_transform(const GatherArgs& a, hipStream_t st);
 // unfused baseline: materialise msg (E x ldm, CSR order), then reduce it
 hipError_t launch_unfused(const GatherArgs& a, int64_t E, void* msg, int64_t ldm, hipStream_t st);
 

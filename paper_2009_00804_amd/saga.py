@@ -36,7 +36,8 @@ ACT = {"none": 0, "relu": 1, "elu": 2, "sigmoid": 3, "tanh": 4}
 EXPORTS = [
     "saga_plan_workspace_size", "saga_plan_build", "saga_plan_build_split", "saga_plan_check",
     "saga_gather_workspace_size", "saga_scatter_apply_edge_gather",
-    "saga_scatter_apply_edge_gather_noalloc",
+    "saga_scatter_apply_edge_gather_noalloc", "saga_gather_transform_workspace_size",
+    "saga_scatter_apply_edge_gather_transform",
     "saga_unfused_workspace_size", "saga_scatter_gather_unfused",
     "saga_lstm_gather_workspace_size", "saga_lstm_gather", "saga_lstm_gather_rows",
     "saga_rel_plan_workspace_size", "saga_rel_plan_build", "saga_rel_plan_check",
@@ -106,6 +107,11 @@ class saga_edge_inputs(C.Structure):
                 ("self", saga_cmat)]
 
 
+class saga_next_transform(C.Structure):
+    _fields_ = [("w", saga_cmat), ("row_scale_deg", C.c_void_p), ("split_col", C.c_int32),
+                ("tail", saga_mat)]
+
+
 class saga_gemm_op(C.Structure):
     _fields_ = [("dtype", C.c_int), ("mode", C.c_int), ("act", C.c_int),
                 ("row_scale_deg", C.c_void_p), ("split_col", C.c_int32), ("tail", saga_mat)]
@@ -149,6 +155,11 @@ def lib():
                                                C.c_void_p, C.c_size_t, C.c_void_p]),
         "saga_scatter_apply_edge_gather_noalloc": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs),
                                                        saga_mat, C.c_void_p]),
+        "saga_gather_transform_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64,
+                                                     P(C.c_size_t)]),
+        "saga_scatter_apply_edge_gather_transform": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs),
+                                                         P(saga_next_transform), saga_mat, C.c_void_p,
+                                                         C.c_size_t, C.c_void_p]),
         "saga_unfused_workspace_size": (S, [P(saga_plan), P(saga_edge_op), C.c_int64, P(C.c_size_t)]),
         "saga_scatter_gather_unfused": (S, [P(saga_plan), P(saga_edge_op), P(saga_edge_inputs), saga_mat,
                                             C.c_void_p, C.c_size_t, C.c_void_p]),
@@ -251,6 +262,19 @@ def saga_scatter_apply_edge_gather_noalloc(plan, op, inputs, out, stream):
     return _check(lib().saga_scatter_apply_edge_gather_noalloc(C.byref(plan), C.byref(op), C.byref(inputs),
                                                                out, stream),
                   "saga_scatter_apply_edge_gather_noalloc")
+
+
+def saga_gather_transform_workspace_size(plan, op, feat):
+    out = C.c_size_t(0)
+    _check(lib().saga_gather_transform_workspace_size(C.byref(plan), C.byref(op), feat, C.byref(out)),
+           "saga_gather_transform_workspace_size")
+    return out.value
+
+
+def saga_scatter_apply_edge_gather_transform(plan, op, inputs, nxt, out, workspace, ws_bytes, stream):
+    return _check(lib().saga_scatter_apply_edge_gather_transform(
+        C.byref(plan), C.byref(op), C.byref(inputs), C.byref(nxt), out, workspace, ws_bytes, stream),
+        "saga_scatter_apply_edge_gather_transform")
 
 
 def saga_unfused_workspace_size(plan, op, feat):

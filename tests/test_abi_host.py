@@ -160,6 +160,37 @@ def test_trace_stages_rejects_bad_arguments(S):
     assert L.saga_trace_stages(None, 0, 0) == S.SAGA_OK         # tracing off
 
 
+def test_gather_transform_rejects_unsupported_shapes(S):
+    p = _fake_plan(S)
+    L = S.lib()
+    inp = S.saga_edge_inputs()
+    inp.src = S.saga_cmat(0x50000, 16, 32, 32)          # one 128-byte line of float32
+    nx = S.saga_next_transform()
+    nx.w = S.saga_cmat(0x70000, 32, 8, 8)
+    out = S.saga_mat(0x40000, 16, 8, 8)
+    ws, wsb = C.c_void_p(0x100000), 1 << 20
+
+    def call(op, ou=out):
+        return L.saga_scatter_apply_edge_gather_transform(C.byref(p), C.byref(op), C.byref(inp),
+                                                          C.byref(nx), ou, ws, wsb, None)
+
+    sum_op = S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_SUM, S.SAGA_F32, 1, 0, 0, 0.2, 0)
+    assert call(S.saga_edge_op(S.SAGA_MSG_COPY, S.SAGA_RED_MAX, S.SAGA_F32, 1, 0, 0, 0.2, 0)) \
+        == S.SAGA_EUNSUPPORTED
+    inp.src = S.saga_cmat(0x50000, 16, 24, 24)           # not whole 128-byte lines
+    assert call(sum_op) == S.SAGA_EUNSUPPORTED
+    inp.src = S.saga_cmat(0x50000, 16, 32, 32)
+    nx.w = S.saga_cmat(0x70000, 32, 65, 65)               # more than 64 outputs
+    assert call(sum_op, ou=S.saga_mat(0x40000, 16, 65, 68)) == S.SAGA_EUNSUPPORTED
+    nx.w = S.saga_cmat(0x70000, 32, 8, 12)                # weights not dense
+    assert call(sum_op) == S.SAGA_EINVAL
+    nx.w = S.saga_cmat(0x70000, 32, 8, 8)
+    nx.split_col = 2                                      # split inside a 16-byte vector
+    assert call(sum_op, ou=S.saga_mat(0x40000, 16, 2, 4)) == S.SAGA_EINVAL
+    nx.split_col = 0
+    assert call(sum_op, ou=S.saga_mat(0x70000 + 16, 16, 8, 8)) == S.SAGA_EINVAL   # out on w
+
+
 def test_unfused_rejects_bad_arguments(S):
     """The unfused baseline: unsupported ops, workspace size, alignment and
     overlap are all rejected on the host before any launch."""

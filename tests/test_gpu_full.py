@@ -221,3 +221,56 @@ def test_full_bench_step_sampled(big, dtype, split):
     assert e2t <= tol
     del step
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_full_bench_step_fused_sampled(big, dtype):
+    """The benchmark's step with layer 2's transform fused into layer 1's
+    Gather (and the plan's row order on a second stream): layer 2's
+    transformed rows Z2 = d_out^-1/2 (H1 W2) on sampled rows (hubs and split
+    rows, whose transform runs in the combine, included) against the
+    oracle's layer 1 and product, and the two-layer output on rows with small
+    two-hop neighbourhoods."""
+    import bench
+
+    g = big
+    if dtype == "bf16":
+        C.add_bf16_variant(g)
+        Xo = T.bf16_to_f32(g["X_bf16"][:, :g["dims"][0]])
+        W1, W2, tol = g["W1_bf"], g["W2_bf"], BF16_TOL
+    else:
+        Xo = g["X"][:, :g["dims"][0]]
+        W1, W2, tol = g["W1"], g["W2"], FP32_TOL
+    step = bench.Step(g, dtype, torch.device("cuda:0"))
+    step.split = True
+    step.fused = True
+    print(f"bench step ({dtype}, pipelined, fused) on the GPU", flush=True)
+    step.run()
+    torch.cuda.synchronize()
+    y = step.Y.clone()
+    z2 = torch.cat([step.Z2, step.Z2t], dim=1) if step.split2 else step.Z2
+    z2 = z2.clone()
+    step.run()
+    torch.cuda.synchronize()
+    assert torch.equal(y, step.Y)                  # deterministic bytes
+    rp, col = g["row_ptr"], g["col_idx"]
+    rows = _samples(g, seed=6)
+    print(f"oracle layer 1 and the layer-2 product on {len(rows)} sampled rows", flush=True)
+    h1 = O.gcn_layer(rp, col, Xo, W1, g["b1"], "relu", rows=rows)
+    s_out = O.degree_scale(O.out_degrees(col, g["num_vertices"]))[rows]
+    ref_z = O.dense(h1, W2) * s_out[:, None]
+    mag_z = O.dense(np.abs(_layer_mag(rp, col, Xo, W1, g["b1"], rows)), np.abs(W2)) * s_out[:, None]
+    got_z = to_np(z2[torch.from_numpy(rows).cuda()])
+    ez, ezt = rel_err(got_z, ref_z), rel_err_terms(got_z, ref_z, mag_z)
+    rows2 = _small_two_hop(g, seed=7)
+    print(f"oracle two layers on {len(rows2)} sampled rows", flush=True)
+    ref2 = O.gcn_2layer(dict(g, X=Xo), X=Xo, W1=W1, W2=W2, rows=rows2)
+    got2 = to_np(y[torch.from_numpy(rows2).cuda()])
+    e2 = rel_err(got2, ref2)
+    e2t = rel_err_terms(got2, ref2, _model_mag(g, Xo, W1, W2, rows2))
+    print(f"{dtype} fused: Z2 err {ez:.3e} (terms {ezt:.3e}), two-layer err {e2:.3e} "
+          f"(terms {e2t:.3e})", flush=True)
+    assert ez <= tol and ezt <= tol
+    assert e2 <= tol and e2t <= tol
+    del step
+    torch.cuda.empty_cache()

@@ -486,3 +486,70 @@ def test_gather_maximum_widths(dtype, F):
     wider = dev_padded(np.zeros((n, limit + 1), np.float32), tdt)
     with pytest.raises(S.SagaError):
         run_gather(g, wider, dict(reduce=S.SAGA_RED_SUM), limit + 1, tdt)
+
+
+def _transform_ref(rp, col, X, red, dn, bias, act, n, W, rs_deg):
+    """out[v] = rs(v) * (h_v W) with h the Gather output (the fused call's
+    definition), from the oracle's Gather and a float64 product."""
+    h = _ref_simple(rp, col, X, red, "copy", dn, bias, act, n)
+    rs = O.degree_scale(rs_deg) if rs_deg is not None else np.ones(n)
+    return O.dense(h, W) * rs[:, None], h
+
+
+@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_random"])
+@pytest.mark.parametrize("dtype,F,N,split", [("f32", 128, 41, 32), ("f32", 32, 8, 0), ("f32", 64, 64, 0),
+                                             ("bf16", 128, 41, 0), ("bf16", 64, 16, 8)])
+def test_gather_transform_fused(gname, dtype, F, N, split):
+    """The Gather with the next layer's transform fused into its last slice
+    pass: against the oracle's definition (Gather, then the product with the
+    row scale), and against the two separate calls it replaces."""
+    S = lib()
+    rp, col, n, g = _get_graph(gname)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rng = np.random.default_rng(60 + F + N)
+    X = rng.standard_normal((n, F)).astype(np.float32)
+    W = (rng.standard_normal((F, N)) / np.sqrt(F)).astype(np.float32)
+    if dtype == "bf16":
+        X, W = _bf16_round(X), _bf16_round(W)
+    bias = rng.standard_normal(F)
+    tol = FP32_TOL if dtype == "f32" else BF16_TOL
+    d_out = O.out_degrees(col, n)
+    dout_t = torch.from_numpy(d_out.astype(np.int32)).to(device())
+    Xt, Wt = dev_padded(X, tdt), torch.from_numpy(W).to(tdt).to(device()).contiguous()
+    b_t = torch.from_numpy(bias.astype(np.float32)).to(device())
+    for red, dn, act, rsd in (("sum", 1, "relu", d_out), ("mean", 0, "none", None)):
+        print(f"gather+transform {gname} {dtype} F={F} N={N} split={split} {red}", flush=True)
+        op = S.saga_edge_op(S.SAGA_MSG_COPY, {"sum": S.SAGA_RED_SUM, "mean": S.SAGA_RED_MEAN}[red],
+                            S.dtype_code(tdt), 1, 0, dn, 0.0, ACTS[act])
+        inp = S.saga_edge_inputs()
+        inp.src = S.cmat(Xt)
+        inp.bias = b_t.data_ptr()
+        head = split if split else N
+        out = dev_padded(np.zeros((n, head)), dtype=tdt, fill=7.0)
+        tail = dev_padded(np.zeros((n, N - split)), dtype=tdt, fill=7.0) if split else None
+        nx = S.saga_next_transform()
+        nx.w = S.cmat(Wt)
+        nx.row_scale_deg = dout_t.data_ptr() if rsd is not None else None
+        nx.split_col = split
+        if split:
+            nx.tail = S.mat(tail)
+        ws = S.workspace(S.saga_gather_transform_workspace_size(g.plan, op, F), device())
+        S.saga_scatter_apply_edge_gather_transform(g.plan, op, inp, nx, S.mat(out),
+                                                   C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
+        torch.cuda.synchronize()
+        got = to_np(out) if not split else np.concatenate([to_np(out), to_np(tail)], axis=1)
+        ref, h = _transform_ref(rp, col, X, red, dn, bias, act, n, W, rsd)
+        mag = O.dense(np.abs(h), np.abs(W)) * (O.degree_scale(rsd)[:, None] if rsd is not None else 1.0)
+        assert rel_err(got, ref) <= tol
+        assert rel_err_terms(got, ref, mag) <= tol
+        # the two calls it replaces: Gather, then the transform on the stored h
+        hh = run_gather(g, Xt, dict(reduce=op.reduce, dst_norm=dn, act=act), F, tdt, bias=bias)
+        gop = S.saga_gemm_op(S.dtype_code(tdt), S.SAGA_GEMM_PLAIN, S.SAGA_ACT_NONE,
+                             dout_t.data_ptr() if rsd is not None else None)
+        y2 = dev_padded(np.zeros((n, N)), dtype=tdt)
+        gws = S.workspace(S.saga_apply_vertex_workspace_size(gop, F, 0, N), device())
+        none = S.saga_cmat(None, 0, 0, 0)
+        S.saga_apply_vertex(gop, S.cmat(hh), S.cmat(Wt), none, none, None, None, S.mat(y2),
+                            C.c_void_p(gws.data_ptr()), gws.numel(), S.stream_handle())
+        torch.cuda.synchronize()
+        assert rel_err(got, to_np(y2)) <= tol
