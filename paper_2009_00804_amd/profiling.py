@@ -15,6 +15,12 @@ Usage:
   python -m paper_2009_00804_amd.profiling --trace DIR --fetch DIR --write DIR \\
       --copy-mib 1024 --dtype f32 --command "..." --out profiles
 
+Counter mode: any other --pmc passes of the same bench.py command,
+summarised per stage with derived figures (L2 hit rate, L1->L2 latency and
+reads in flight, MFMA busy):
+  python -m paper_2009_00804_amd.profiling --counters DIR1,DIR2 --dtype f32 \\
+      --command "..." --passes "..." --out profiles
+
 Suite mode (the other workloads, stage by stage): bench.py run with
 ``--suite-schedule FILE`` launches the library's stage markers
 (k_stage_begin, k_stage_mark) around every stage of its traced layer calls
@@ -69,6 +75,7 @@ STAGES = {
 def _short(name):
     name = name.replace("void saga::(anonymous namespace)::", "")
     name = name.replace("saga::(anonymous namespace)::", "")
+    name = name.replace("(anonymous namespace)::", "")
     return re.sub(r"\((saga::|int|long|unsigned).*$", "", name)
 
 
@@ -209,6 +216,122 @@ def suite_main(a):
         json.dump(rec, f, indent=1, sort_keys=True)
 
 
+def all_counter_lists(counter_dir):
+    """{counter: {short kernel name: [value per dispatch, ...]}} in dispatch
+    order, every counter of one --pmc pass."""
+    rows = list(csv.DictReader(open(_csv(counter_dir, "counter_collection.csv"))))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    acc = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in rows:
+        acc[r["Counter_Name"]][_short(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+    return acc
+
+
+# derived figures of a stage from its per-launch counter sums: (label,
+# numerator, denominator terms, scale).  GRBM_GUI_ACTIVE reads the sum over
+# the 8 XCDs (8 x the kernel's cycles: about 8.5e7 for a 4.7 ms launch at
+# 2.4 GHz), the TCP counters the sum over the 256 CUs' L1s and
+# SQ_VALU_MFMA_BUSY_CYCLES the sum over the 1,024 SIMDs, so "per CU" divides
+# by 256 x GRBM_GUI_ACTIVE / 8 and "per SIMD" by 1,024 x GRBM_GUI_ACTIVE / 8.
+NUM_XCD, NUM_CU, NUM_SIMD = 8, 256, 1024
+DERIVED = [
+    ("L2 hit rate", "TCC_HIT_sum", ("TCC_HIT_sum", "TCC_MISS_sum"), 1.0),
+    ("L1->L2 read latency, cycles per request", "TCP_TCC_READ_REQ_LATENCY_sum",
+     ("TCP_TCC_READ_REQ_sum",), 1.0),
+    ("L1->L2 reads in flight per CU", "TCP_TCC_READ_REQ_LATENCY_sum", ("GRBM_GUI_ACTIVE",),
+     NUM_XCD / NUM_CU),
+    ("fraction of CU cycles with L1 misses pending (stalled)", "TCP_PENDING_STALL_CYCLES_sum",
+     ("GRBM_GUI_ACTIVE",), NUM_XCD / NUM_CU),
+    ("MFMA busy fraction per SIMD", "SQ_VALU_MFMA_BUSY_CYCLES", ("GRBM_GUI_ACTIVE",),
+     NUM_XCD / NUM_SIMD),
+    ("LDS bank conflicts per LDS instruction", "SQ_LDS_BANK_CONFLICT", ("SQ_INSTS_LDS",), 1.0),
+]
+
+
+def counters_main(a):
+    """Per-stage counter summary of --pmc passes over the benchmark step."""
+    per_stage = collections.defaultdict(dict)
+    names = []
+    for d in a.counters.split(","):
+        for cname, by_kernel in all_counter_lists(d).items():
+            if cname in names:
+                continue
+            names.append(cname)
+            for stage, (pats, _src) in STAGES.items():
+                total, ok = 0.0, True
+                for pat, per, cycle, slots in pats[a.dtype]:
+                    keys = [k for k in by_kernel if k.startswith(pat)]
+                    if len(keys) != 1:
+                        ok = False
+                        break
+                    v = [x for i, x in enumerate(by_kernel[keys[0]]) if i % cycle in slots]
+                    if not v:
+                        ok = False
+                        break
+                    total += per * sum(v) / len(v)
+                if ok:
+                    per_stage[stage][cname] = total
+    lines = [f"# Counters per stage launch: {a.tag} ({a.dtype})", "",
+             f"command: {a.command} (one run per pass; passes: {a.passes})", "",
+             "Each value is the counter's per-dispatch average over the run, summed over",
+             "the dispatches one launch of the stage makes (the kernel-to-stage rules",
+             "are profiling.STAGES).", ""]
+    for stage in STAGES:
+        if stage not in per_stage:
+            continue
+        c = per_stage[stage]
+        lines.append(f"## {stage}")
+        for cname in names:
+            if cname in c:
+                lines.append(f"  {cname:36s} {c[cname]:16.4g}")
+        for label, num, den, scale in DERIVED:
+            if num in c and all(d in c for d in den):
+                dv = sum(c[d] for d in den)
+                if dv > 0:
+                    lines.append(f"  = {label}: {scale * c[num] / dv:.4g}")
+        lines.append("")
+    with open(os.path.join(a.out, f"counters_{a.tag}_{a.dtype}.txt"), "w") as f:
+        f.write("\n".join(lines))
+
+
+def suite_counters_main(a):
+    """Per-stage counter summary of --pmc passes over the suite's traced
+    layer calls (stage markers on), with the derived figures of DERIVED."""
+    schedule = json.load(open(a.suite))
+    ncalls = {w["workload"]: w["calls"] for w in schedule}
+    per, kern, names = collections.defaultdict(dict), {}, []
+    for d in a.counters.split(","):
+        for cname in sorted(all_counter_lists(d)):
+            if cname in names:
+                continue
+            names.append(cname)
+            acc, k = attribute(dispatches(d, cname), schedule)
+            for key, v in acc.items():
+                per[key][cname] = v / ncalls[key[0]]
+                kern.setdefault(key, k[key])
+    order = [w["workload"] for w in schedule]
+    lines = ["# Counters per stage: the suite workloads (float32)", "",
+             f"command: {a.command} (one run per pass; passes: {a.passes})", "",
+             "Each value is the stage's counter total over one layer call (the sum over",
+             "the dispatches between the library's stage markers, averaged over the",
+             "traced calls); derived figures as in the benchmark step's summary.", ""]
+    for key in sorted(per, key=lambda k: (order.index(k[0]), k[1])):
+        wl, li, stage = key
+        c = per[key]
+        lines.append(f"## {wl} layer {li}: {stage}  ({', '.join(sorted(x[:40] for x in kern[key]))})")
+        for cname in names:
+            if cname in c:
+                lines.append(f"  {cname:36s} {c[cname]:16.4g}")
+        for label, num, den, scale in DERIVED:
+            if num in c and all(x in c for x in den):
+                dv = sum(c[x] for x in den)
+                if dv > 0:
+                    lines.append(f"  = {label}: {scale * c[num] / dv:.4g}")
+        lines.append("")
+    with open(os.path.join(a.out, "counters_suite_f32.txt"), "w") as f:
+        f.write("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace")
@@ -220,10 +343,14 @@ def main():
     ap.add_argument("--command", default="")
     ap.add_argument("--out", default="profiles")
     ap.add_argument("--tag", default="gcn_rmat21")
+    ap.add_argument("--counters", help="comma-separated --pmc output directories (counter mode)")
+    ap.add_argument("--passes", default="", help="the counters of each pass, for the header")
     a = ap.parse_args()
     os.makedirs(a.out, exist_ok=True)
     if a.suite:
-        return suite_main(a)
+        return suite_counters_main(a) if a.counters else suite_main(a)
+    if a.counters:
+        return counters_main(a)
 
     st = kernel_stats(a.trace)
     tot = sum(v[2] for v in st.values())

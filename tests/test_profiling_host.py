@@ -28,3 +28,51 @@ def test_attribution_refuses_a_profile_that_disagrees_with_the_schedule():
         P.attribute(one_call, sched)
     with pytest.raises(ValueError):
         P.attribute(one_call * 3, sched)
+
+
+def test_counter_summary_sums_a_stages_dispatches_by_slot(tmp_path):
+    """Counter mode: gather1 (fp32) is dispatches 0-3 of every five of the
+    sliced-sum kernel plus the first of every three combines; its derived
+    figures come from the per-launch sums."""
+    import csv
+    import types
+    names = (["k_gather_sum<float, 8, 1, 4, 4>(saga::GatherArgs, int, int)"] * 5
+             + ["k_combine<float>(saga::GatherArgs)"] * 3)
+    rows, did = [], 0
+    for _ in range(2):
+        for i, n in enumerate(names):
+            did += 1
+            hit = 30.0 if i < 4 else (5.0 if n.startswith("k_gather") else 1.0)
+            for c, v in (("TCC_HIT_sum", hit), ("TCC_MISS_sum", 10.0), ("GRBM_GUI_ACTIVE", 1000.0),
+                         ("TCP_TCC_READ_REQ_sum", 100.0), ("TCP_TCC_READ_REQ_LATENCY_sum", 54500.0)):
+                rows.append({"Dispatch_Id": did, "Kernel_Name": n, "Counter_Name": c,
+                             "Counter_Value": v})
+    d = tmp_path / "p1"
+    d.mkdir()
+    with open(d / "run_counter_collection.csv", "w") as f:
+        w = csv.DictWriter(f, fieldnames=list(rows[0]))
+        w.writeheader()
+        w.writerows(rows)
+    a = types.SimpleNamespace(counters=str(d), dtype="f32", command="cmd", passes="p", out=str(tmp_path),
+                              tag="t")
+    P.counters_main(a)
+    text = (tmp_path / "counters_t_f32.txt").read_text()
+    g1 = text.split("## gather1")[1].split("##")[0]
+    # four sliced passes at 30 hits + one combine at 1 hit; five dispatches of misses
+    assert "TCC_HIT_sum" in g1 and " 121\n" in g1
+    assert "= L2 hit rate: %.4g" % (121 / 171) in g1
+    assert "= L1->L2 read latency, cycles per request: 545" in g1
+    assert "= L1->L2 reads in flight per CU: %.4g" % (8 * 5 * 54500 / (5 * 1000 * 256)) in g1
+    # gather2 takes the fifth sliced pass (5 hits) and combines 1 and 2, but
+    # its 9-column kernel is absent from this profile: no gather2 section
+    assert "## gather2" not in text
+
+
+def test_short_names_drop_namespaces_and_arguments():
+    """The library's stage markers live in an anonymous namespace of their
+    own (not saga's): their short names must still be the bare kernel names
+    the attribution looks for."""
+    assert P._short("(anonymous namespace)::k_stage_begin()") == "k_stage_begin()"
+    assert P._short("saga::(anonymous namespace)::k_stage_mark()").startswith("k_stage_mark")
+    assert P._short("void saga::(anonymous namespace)::k_combine<float>(saga::GatherArgs)") == \
+        "k_combine<float>"
