@@ -60,13 +60,14 @@ struct ArrF {
   const int32_t* p;
   __device__ int32_t operator()(int64_t i) const { return p[i]; }
 };
-// number of segments of perm position i
+// the in-degree behind a degree-order sort key (key = 0x7fffffff - d_in)
+__device__ __forceinline__ int32_t key_degree(uint32_t key) { return (int32_t)(0x7fffffffu - key); }
+// number of segments of perm position i, from the sorted keys
 struct NsegF {
-  const int32_t* d_in;
-  const int32_t* perm;
+  const uint32_t* keys;
   int32_t T;
   __device__ int32_t operator()(int64_t i) const {
-    int32_t d = d_in[perm[i]];
+    const int32_t d = key_degree(keys[i]);
     return d > T ? (d + T - 1) / T : 1;
   }
 };
@@ -397,12 +398,15 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(const int32_t* __restri
 // item j*256 + t); an item's rank among equal digits inside the tile comes
 // from a wave-level match (8 ballots) plus the counts of lower waves and of
 // earlier rounds, so equal keys keep their input order.
-template <bool FIRST, bool LAST>
+// Each item carries a second value, its row's first CSR entry (row_ptr[v]
+// on the first pass), so that the segment builder reads it in perm order
+// instead of gathering row_ptr at random.
+template <bool FIRST>
 __global__ __launch_bounds__(kThreads) void k_radix_scatter(
     const int32_t* __restrict__ d_in, const uint32_t* __restrict__ keys_in,
-    const int32_t* __restrict__ vals_in, int32_t n, int shift,
+    const int32_t* __restrict__ vals_in, const int32_t* __restrict__ rb_in, int32_t n, int shift,
     const int32_t* __restrict__ offsets, int64_t ntiles, uint32_t* __restrict__ keys_out,
-    int32_t* __restrict__ vals_out, const int32_t* counts) {
+    int32_t* __restrict__ vals_out, int32_t* __restrict__ rb_out, const int32_t* counts) {
   if (counts[kErrFlags]) return;
   __shared__ int32_t running[kBins];
   __shared__ int32_t wcnt[kThreads / 64][kBins];
@@ -418,11 +422,12 @@ __global__ __launch_bounds__(kThreads) void k_radix_scatter(
     const int64_t i = tile * kTile + j * kThreads + t;
     const bool valid = i < n;
     uint32_t key = 0;
-    int32_t val = 0;
+    int32_t val = 0, rb = 0;
     int dg = 0;
     if (valid) {
       key = FIRST ? (0x7fffffffu - (uint32_t)d_in[i]) : keys_in[i];
       val = FIRST ? (int32_t)i : vals_in[i];
+      rb = rb_in[i];
       dg = (key >> shift) & (kBins - 1);
     }
     uint64_t m = __ballot(valid);
@@ -439,8 +444,9 @@ __global__ __launch_bounds__(kThreads) void k_radix_scatter(
       int32_t pos = running[dg] + rank;
       for (int k = 0; k < w; ++k) pos += wcnt[k][dg];
       if (pos >= 0 && pos < n) {
-        if (!LAST) keys_out[pos] = key;
+        keys_out[pos] = key;
         vals_out[pos] = val;
+        rb_out[pos] = rb;
       } else {
         atomicOr(const_cast<int32_t*>(counts) + kErrFlags, kErrInternal);
       }
@@ -519,8 +525,8 @@ __global__ __launch_bounds__(kThreads) void k_scan_apply(F f, int64_t n_host,
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_segments(const int32_t* __restrict__ rp,
-                                                       const int32_t* __restrict__ d_in,
+__global__ __launch_bounds__(kThreads) void k_segments(const uint32_t* __restrict__ keys,
+                                                       const int32_t* __restrict__ rbeg,
                                                        const int32_t* __restrict__ perm,
                                                        const int32_t* __restrict__ first,
                                                        int32_t V, int32_t T, int64_t max_seg,
@@ -534,14 +540,14 @@ __global__ __launch_bounds__(kThreads) void k_segments(const int32_t* __restrict
       atomicOr(&counts[kErrFlags], kErrInternal);
       return;
     }
-    const int32_t d = d_in[v];
+    const int32_t d = key_degree(keys[i]);
     const int32_t f = first[i];
     const int32_t ns = d > T ? (d + T - 1) / T : 1;
     if (f < 0 || (int64_t)f + ns > max_seg) {
       atomicOr(&counts[kErrFlags], kErrInternal);
       return;
     }
-    const int32_t b0 = rp[v], e0 = rp[v + 1];
+    const int32_t b0 = rbeg[i], e0 = b0 + d;
     for (int32_t j = 0; j < ns; ++j) {
       const int32_t b = b0 + j * T;
       seg_row[f + j] = v;
@@ -549,7 +555,7 @@ __global__ __launch_bounds__(kThreads) void k_segments(const int32_t* __restrict
       seg_end[f + j] = (e0 - b) > T ? b + T : e0;
     }
     const bool split = d > T;
-    const bool next_split = (i + 1 < V) && d_in[perm[i + 1]] > T;
+    const bool next_split = (i + 1 < V) && key_degree(keys[i + 1]) > T;
     if (split && !next_split) {
       counts[kNSplit] = (int32_t)(i + 1);
       counts[kSSplit] = f + ns;
@@ -644,9 +650,9 @@ bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t
   L->off_block_ptr = take(L->max_blocks + 1);
   L->off_counts = take(kCountSlots);
   L->off_scratch = o;
-  // scratch: keysA, valsA, keysB, valsB, hist, tile sums, cost prefix,
-  // bucketed source ids, bucket histogram
-  take(V); take(V); take(V); take(V);
+  // scratch: keysA, valsA, keysB, valsB, row begins A and B, hist, tile
+  // sums, cost prefix, bucketed source ids, bucket histogram
+  take(V); take(V); take(V); take(V); take(V); take(V);
   take(hist_n);
   take(scan_tiles + 1);
   take(L->outdeg_bucketed ? scan_tiles + 1 : 0);  // tile sums of the out-degree branch
@@ -674,6 +680,8 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   int32_t* valsA = reinterpret_cast<int32_t*>(take(V));
   uint32_t* keysB = reinterpret_cast<uint32_t*>(take(V));
   int32_t* valsB = reinterpret_cast<int32_t*>(take(V));
+  int32_t* rbA = reinterpret_cast<int32_t*>(take(V));
+  int32_t* rbB = reinterpret_cast<int32_t*>(take(V));
   const int64_t ntiles = L.radix_tiles;
   int32_t* hist = reinterpret_cast<int32_t*>(take((int64_t)kBins * ntiles));
   int64_t scan_tiles = cdiv((int64_t)kBins * ntiles, kTile);
@@ -733,11 +741,14 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   }
   st = qst;  // the row order
 
-  // degree order: 4 stable passes of 8 bits over key = 0x7fffffff - d_in
+  // degree order: 4 stable passes of 8 bits over key = 0x7fffffff - d_in;
+  // the sorted keys end in keysB, the row begins in rbB
   const uint32_t* kin[4] = {nullptr, keysA, keysB, keysA};
   const int32_t* vin[4] = {nullptr, valsA, valsB, valsA};
-  uint32_t* kout[4] = {keysA, keysB, keysA, nullptr};
+  const int32_t* rin[4] = {p.row_ptr, rbA, rbB, rbA};
+  uint32_t* kout[4] = {keysA, keysB, keysA, keysB};
   int32_t* vout[4] = {valsA, valsB, valsA, p.perm};
+  int32_t* rout[4] = {rbA, rbB, rbA, rbB};
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 8 * pass;
     if (pass == 0)
@@ -748,25 +759,20 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
                          kin[pass], V, shift, hist, ntiles, p.counts);
     scan(ArrF{hist}, (int64_t)kBins * ntiles, nullptr, hist, nullptr, tile_sums, p.counts, st);
     if (pass == 0)
-      hipLaunchKernelGGL((k_radix_scatter<true, false>), dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st,
-                         p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
-                         vout[pass], p.counts);
-    else if (pass < 3)
-      hipLaunchKernelGGL((k_radix_scatter<false, false>), dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st,
-                         p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
-                         vout[pass], p.counts);
+      hipLaunchKernelGGL((k_radix_scatter<true>), dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st,
+                         p.d_in, kin[pass], vin[pass], rin[pass], V, shift, hist, ntiles,
+                         kout[pass], vout[pass], rout[pass], p.counts);
     else
-      hipLaunchKernelGGL((k_radix_scatter<false, true>), dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st,
-                         p.d_in, kin[pass], vin[pass], V, shift, hist, ntiles, kout[pass],
-                         vout[pass], p.counts);
+      hipLaunchKernelGGL((k_radix_scatter<false>), dim3(xcd_grid(ntiles)), dim3(kThreads), 0, st,
+                         p.d_in, kin[pass], vin[pass], rin[pass], V, shift, hist, ntiles,
+                         kout[pass], vout[pass], rout[pass], p.counts);
   }
 
   // segments per row in perm order -> row_seg_first (total at [V])
-  scan(NsegF{p.d_in, p.perm, T}, V, nullptr, p.row_seg_first, p.row_seg_first + V, tile_sums,
-       p.counts, st);
-  hipLaunchKernelGGL(k_segments, dim3(grid_for(V)), dim3(kThreads), 0, st, p.row_ptr, p.d_in,
-                     p.perm, p.row_seg_first, V, T, L.max_segments, p.seg_row, p.seg_beg,
-                     p.seg_end, p.counts);
+  scan(NsegF{keysB, T}, V, nullptr, p.row_seg_first, p.row_seg_first + V, tile_sums, p.counts, st);
+  hipLaunchKernelGGL(k_segments, dim3(grid_for(V)), dim3(kThreads), 0, st, keysB, rbB, p.perm,
+                     p.row_seg_first, V, T, L.max_segments, p.seg_row, p.seg_beg, p.seg_end,
+                     p.counts);
   // cost prefix over segments -> row blocks
   scan(CostF{p.seg_beg, p.seg_end, p.row_cost}, L.max_segments, p.counts + kNumSegments, P,
        nullptr, tile_sums, p.counts, st);
