@@ -356,8 +356,9 @@ saga_status saga_rel_transform(const saga_rel_plan* rel, saga_dtype dtype, saga_
  * added before the bias: out[v] = act(post(agg_v) + self[v] + bias).
  * Output: num_dst x F (x F/heads if head_mean), same dtype as src.
  * Supported: COPY/SRC_NORM with SUM/MEAN/MAX in f32 and bf16, GAT with
- * SOFTMAX in f32, GATED with SUM in f32, TYPED with SUM in f32 and bf16;
- * others give SAGA_EUNSUPPORTED.
+ * SOFTMAX in f32, GATED with SUM in f32, TYPED with SUM in f32 and bf16,
+ * F <= 1024 (GAT: F <= 256, GATED: F == 64); others give
+ * SAGA_EUNSUPPORTED.
  */
 typedef struct saga_edge_op {
   saga_msg msg;

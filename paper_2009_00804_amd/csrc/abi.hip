@@ -156,8 +156,8 @@ saga_status validate_edge_op(const saga_plan& p, const saga_edge_op& op,
   if (op.dtype != SAGA_F32 && op.dtype != SAGA_BF16) return fail(SAGA_EINVAL, "bad dtype");
   if (op.act < SAGA_ACT_NONE || op.act > SAGA_ACT_TANH) return fail(SAGA_EINVAL, "bad activation");
   if (F <= 0) return fail(SAGA_EINVAL, "src: no feature columns");
-  if (F > (op.dtype == SAGA_BF16 ? 1024 : 512))
-    return fail(SAGA_EUNSUPPORTED, "feature width %lld too large", (long long)F);
+  // the split-row combine holds a row of at most 1024 columns
+  if (F > 1024) return fail(SAGA_EUNSUPPORTED, "feature width %lld too large", (long long)F);
   int64_t src_rows = p.num_src;
   if (op.msg == SAGA_MSG_TYPED) {
     saga_status s0 = check_rel(p, in.rel);

@@ -971,6 +971,9 @@ hipError_t launch_simple(const GatherArgs& a, int nv, unsigned blocks, hipStream
     }
 #endif
   }
+  // rows past 2 KB (64 lanes x 2 vectors): 128-byte slices, the last one
+  // ragged (its lanes past the row end load nothing)
+  if (nv > 128) return launch_simple_lpr<T, 8, 1>(a, blocks, (nv + 7) / 8, st);
   if (nv > 64) return launch_simple_lpr<T, 64, 2>(a, blocks, 1, st);
   switch (next_pow2(nv)) {
     case 1: return launch_simple_lpr<T, 1, 1>(a, blocks, 1, st);
@@ -1098,6 +1101,7 @@ namespace {
 // (the tensor is streamed once, so no slicing for cache reuse)
 template <typename T>
 hipError_t launch_ident(const GatherArgs& a, int nv, unsigned blocks, hipStream_t st) {
+  if (nv > 128) return launch_simple_lpr<T, 8, 1>(a, blocks, (nv + 7) / 8, st);
   if (nv > 64) return launch_simple_lpr<T, 64, 2>(a, blocks, 1, st);
   switch (next_pow2(nv)) {
     case 1: return launch_simple_lpr<T, 1, 1>(a, blocks, 1, st);

@@ -461,10 +461,12 @@ def test_gemm_split_output_equals_single_output(dtype, N, split, K, aligned):
                             C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
 
 
-@pytest.mark.parametrize("dtype,F", [("f32", 512), ("bf16", 1024), ("f32", 508), ("bf16", 1000)])
+@pytest.mark.parametrize("dtype,F", [("f32", 512), ("bf16", 1024), ("f32", 508), ("bf16", 1000),
+                                     ("f32", 602), ("f32", 1024), ("f32", 1000), ("bf16", 602)])
 def test_gather_maximum_widths(dtype, F):
-    """The widest rows the simple Gather takes (512 float32 / 1024 bfloat16
-    columns, whole and ragged), sum with both norms and max, on the
+    """Wide rows up to the widest the simple Gather takes (1024 columns in
+    both dtypes; float32 rows past 512 columns run as 128-byte slices, 602
+    and 1000 with a ragged last slice), sum with both norms and max, on the
     power-law graph with split rows."""
     S = lib()
     rp, col, n, g = _get_graph("rmat")
@@ -482,7 +484,7 @@ def test_gather_maximum_widths(dtype, F):
     assert rel_err(to_np(out), ref) <= tol
     out = run_gather(g, Xt, dict(reduce=S.SAGA_RED_MAX), F, tdt)
     assert np.array_equal(to_np(out), O.gather(rp, col, X, "max"))
-    limit = 512 if dtype == "f32" else 1024  # one column past the widest row is refused
+    limit = 1024  # one column past the widest row is refused
     wider = dev_padded(np.zeros((n, limit + 1), np.float32), tdt)
     with pytest.raises(S.SagaError):
         run_gather(g, wider, dict(reduce=S.SAGA_RED_SUM), limit + 1, tdt)

@@ -41,7 +41,7 @@ def run_unfused(g, src_t, op_kw, out_cols, out_dtype, bias=None):
 
 
 @pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_star", "tiny_random", "tiny_chain"])
-@pytest.mark.parametrize("F", [1, 8, 41, 128, 300])
+@pytest.mark.parametrize("F", [1, 8, 41, 128, 300, 602])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_unfused_matches_oracle(gname, F, dtype):
     S = lib()
