@@ -321,10 +321,10 @@ saga_status saga_rel_plan_check(const saga_rel_plan* rel, void* stream, saga_rel
  * (num_rel * K) x N (rows r*K .. r*K+K-1 are W_r; dtype); out: max_pairs x
  * N (dtype).  N <= 4096.  Workspace: saga_rel_transform_workspace_size()
  * bytes, 256-byte aligned (the packed, transposed weights). */
-saga_status saga_rel_transform_workspace_size(const saga_rel_plan* rel, saga_dtype dtype,
+saga_status saga_rel_transform_workspace_size(const saga_rel_plan* rel, int32_t dtype,
                                               int64_t k, int64_t n, size_t* bytes);
 
-saga_status saga_rel_transform(const saga_rel_plan* rel, saga_dtype dtype, saga_cmat x,
+saga_status saga_rel_transform(const saga_rel_plan* rel, int32_t dtype, saga_cmat x,
                                saga_cmat w, saga_mat out, void* workspace,
                                size_t workspace_bytes, void* stream);
 
@@ -361,14 +361,16 @@ saga_status saga_rel_transform(const saga_rel_plan* rel, saga_dtype dtype, saga_
  * SAGA_EUNSUPPORTED.
  */
 typedef struct saga_edge_op {
-  saga_msg msg;
-  saga_reduce reduce;
-  saga_dtype dtype;
+  /* enumerated fields are plain int32_t (the enum named in the comment), so
+     that the library can range-check whatever value a caller stores */
+  int32_t msg;         /* saga_msg */
+  int32_t reduce;      /* saga_reduce */
+  int32_t dtype;       /* saga_dtype */
   int32_t heads;       /* GAT: number of heads; else ignored */
   int32_t head_mean;   /* GAT: 1 = average over heads */
   int32_t dst_norm;    /* 1 = multiply SUM/MAX aggregate by d_in(v)^-1/2 */
   float neg_slope;     /* GAT LeakyReLU slope (0.2 in GAT) */
-  saga_act act;
+  int32_t act;         /* saga_act */
 } saga_edge_op;
 
 typedef struct saga_edge_inputs {
@@ -541,9 +543,9 @@ saga_status saga_lstm_gather_rows(const saga_plan* plan, int32_t perm_begin, int
 typedef enum saga_gemm_mode { SAGA_GEMM_PLAIN = 0, SAGA_GEMM_CONCAT = 1, SAGA_GEMM_GRU = 2 } saga_gemm_mode;
 
 typedef struct saga_gemm_op {
-  saga_dtype dtype;
-  saga_gemm_mode mode;
-  saga_act act;                   /* PLAIN / CONCAT */
+  int32_t dtype;                  /* saga_dtype */
+  int32_t mode;                   /* saga_gemm_mode */
+  int32_t act;                    /* saga_act; PLAIN / CONCAT */
   const int32_t* row_scale_deg;   /* nullable, int32[M] */
   int32_t split_col;              /* PLAIN / CONCAT: 0 = one output matrix; s > 0: columns
                                      [0, s) go to `out` (M x s) and [s, N) to `tail` */
@@ -594,12 +596,12 @@ typedef enum saga_layer_kind {
 } saga_layer_kind;
 
 typedef struct saga_layer_desc {
-  saga_layer_kind kind;
-  saga_dtype dtype;
+  int32_t kind;                   /* saga_layer_kind */
+  int32_t dtype;                  /* saga_dtype */
   int32_t in_feat, out_feat;
   int32_t heads, head_mean;       /* GAT */
   float neg_slope;                /* GAT */
-  saga_act act;                   /* GCN, GAT, RGCN */
+  int32_t act;                    /* saga_act; GCN, GAT, RGCN */
   int32_t edge_feat;              /* GATED_GRU: Fe */
   const void* w;  const float* b;             /* GCN, GAT, SAGE_POOL */
   const void* w_pool; const float* b_pool;    /* SAGE_POOL */

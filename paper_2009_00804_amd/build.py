@@ -63,6 +63,64 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host sanitizers for the C-ABI layer: abi.hip (argument validation, shape
+# and overlap checks, error messages) rebuilt with AddressSanitizer and
+# UndefinedBehaviorSanitizer on its host code only (device code is built as
+# usual), linked with the package's other objects from build().  The result
+# is for host-side tests on a machine without a GPU: load it with the ASan
+# runtime preloaded (asan_runtime()) and drive the validation paths.
+SANITIZED = os.path.join(BUILD, "sanitize", "libsaga_sanitized.so")
+SAN_FLAGS = [
+    "-Xarch_host", "-fsanitize=address",
+    "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=undefined",
+    "-Xarch_host", "-fno-omit-frame-pointer",
+    "-g",
+]
+
+
+def clangxx() -> str:
+    return os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "llvm", "bin", "clang++")
+
+
+def asan_runtime() -> str:
+    r = subprocess.run([clangxx(), "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True,
+                       text=True, check=True)
+    return r.stdout.strip()
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """libsaga with abi.hip's host code under ASan + UBSan (see above).
+    Needs the objects of build(); rebuilt only when abi.hip or a header is
+    newer than the library."""
+    out_dir = os.path.dirname(SANITIZED)
+    os.makedirs(out_dir, exist_ok=True)
+    others = [os.path.join(BUILD, os.path.splitext(s)[0] + ".o") for s in SOURCES if s != "abi.hip"]
+    if not all(os.path.exists(o) for o in others):
+        build()
+    deps = [os.path.join(CSRC, "abi.hip"), os.path.join(INCLUDE, "saga.h"),
+            os.path.join(CSRC, "saga_internal.h"), os.path.join(CSRC, "saga_device.h"), *others]
+    if os.path.exists(SANITIZED) and os.path.getmtime(SANITIZED) >= max(map(os.path.getmtime, deps)):
+        return SANITIZED
+    obj = os.path.join(out_dir, "abi_sanitized.o")
+    flags = [f for f in FLAGS if f != "-O3"] + ["-O1"] + SAN_FLAGS
+    cmd = [hipcc(), *flags, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "abi.hip"), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on abi.hip (sanitized):\n{r.stderr}")
+    rocm_lib = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "lib")
+    tmp = SANITIZED + ".tmp"
+    cmd = [clangxx(), "-shared", "-fPIC", "-fsanitize=address,undefined", "-shared-libsan", "-o", tmp,
+           obj, *others, "-L", rocm_lib, "-lamdhip64", f"-Wl,-rpath,{rocm_lib}"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{r.stderr}")
+    os.replace(tmp, SANITIZED)
+    if verbose:
+        print("built", SANITIZED)
+    return SANITIZED
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)

@@ -34,7 +34,7 @@ saga_status dev_fail(hipError_t e, const char* where) {
   return fail(SAGA_EDEVICE, "%s: %s", where, hipGetErrorString(e));
 }
 
-inline size_t esize(saga_dtype t) { return t == SAGA_BF16 ? 2 : 4; }
+inline size_t esize(int32_t t) { return t == SAGA_BF16 ? 2 : 4; }
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -504,7 +504,7 @@ struct LayerPlanWs {
 // rows of up to 128 bytes are padded to a power of two (never straddling a
 // 128-byte L2 line), longer rows to a multiple of 64 bytes (each row then
 // touches a whole number of lines).
-int64_t ld_for(int64_t cols, saga_dtype t) {
+int64_t ld_for(int64_t cols, int32_t t) {
   const int64_t es = t == SAGA_BF16 ? 2 : 4;
   int64_t bytes = cols * es;
   if (bytes <= 128) {
@@ -521,7 +521,7 @@ int64_t ld_for(int64_t cols, saga_dtype t) {
 // unfused baseline: index-select into an E x ldm edge tensor, then reduce
 // ---------------------------------------------------------------------------
 size_t unfused_msg_bytes(const saga_plan& p, const saga_edge_op& op, int64_t feat, int64_t* ldm) {
-  const saga_dtype t = op.dtype == SAGA_BF16 ? SAGA_BF16 : SAGA_F32;
+  const int32_t t = op.dtype == SAGA_BF16 ? SAGA_BF16 : SAGA_F32;
   *ldm = ld_for(feat, t);
   return align256((size_t)p.num_edges * (size_t)*ldm * esize(t));
 }
@@ -634,7 +634,7 @@ saga_status run_lstm(const saga_plan& p, const saga_cmat& gx, const saga_cmat& w
 // ---------------------------------------------------------------------------
 // R-GCN: per-relation transform of the distinct (relation, source) pairs
 // ---------------------------------------------------------------------------
-saga_status run_rel_transform(const saga_rel_plan& r, saga_dtype dtype, const saga_cmat& x,
+saga_status run_rel_transform(const saga_rel_plan& r, int32_t dtype, const saga_cmat& x,
                               const saga_cmat& w, const saga_mat& out, void* ws, size_t ws_bytes,
                               hipStream_t st) {
   if (dtype != SAGA_F32 && dtype != SAGA_BF16) return fail(SAGA_EINVAL, "bad dtype");
@@ -746,7 +746,7 @@ bool gcn_transform_first(const saga_layer_desc& d) { return d.out_feat <= d.in_f
 // each is gathered by its own call, so no gathered row straddles a line
 // shared with its neighbour (F = 41 float32: 32 + 9 columns instead of one
 // 192-byte row over two lines).
-int64_t line_split(int64_t cols, saga_dtype t) {
+int64_t line_split(int64_t cols, int32_t t) {
   const int64_t es = t == SAGA_BF16 ? 2 : 4, per_line = 128 / es;
   if (cols <= per_line || cols % per_line == 0) return 0;
   return cols / per_line * per_line;
@@ -755,7 +755,7 @@ int64_t line_split(int64_t cols, saga_dtype t) {
 size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, LayerBufs* b) {
   Carve c(base, (size_t)-1);
   const int64_t V = p.num_dst;
-  const saga_dtype t = d.dtype;
+  const int32_t t = d.dtype;
   const size_t es = esize(t);
   saga_edge_op op;
   memset(&op, 0, sizeof(op));
@@ -1529,7 +1529,7 @@ saga_status saga_rel_plan_check(const saga_rel_plan* rel, void* stream, saga_rel
   }
 }
 
-saga_status saga_rel_transform_workspace_size(const saga_rel_plan* rel, saga_dtype dtype,
+saga_status saga_rel_transform_workspace_size(const saga_rel_plan* rel, int32_t dtype,
                                               int64_t k, int64_t n, size_t* bytes) {
   try {
     if (!rel || !bytes) return fail(SAGA_EINVAL, "null argument");
@@ -1544,7 +1544,7 @@ saga_status saga_rel_transform_workspace_size(const saga_rel_plan* rel, saga_dty
   }
 }
 
-saga_status saga_rel_transform(const saga_rel_plan* rel, saga_dtype dtype, saga_cmat x,
+saga_status saga_rel_transform(const saga_rel_plan* rel, int32_t dtype, saga_cmat x,
                                saga_cmat w, saga_mat out, void* workspace,
                                size_t workspace_bytes, void* stream) {
   try {
