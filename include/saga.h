@@ -627,7 +627,10 @@ saga_status saga_layer(const saga_plan* plan, const saga_layer_desc* desc, saga_
  * stages past n_events record nothing), and with markers != 0 launches an
  * empty kernel named k_stage_mark there (and k_stage_begin before the first
  * stage), which delimit the stages in a counter profile's list of
- * dispatches.  The stages, in order:
+ * dispatches; with markers the host side of each call is also bracketed by
+ * roctx ranges, "saga_layer" around the call and "saga stage k" around the
+ * enqueue of stage k (k from 0, in the order below), for a timeline trace.
+ * The stages, in order:
  *   GCN (transform first)   transform, gather (a split output: transform,
  *                           gather of the whole-line columns, gather of the
  *                           rest)

@@ -39,6 +39,10 @@ FLAGS = [
 ]
 
 
+# roctx: the stage ranges saga_layer opens when stage markers are on
+LIBS = ["-lrocprofiler-sdk-roctx"]
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
     cmd = [hipcc(), *FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]
@@ -53,7 +57,7 @@ def build(verbose: bool = False) -> str:
     with cf.ThreadPoolExecutor(len(SOURCES)) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
+    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs, *LIBS]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
@@ -111,7 +115,7 @@ def build_sanitized(verbose: bool = False) -> str:
     rocm_lib = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "lib")
     tmp = SANITIZED + ".tmp"
     cmd = [clangxx(), "-shared", "-fPIC", "-fsanitize=address,undefined", "-shared-libsan", "-o", tmp,
-           obj, *others, "-L", rocm_lib, "-lamdhip64", f"-Wl,-rpath,{rocm_lib}"]
+           obj, *others, "-L", rocm_lib, "-lamdhip64", *LIBS, f"-Wl,-rpath,{rocm_lib}"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"sanitized link failed:\n{r.stderr}")

@@ -1,6 +1,7 @@
 // C-ABI entry points: argument validation, workspace carving and dispatch
 // to the kernel launchers; whole-layer composition of the Table I models.
 #include <hip/hip_runtime.h>
+#include <rocprofiler-sdk-roctx/roctx.h>
 
 #include <algorithm>
 #include <cstdarg>
@@ -880,7 +881,10 @@ size_t layer_carve(const saga_plan& p, const saga_layer_desc& d, void* base, Lay
 // the next of the caller's events on the layer's stream and, with markers,
 // launch k_stage_mark, an empty kernel that delimits the stages in a
 // counter profile's dispatch list (k_stage_begin opens each traced layer
-// call).  Thread-local; off unless set.
+// call).  With markers, the host side of the call is also bracketed by
+// roctx ranges ("saga_layer", and "saga stage k" around the enqueue of
+// stage k) for a timeline trace (rocprofv3 --marker-trace).
+// Thread-local; off unless set.
 // ---------------------------------------------------------------------------
 __global__ void k_stage_begin() {}
 __global__ void k_stage_mark() {}
@@ -888,8 +892,22 @@ __global__ void k_stage_mark() {}
 thread_local std::vector<hipEvent_t> g_stage_events;
 thread_local int g_stage_next = 0;
 thread_local int g_stage_markers = 0;
+thread_local int g_range_depth = 0;  // roctx ranges this layer call has open
 
-saga_status stage_done(hipStream_t st) {
+void stage_range_push(int k) {
+  char name[32];
+  snprintf(name, sizeof(name), "saga stage %d", k);
+  roctxRangePushA(name);
+  ++g_range_depth;
+}
+
+void stage_ranges_close() {
+  for (; g_range_depth > 0; --g_range_depth) roctxRangePop();
+}
+
+// after stage k: record event k, mark the dispatch list, and (last ==
+// false) open stage k + 1's range
+saga_status stage_done(hipStream_t st, bool last = false) {
   if (g_stage_next < (int)g_stage_events.size()) {
     const hipError_t e = hipEventRecord(g_stage_events[g_stage_next], st);
     if (e != hipSuccess) return dev_fail(e, "stage event");
@@ -899,6 +917,11 @@ saga_status stage_done(hipStream_t st) {
     hipLaunchKernelGGL(k_stage_mark, dim3(1), dim3(64), 0, st);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return dev_fail(e, "stage marker");
+    if (g_range_depth > 1) {  // this stage's range
+      roctxRangePop();
+      --g_range_depth;
+    }
+    if (!last) stage_range_push(g_stage_next);
   }
   return SAGA_OK;
 }
@@ -917,6 +940,9 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
   layer_carve(p, d, ws, &b);
   g_stage_next = 0;
   if (g_stage_markers) {
+    roctxRangePushA("saga_layer");
+    ++g_range_depth;
+    stage_range_push(0);
     hipLaunchKernelGGL(k_stage_begin, dim3(1), dim3(64), 0, st);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return dev_fail(e, "stage marker");
@@ -964,7 +990,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
           in.bias = d.b;
           s = run_gather(p, op, in, out, b.part, b.part_bytes, st);
           if (s) return s;
-          return stage_done(st);
+          return stage_done(st, true);
         }
         // the whole-line columns, then the rest, into the two column ranges of out
         in.src = saga_cmat{b.z, V, sp, b.ldz};
@@ -978,7 +1004,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
                        saga_mat{static_cast<char*>(out.ptr) + sp * es, out.rows, Fo - sp, out.ld},
                        b.part, b.part_bytes, st);
         if (s) return s;
-        return stage_done(st);
+        return stage_done(st, true);
       }
       // aggregate first: agg = d_in^-1/2 sum_u d_out(u)^-1/2 X_u; out = act(agg W + b)
       op.msg = SAGA_MSG_SRC_NORM;
@@ -993,7 +1019,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       s = run_gemm(g, saga_cmat{b.z2, V, Fi, b.ldz2}, saga_cmat{d.w, Fi, Fo, Fo}, none, none,
                    d.b, nullptr, out, b.gws, b.gws_bytes, st);
       if (s) return s;
-      return stage_done(st);
+      return stage_done(st, true);
     }
     case SAGA_LAYER_GAT: {
       const int64_t H = d.heads;
@@ -1020,7 +1046,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       in.bias = d.b;
       s = run_gather(p, op, in, out, b.part, b.part_bytes, st);
       if (s) return s;
-      return stage_done(st);
+      return stage_done(st, true);
     }
     case SAGA_LAYER_SAGE_POOL: {
       g.mode = SAGA_GEMM_PLAIN;
@@ -1041,7 +1067,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       s = run_gemm(g, x, saga_cmat{w, Fi, Fo, Fo}, saga_cmat{b.z2, V, Fi, b.ldz2},
                    saga_cmat{w + (size_t)Fi * Fo * es, Fi, Fo, Fo}, d.b, nullptr, out, b.gws, b.gws_bytes, st);
       if (s) return s;
-      return stage_done(st);
+      return stage_done(st, true);
     }
     case SAGA_LAYER_SAGE_LSTM: {
       // P = X W_ih + b_ih + b_hh; A = LSTM Gather; out = [X | A] W + b
@@ -1061,7 +1087,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
                    saga_cmat{w + (size_t)Fi * Fo * 4, H, Fo, Fo}, d.b, nullptr, out, b.gws,
                    b.gws_bytes, st);
       if (s) return s;
-      return stage_done(st);
+      return stage_done(st, true);
     }
     case SAGA_LAYER_RGCN: {
       // T = pair rows x_u W_r; S = X W_self + b; out = act(S_v + sum_e norm_e T[pair_e])
@@ -1083,7 +1109,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       in.self = saga_cmat{b.z2, V, Fo, b.ldz2};
       s = run_gather(p, op, in, out, b.part, b.part_bytes, st);
       if (s) return s;
-      return stage_done(st);
+      return stage_done(st, true);
     }
     case SAGA_LAYER_GATED_GRU: {
       const int64_t F = Fi, Fe = d.edge_feat;
@@ -1112,7 +1138,7 @@ saga_status run_layer(const saga_plan& p, const saga_layer_desc& d, const saga_c
       s = run_gemm(g, saga_cmat{b.z3, V, F, b.ldz3}, saga_cmat{d.w_ih, F, 3 * F, 3 * F}, x,
                    saga_cmat{d.w_hh, F, 3 * F, 3 * F}, d.b_ih, d.b_hh, out, b.gws, b.gws_bytes, st);
       if (s) return s;
-      return stage_done(st);
+      return stage_done(st, true);
     }
   }
   return fail(SAGA_EINVAL, "bad layer kind");
@@ -1636,9 +1662,12 @@ saga_status saga_layer(const saga_plan* plan, const saga_layer_desc* desc, saga_
     saga_status s = check_plan(plan);
     if (s) return s;
     if (!desc) return fail(SAGA_EINVAL, "desc is null");
-    return run_layer(*plan, *desc, x, edge_feat, out, workspace, workspace_bytes,
-                     static_cast<hipStream_t>(stream));
+    s = run_layer(*plan, *desc, x, edge_feat, out, workspace, workspace_bytes,
+                  static_cast<hipStream_t>(stream));
+    stage_ranges_close();
+    return s;
   } catch (...) {
+    stage_ranges_close();
     return fail(SAGA_EINTERNAL, "exception");
   }
 }
