@@ -79,6 +79,9 @@ GRAPHS = {"tiny_" + c[0]: c for c in tiny_graphs()}
 def _get_graph(name, seg_len=16, block_cost=128):
     if name == "rmat":
         rp, col, n = _power_law()
+    elif name == "edgeless":  # every row empty: the Gather output is act(bias)
+        n = 37
+        rp, col = np.zeros(n + 1, np.int32), np.zeros(0, np.int32)
     else:
         _, n, src, dst = GRAPHS[name]
         rp, col, _ = edges_to_csr(n, src, dst)
@@ -498,7 +501,7 @@ def _transform_ref(rp, col, X, red, dn, bias, act, n, W, rs_deg):
     return O.dense(h, W) * rs[:, None], h
 
 
-@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_random"])
+@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_random", "edgeless"])
 @pytest.mark.parametrize("dtype,F,N,split", [("f32", 128, 41, 32), ("f32", 32, 8, 0), ("f32", 64, 64, 0),
                                              ("bf16", 128, 41, 0), ("bf16", 64, 16, 8)])
 def test_gather_transform_fused(gname, dtype, F, N, split):
