@@ -873,6 +873,10 @@ def main():
         ms_seq = wall * 1e3 / args.steps
         med = {n: statistics.median(v) for n, v in per.items()}
         mean = {n: statistics.fmean(v) for n, v in per.items()}
+        # per stage over the timed steps: median, min and 90th percentile
+        spread = {n: {"median": round(statistics.median(v), 4), "min": round(min(v), 4),
+                      "p90": round(sorted(v)[min(len(v) - 1, int(0.9 * len(v)))], 4)}
+                  for n, v in per.items()}
         step.split = True
         wall_p, _, _ = time_step(step, args.steps, args.warmup)
         ms_pipe = wall_p * 1e3 / args.steps
@@ -884,7 +888,7 @@ def main():
         step.split = args.pipeline == "on"
         step.fused = args.fused == "on"
         ms = ms_fused if step.fused else (ms_pipe if step.split else ms_seq)
-        results[dt] = dict(step=step, ms=ms, med=med, mean=mean, counts=counts,
+        results[dt] = dict(step=step, ms=ms, med=med, mean=mean, spread=spread, counts=counts,
                            ev_ms=statistics.median(tot), ms_seq=ms_seq, ms_pipe=ms_pipe,
                            ms_fused=ms_fused, fused_gather1=fused_gather1)
         log(f"{dt}: {ms_seq:.3f} ms/step stage by stage (events {statistics.median(tot):.3f}); "
@@ -929,6 +933,8 @@ def main():
         # measured HBM traffic (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)
         roof["counter_GBps"] = roof["traffic"] / dur / 1e9
         roof["counter_frac_of_8TBps"] = roof["counter_GBps"] / (PEAK_HBM / 1e9)
+        roof["traffic_note"] = ("FETCH_SIZE counts L2 egress, Infinity Cache hits included: an "
+                                "upper bound on DRAM bytes")
     stage_ms = {n: round(r["mean"][n], 4) for n in step.names}
     out = {
         "metric": "GNN layer throughput: edges/s (GTEPS) + achieved HBM GB/s fraction, 1 MI355X",
@@ -949,6 +955,7 @@ def main():
         "gteps": value / 1e9,
         "vertices_per_s": 2 * V / (r["ms"] * 1e-3),
         "stage_ms": stage_ms,
+        "stage_ms_spread": r["spread"],
         "gather1_noreuse_GBps": noreuse_bytes(step, "gather1") / (r["mean"]["gather1"] * 1e-3) / 1e9,
         "gemm1_TFLOPs": algorithmic(step, "gemm1")[1] / (r["mean"]["gemm1"] * 1e-3) / 1e12,
         "plan": {"segments": r["counts"].num_segments, "blocks": r["counts"].num_blocks,
@@ -982,6 +989,7 @@ def main():
             "stage_by_stage_ms": rr["ms_seq"], "pipelined_ms": rr["ms_pipe"],
             "fused_ms": rr["ms_fused"], "fused_stage_ms": rr["fused_gather1"],
             "stage_ms": {n: round(rr["mean"][n], 4) for n in rr["mean"]},
+            "stage_ms_spread": rr["spread"],
             "stage_rooflines": stage_rooflines(V, E, step.dims, dt, rr["mean"])}
         if "unfused_ms" in rr:
             out["variants"][dt]["fusion"] = {"fused_ms": rr["mean"]["gather1"],
