@@ -144,8 +144,9 @@ class Step:
         self.stream = torch.cuda.current_stream()
         self.sh = S.stream_handle(self.stream)
         self.names = ["plan", "gemm1", "gather1", "gemm2", "gather2"]
-        # cross-stage fusion: layer 1's Gather with layer 2's transform in its
-        # last slice pass writes Z2 directly (no H1, no separate gemm2)
+        # cross-stage fusion: layer 1's Gather with layer 2's transform done
+        # in its last slice pass writes Z2 (H1 lives only in the call's
+        # workspace; no separate gemm2)
         self.fused = False
         self.nx = S.saga_next_transform()
         self.nx.w = S.cmat(self.W2)
