@@ -489,7 +489,15 @@ def suite_rooflines(name, stages, ms):
     return out
 
 
-def suite(dev, reps=10, oracle=True, schedule=None):
+def spread(v, nd=4):
+    """Median, min and 90th percentile (nearest rank: the ceil(0.9 n)-th
+    smallest) of a list of timings."""
+    k = max(1, -(-9 * len(v) // 10))
+    return {"median": round(statistics.median(v), nd), "min": round(min(v), nd),
+            "p90": round(sorted(v)[k - 1], nd)}
+
+
+def suite(dev, reps=20, oracle=True, schedule=None):
     """Per-workload, per-layer timing of the other six workloads through
     saga_layer (plan built once per graph and timed separately), each layer
     also stage by stage against its roofline; with `oracle`, the oracle's
@@ -538,7 +546,7 @@ def suite(dev, reps=10, oracle=True, schedule=None):
         stage_ms = time_stages(S, torch, model, x, ef, names, reps, markers=schedule is not None)
         if schedule is not None:
             schedule.append({"workload": name, "layers": names, "calls": reps})
-        per = [0.0] * len(model)
+        samples = [[] for _ in model]
         for _ in range(reps):
             h = x
             ev[0].record(st)
@@ -547,22 +555,26 @@ def suite(dev, reps=10, oracle=True, schedule=None):
                 ev[i + 1].record(st)
             torch.cuda.synchronize()
             for i in range(len(model)):
-                per[i] += ev[i].elapsed_time(ev[i + 1]) / reps
+                samples[i].append(ev[i].elapsed_time(ev[i + 1]))
+        per = [statistics.fmean(v) for v in samples]
         # plan build alone
+        plan_t = []
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(st)
         for _ in range(reps):
+            e0.record(st)
             S.saga_plan_build(graph.num_dst, graph.num_src, graph.num_edges,
                               C.c_void_p(rp.data_ptr()), C.c_void_p(col.data_ptr()), graph.opts,
                               C.c_void_p(graph.ws.data_ptr()), graph.ws.numel(),
                               S.stream_handle(st))
-        e1.record(st)
-        torch.cuda.synchronize()
+            e1.record(st)
+            torch.cuda.synchronize()
+            plan_t.append(e0.elapsed_time(e1))
         out[name] = {
             "workload": desc, "vertices": V, "edges": E,
-            "plan_ms": e0.elapsed_time(e1) / reps,
-            "layers": [{"ms": round(ms, 5), "gteps": E / (ms * 1e-3) / 1e9,
-                        "vertices_per_s": V / (ms * 1e-3)} for ms in per],
+            "plan_ms": statistics.fmean(plan_t), "plan_ms_spread": spread(plan_t, 5),
+            "layers": [{"ms": round(ms, 5), "ms_spread": spread(v, 5),
+                        "gteps": E / (ms * 1e-3) / 1e9, "vertices_per_s": V / (ms * 1e-3)}
+                       for ms, v in zip(per, samples)],
             "stage_rooflines": suite_rooflines(name, stages, stage_ms)}
         log(f"suite {name}: V={V} E={E} plan {out[name]['plan_ms']:.3f} ms, layers "
             + ", ".join(f"{ms:.3f} ms" for ms in per))
@@ -875,9 +887,7 @@ def main():
         med = {n: statistics.median(v) for n, v in per.items()}
         mean = {n: statistics.fmean(v) for n, v in per.items()}
         # per stage over the timed steps: median, min and 90th percentile
-        spread = {n: {"median": round(statistics.median(v), 4), "min": round(min(v), 4),
-                      "p90": round(sorted(v)[min(len(v) - 1, int(0.9 * len(v)))], 4)}
-                  for n, v in per.items()}
+        stage_spread = {n: spread(v) for n, v in per.items()}
         step.split = True
         wall_p, _, _ = time_step(step, args.steps, args.warmup)
         ms_pipe = wall_p * 1e3 / args.steps
@@ -889,7 +899,7 @@ def main():
         step.split = args.pipeline == "on"
         step.fused = args.fused == "on"
         ms = ms_fused if step.fused else (ms_pipe if step.split else ms_seq)
-        results[dt] = dict(step=step, ms=ms, med=med, mean=mean, spread=spread, counts=counts,
+        results[dt] = dict(step=step, ms=ms, med=med, mean=mean, spread=stage_spread, counts=counts,
                            ev_ms=statistics.median(tot), ms_seq=ms_seq, ms_pipe=ms_pipe,
                            ms_fused=ms_fused, fused_gather1=fused_gather1)
         log(f"{dt}: {ms_seq:.3f} ms/step stage by stage (events {statistics.median(tot):.3f}); "
