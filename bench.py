@@ -376,6 +376,82 @@ def _oracle_model(name, g, rows=None):
     return O.gated_layer_of(g)
 
 
+# layers of each suite workload's model (the others have one)
+SUITE_LAYERS = {"gcn_er": 2, "gat_ba": 2}
+_SUITE_G = {}
+
+
+def _suite_rows(name, g):
+    """The bounded destination-row sample the oracle runs on for the
+    workloads whose oracle loops over rows (and, for the LSTM, steps);
+    None: the whole model."""
+    import numpy as np
+
+    if name not in ("sage_lstm", "rgcn_rmat"):
+        return None
+    return np.random.default_rng(7).choice(g["num_vertices"], 1500 if name == "sage_lstm" else 4000,
+                                           replace=False)
+
+
+def _suite_oracle_runs(args):
+    """(runs, seconds): the oracle of one workload on one thread, repeated
+    until `budget_s` has passed (at least once)."""
+    name, budget_s = args
+    from threadpoolctl import threadpool_limits
+
+    g = _SUITE_G[name]
+    rows = _suite_rows(name, g)
+    runs, t = 0, 0.0
+    with threadpool_limits(1):
+        while runs == 0 or t < budget_s:
+            t0 = time.perf_counter()
+            _oracle_model(name, g, rows=rows)
+            t += time.perf_counter() - t0
+            runs += 1
+    return runs, t
+
+
+def suite_oracles(reps=3, budget_s=1.0):
+    """The oracle of each suite workload, run before the GPU is touched
+    (the all-cores leg forks worker processes): on one thread, the median
+    of `reps` runs; and on every core of the affinity mask (at most 16),
+    each worker process one thread repeating the whole evaluation for
+    `budget_s`, the throughput summed over the workers."""
+    import multiprocessing as mp
+
+    import numpy as np
+
+    from synth import configs as Cfg
+
+    out = {}
+    cores = max(1, min(len(os.sched_getaffinity(0)), 16))
+    for name, _ in SUITE:
+        g = Cfg.build(name)
+        _SUITE_G.clear()
+        _SUITE_G[name] = g
+        rows = _suite_rows(name, g)
+        work = SUITE_LAYERS.get(name, 1) * (g["num_edges"] if rows is None
+                                             else int(np.diff(g["row_ptr"])[rows].sum()))
+        sample = ("whole model, float64" if rows is None else
+                  f"layer on {len(rows)} random destination rows ({work} in-edges), float64")
+        t1 = statistics.median(_suite_oracle_runs((name, 0.0))[1] for _ in range(reps))
+        rec = {"ms": t1 * 1e3, "edges_per_s": work / t1, "cores": 1, "kind": "oracle",
+               "sample": f"{sample}, median of {reps} runs", "cpu_model": _cpu_model()}
+        if cores > 1:
+            with mp.get_context("fork").Pool(cores) as pool:
+                res = pool.map(_suite_oracle_runs, [(name, budget_s)] * cores)
+            rec["all_cores"] = {
+                "edges_per_s": sum(r[0] * work / r[1] for r in res), "cores": cores,
+                "sample": f"{cores} worker processes of one thread, each repeating the "
+                          f"evaluation for {budget_s:g} s ({sum(r[0] for r in res)} runs)"}
+        out[name] = rec
+        log(f"suite oracle {name}: {t1 * 1e3:.1f} ms on one thread"
+            + (f", {rec['all_cores']['edges_per_s']:.3e} edges/s on {cores} cores"
+               if cores > 1 else ""))
+    _SUITE_G.clear()
+    return out
+
+
 def _gemm_work(M, K, N, es=4):
     """(compulsory bytes, flops) of an M x K by K x N product: A, W and the
     output once; 2 M K N."""
@@ -497,14 +573,14 @@ def spread(v, nd=4):
             "p90": round(sorted(v)[k - 1], nd)}
 
 
-def suite(dev, reps=20, oracle=True, schedule=None):
+def suite(dev, reps=20, oracles=None, schedule=None):
     """Per-workload, per-layer timing of the other six workloads through
     saga_layer (plan built once per graph and timed separately), each layer
-    also stage by stage against its roofline; with `oracle`, the oracle's
-    whole model on the same inputs (or a bounded row sample of it), one
-    thread.  With `schedule` (a list), the stage loop runs with the
-    library's stage markers on and the calls are appended to it (for
-    attributing a counter profile's dispatches to stages)."""
+    also stage by stage against its roofline; `oracles` (suite_oracles'
+    result, taken before the GPU was touched) is reported beside each.
+    With `schedule` (a list), the stage loop runs with the library's stage
+    markers on and the calls are appended to it (for attributing a counter
+    profile's dispatches to stages)."""
     import numpy as np
     import torch
 
@@ -589,23 +665,8 @@ def suite(dev, reps=20, oracle=True, schedule=None):
                 f"({d['lstm_us_per_step_of_longest_row']:.3f} us/step of the longest row), "
                 f"{d['degree_traversal_ms']:.3f} ms as {d['degree_traversal_launches']} "
                 f"per-degree launches")
-        if oracle:
-            from threadpoolctl import threadpool_limits
-
-            rows, e_s, sample = None, E, "whole model, float64"
-            if name in ("sage_lstm", "rgcn_rmat"):
-                # the oracle loops over rows (and, for the LSTM, steps): a bounded sample
-                rows = np.random.default_rng(7).choice(V, 1500 if name == "sage_lstm" else 4000,
-                                                       replace=False)
-                e_s = int(np.diff(g["row_ptr"])[rows].sum())
-                sample = f"layer on {len(rows)} random destination rows ({e_s} in-edges), float64"
-            with threadpool_limits(1):
-                t0 = time.perf_counter()
-                _oracle_model(name, g, rows=rows)
-                t = time.perf_counter() - t0
-            out[name]["cpu_oracle"] = {"ms": t * 1e3, "edges_per_s": len(per) * e_s / t, "cores": 1,
-                                       "kind": "oracle", "sample": sample, "cpu_model": _cpu_model()}
-            log(f"suite {name}: oracle {t:.2f} s")
+        if oracles and name in oracles:
+            out[name]["cpu_oracle"] = oracles[name]
         del model, graph
         torch.cuda.empty_cache()
     return out
@@ -862,6 +923,9 @@ def main():
         cpu = cpu_baseline(g, args.cpu_budget)
         log(f"cpu baseline: {cpu['value']:.3e} edges/s on {cpu['cores']} cores, "
             f"{cpu['single_thread']['value']:.3e} on one")
+    oracles = None
+    if not args.no_cpu_baseline and not args.no_suite:
+        oracles = suite_oracles()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     dtypes = [args.dtype] + [d for d in args.variants.split(",") if d and d != args.dtype]
@@ -1008,7 +1072,7 @@ def main():
                                              "speedup": rr["unfused_ms"] / rr["mean"]["gather1"]}
     if not args.no_suite:
         schedule = [] if args.suite_schedule else None
-        out["suite"] = suite(dev, oracle=not args.no_cpu_baseline, schedule=schedule)
+        out["suite"] = suite(dev, oracles=oracles, schedule=schedule)
         if schedule is not None:
             with open(args.suite_schedule, "w") as f:
                 json.dump(schedule, f)
