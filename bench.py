@@ -523,8 +523,9 @@ def suite_stages(name, g, rel_counts=None):
 
 
 def time_stages(S, torch, model, x, ef, stages, reps, markers=False):
-    """Mean ms of every stage of every layer: events recorded by the library
-    after each stage (saga_trace_stages), one more before each layer."""
+    """Per-repetition ms of every stage of every layer ([layer][stage] lists):
+    events recorded by the library after each stage (saga_trace_stages), one
+    more before each layer."""
     st = torch.cuda.current_stream()
     evs = []
     for _ in range(reps):
@@ -539,19 +540,22 @@ def time_stages(S, torch, model, x, ef, stages, reps, markers=False):
         evs.append(row)
     S.saga_trace_stages([])
     torch.cuda.synchronize()
-    return [[statistics.fmean(evs[r][i][k].elapsed_time(evs[r][i][k + 1]) for r in range(reps))
+    return [[[evs[r][i][k].elapsed_time(evs[r][i][k + 1]) for r in range(reps)]
              for k in range(len(names))] for i, names in enumerate(stages)]
 
 
-def suite_rooflines(name, stages, ms):
-    """Each stage against its roofline: compulsory bytes against 8 TB/s, the
-    transforms' flops against the float32 MFMA peak, and, where a counter
-    record in profiles/ matches the kernel sources, the measured HBM bytes."""
+def suite_rooflines(name, stages, samples):
+    """Each stage against its roofline (its mean over the repetitions, with
+    median, min and p90): compulsory bytes against 8 TB/s, the transforms'
+    flops against the float32 MFMA peak, and, where a counter record in
+    profiles/ matches the kernel sources, the measured HBM bytes."""
     out = []
-    for li, (layer, tl) in enumerate(zip(stages, ms)):
-        for (st, kind, byts, flops), t_ms in zip(layer, tl):
+    for li, (layer, tl) in enumerate(zip(stages, samples)):
+        for (st, kind, byts, flops), v in zip(layer, tl):
+            t_ms = statistics.fmean(v)
             t = t_ms * 1e-3
             d = {"layer": li + 1, "stage": st, "bound": kind, "ms": round(t_ms, 5),
+                 "ms_spread": spread(v, 5),
                  "compulsory_bytes": byts, "compulsory_GBps": byts / t / 1e9,
                  "compulsory_frac_of_8TBps": byts / t / PEAK_HBM}
             if kind == "mfma":
@@ -619,7 +623,7 @@ def suite(dev, reps=20, oracles=None, schedule=None):
         torch.cuda.synchronize()
         stages = suite_stages(name, g, relg.check() if name == "rgcn_rmat" else None)
         names = [[st_[0] for st_ in layer] for layer in stages]
-        stage_ms = time_stages(S, torch, model, x, ef, names, reps, markers=schedule is not None)
+        stage_samples = time_stages(S, torch, model, x, ef, names, reps, markers=schedule is not None)
         if schedule is not None:
             schedule.append({"workload": name, "layers": names, "calls": reps})
         samples = [[] for _ in model]
@@ -651,7 +655,7 @@ def suite(dev, reps=20, oracles=None, schedule=None):
             "layers": [{"ms": round(ms, 5), "ms_spread": spread(v, 5),
                         "gteps": E / (ms * 1e-3) / 1e9, "vertices_per_s": V / (ms * 1e-3)}
                        for ms, v in zip(per, samples)],
-            "stage_rooflines": suite_rooflines(name, stages, stage_ms)}
+            "stage_rooflines": suite_rooflines(name, stages, stage_samples)}
         log(f"suite {name}: V={V} E={E} plan {out[name]['plan_ms']:.3f} ms, layers "
             + ", ".join(f"{ms:.3f} ms" for ms in per))
         if name == "rgcn_rmat":
@@ -672,7 +676,7 @@ def suite(dev, reps=20, oracles=None, schedule=None):
     return out
 
 
-def lstm_detail(S, torch, graph, g, x, dev, reps=5):
+def lstm_detail(S, torch, graph, g, x, dev, reps=20):
     """The LSTM Gather alone: the single persistent call against the degree
     traversal the paper profiles (Sec. 3.2, Fig. 8b: one launch per distinct
     in-degree, rows of equal degree batched), through saga_lstm_gather_rows
@@ -711,17 +715,23 @@ def lstm_detail(S, torch, graph, g, x, dev, reps=5):
             S.saga_lstm_gather_rows(graph.plan, a, b, S.cmat(P), S.cmat(Whh), S.mat(out),
                                     C.c_void_p(ws.data_ptr()), ws.numel(), sh)
 
-    res = {}
-    for name, f, n in (("persistent", persistent, reps), ("traversal", traversal, 2)):
+    res, spr = {}, {}
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for name, f, n in (("persistent", persistent, reps), ("traversal", traversal, 5)):
         f()
         torch.cuda.synchronize()
-        t0 = time.perf_counter()
+        v = []
         for _ in range(n):
+            e0.record(st)
             f()
-        torch.cuda.synchronize()
-        res[name] = (time.perf_counter() - t0) * 1e3 / n
+            e1.record(st)
+            torch.cuda.synchronize()
+            v.append(e0.elapsed_time(e1))
+        res[name], spr[name] = statistics.fmean(v), spread(v)
     dmax = int(d.max())
     return {"max_in_degree": dmax, "lstm_gather_ms": res["persistent"],
+            "lstm_gather_ms_spread": spr["persistent"],
             "lstm_us_per_step_of_longest_row": res["persistent"] * 1e3 / dmax,
             "degree_traversal_ms": res["traversal"], "degree_traversal_launches": len(cuts) - 1,
             "degree_traversal_slowdown": res["traversal"] / res["persistent"]}
