@@ -165,6 +165,52 @@ def test_gather_attention(gname, heads, D, head_mean):
     assert rel_err(to_np(out), ref) <= FP32_TOL
 
 
+@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_star"])
+@pytest.mark.parametrize("heads,D", [(4, 8), (8, 8), (1, 4)])
+def test_gather_attention_weights_sum_to_one(gname, heads, D):
+    """Edge-softmax invariant (Sec. 3.2 attention scores normalised over a
+    destination's in-edges): with every source row z_u = 1, each head's
+    output is the sum of its attention weights, 1 for a non-empty row
+    (within d_in * 2^-23 in float32) and 0 for an empty one.  The scores
+    span about +-100, so the max subtraction and the merge of split rows
+    (segments of 16 edges) are exercised."""
+    S = lib()
+    rp, col, n, g = _get_graph(gname)
+    F = heads * D
+    rng = np.random.default_rng(19 + heads)
+    Zx = np.ones((n, F + 2 * heads), np.float32)
+    Zx[:, F:] = (rng.standard_normal((n, 2 * heads)) * 30).astype(np.float32)
+    zt = dev_padded(Zx, torch.float32)
+    print(f"gather attention sum-to-one {gname} H={heads} D={D}", flush=True)
+    out = run_gather(g, zt[:, :F], dict(msg=S.SAGA_MSG_GAT, reduce=S.SAGA_RED_SOFTMAX, heads=heads,
+                                        neg_slope=0.2), F, torch.float32,
+                     el=zt[:, F:F + heads], er=zt[:, F + heads:])
+    got = to_np(out).astype(np.float64)
+    d = np.diff(rp).astype(np.float64)
+    want = np.broadcast_to((d > 0)[:, None], got.shape).astype(np.float64)
+    assert np.all(np.abs(got - want) <= np.maximum(d, 1.0)[:, None] * 2.0**-23)
+
+
+@pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_random"])
+def test_gather_attention_zero_scores_is_mean(gname):
+    """With el = er = 0 every score is 0, each weight is 1 / d_in, and the
+    attention Gather is the mean Gather of z (the oracle's mean, not its
+    attention code, is the reference)."""
+    S = lib()
+    rp, col, n, g = _get_graph(gname)
+    heads, D = 8, 8
+    F = heads * D
+    rng = np.random.default_rng(23)
+    Zx = np.zeros((n, F + 2 * heads), np.float32)
+    Zx[:, :F] = rng.standard_normal((n, F)).astype(np.float32)
+    zt = dev_padded(Zx, torch.float32)
+    print(f"gather attention zero scores {gname}", flush=True)
+    out = run_gather(g, zt[:, :F], dict(msg=S.SAGA_MSG_GAT, reduce=S.SAGA_RED_SOFTMAX, heads=heads,
+                                        neg_slope=0.2), F, torch.float32,
+                     el=zt[:, F:F + heads], er=zt[:, F + heads:])
+    assert rel_err(to_np(out), O.gather(rp, col, Zx[:, :F], "mean")) <= FP32_TOL
+
+
 @pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_chain"])
 def test_gather_gated(gname):
     """Gated messages: the kernel gets the split form (gate_src = H W_src,
