@@ -165,6 +165,37 @@ def test_gather_attention(gname, heads, D, head_mean):
     assert rel_err(to_np(out), ref) <= FP32_TOL
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_relabelling_moves_degrees_and_max_exactly(dtype):
+    """Permutation equivariance where it is exact: the vertices of a
+    power-law graph relabelled by a seeded permutation pi (in-CSR rebuilt,
+    source rows moved with their labels).  The plan's in- and out-degrees
+    move with the labels bit for bit, and so does the max Gather's output."""
+    from synth import graphs as G
+
+    S = lib()
+    rp, col, n = _power_law()
+    pi = G.rng_for(1603, 5).permutation(n)
+    dst = np.repeat(np.arange(n), np.diff(rp))
+    rp2, col2 = G.to_in_csr(n, pi[col], pi[dst])
+    g1 = graph(rp, col, num_src=n, seg_len=16, block_cost=128, row_cost=4)
+    g2 = graph(rp2, col2, num_src=n, seg_len=16, block_cost=128, row_cost=4)
+    a1 = {k: v.cpu().numpy() for k, v in g1.arrays().items()}
+    a2 = {k: v.cpu().numpy() for k, v in g2.arrays().items()}
+    assert np.array_equal(a2["d_in"][pi], a1["d_in"])
+    assert np.array_equal(a2["d_out"][pi], a1["d_out"])
+    F = 64
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    X = np.random.default_rng(5).standard_normal((n, F)).astype(np.float32)
+    if dtype == "bf16":
+        X = _bf16_round(X)
+    X2 = X[np.argsort(pi)]  # row pi[u] of X2 is row u of X
+    print(f"relabelled max gather {dtype}", flush=True)
+    o1 = to_np(run_gather(g1, dev_padded(X, tdt), dict(reduce=S.SAGA_RED_MAX), F, tdt))
+    o2 = to_np(run_gather(g2, dev_padded(X2, tdt), dict(reduce=S.SAGA_RED_MAX), F, tdt))
+    assert np.array_equal(o2[pi], o1)
+
+
 @pytest.mark.parametrize("gname", ["rmat", "tiny_multi", "tiny_star"])
 @pytest.mark.parametrize("heads,D", [(4, 8), (8, 8), (1, 4)])
 def test_gather_attention_weights_sum_to_one(gname, heads, D):
