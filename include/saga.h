@@ -649,6 +649,13 @@ saga_status saga_layer(const saga_plan* plan, const saga_layer_desc* desc, saga_
 saga_status saga_trace_stages(void* const* events, int32_t n_events, int32_t markers);
 
 /* ====================================================================== */
+/* Every compute call is asynchronous on the caller's stream: its status
+ * covers argument checks and the launch only.  saga_sync_check waits for
+ * all work enqueued on `stream` (NULL: the null stream) and returns
+ * SAGA_EDEVICE, with the HIP error in saga_last_error, if the device
+ * reported one; else SAGA_OK.  It allocates nothing. */
+saga_status saga_sync_check(void* stream);
+
 const char* saga_status_str(saga_status s);
 const char* saga_last_error(void);
 /* Library version string. */

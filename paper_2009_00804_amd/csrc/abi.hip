@@ -1203,6 +1203,16 @@ const char* saga_last_error(void) { return g_err; }
 
 const char* saga_version(void) { return "saga-mi355x 0.1 (gfx950)"; }
 
+saga_status saga_sync_check(void* stream) {
+  try {
+    const hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return dev_fail(e, "stream");
+    return ok();
+  } catch (...) {
+    return fail(SAGA_EINTERNAL, "exception");
+  }
+}
+
 saga_status saga_plan_workspace_size(int32_t num_dst, int32_t num_src, int64_t num_edges,
                                      const saga_plan_opts* opts, size_t* bytes) {
   try {

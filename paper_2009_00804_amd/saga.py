@@ -43,9 +43,8 @@ EXPORTS = [
     "saga_rel_plan_workspace_size", "saga_rel_plan_build", "saga_rel_plan_check",
     "saga_rel_transform_workspace_size", "saga_rel_transform",
     "saga_apply_vertex_workspace_size", "saga_apply_vertex",
-    "saga_layer_workspace_size", "saga_layer", "saga_trace_stages", "saga_status_str",
-    "saga_last_error",
-    "saga_version",
+    "saga_layer_workspace_size", "saga_layer", "saga_trace_stages", "saga_sync_check",
+    "saga_status_str", "saga_last_error", "saga_version",
 ]
 
 
@@ -184,6 +183,7 @@ def lib():
         "saga_layer": (S, [P(saga_plan), P(saga_layer_desc), saga_cmat, saga_cmat, saga_mat, C.c_void_p,
                            C.c_size_t, C.c_void_p]),
         "saga_trace_stages": (S, [C.POINTER(C.c_void_p), C.c_int32, C.c_int32]),
+        "saga_sync_check": (S, [C.c_void_p]),
         "saga_status_str": (C.c_char_p, [S]),
         "saga_last_error": (C.c_char_p, []),
         "saga_version": (C.c_char_p, []),
@@ -380,6 +380,10 @@ def saga_layer(plan, desc, x, edge_feat, out, workspace, ws_bytes, stream):
 
 def saga_version():
     return lib().saga_version().decode()
+
+
+def saga_sync_check(stream):
+    return _check(lib().saga_sync_check(stream), "saga_sync_check")
 
 
 # --------------------------------------------------------------------------

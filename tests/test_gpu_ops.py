@@ -165,6 +165,28 @@ def test_gather_attention(gname, heads, D, head_mean):
     assert rel_err(to_np(out), ref) <= FP32_TOL
 
 
+def test_sync_check_after_work_on_a_stream():
+    """saga_sync_check waits for a side stream's work (a Gather enqueued
+    there) and reports no device error; the output is then complete."""
+    S = lib()
+    rp, col, n, g = _get_graph("rmat")
+    X = np.random.default_rng(2).standard_normal((n, 32)).astype(np.float32)
+    Xt = dev_padded(X)
+    side = torch.cuda.Stream()
+    op = S.saga_edge_op()
+    op.msg, op.reduce, op.dtype, op.heads = S.SAGA_MSG_COPY, S.SAGA_RED_SUM, S.SAGA_F32, 1
+    inp = S.saga_edge_inputs()
+    inp.src = S.cmat(Xt)
+    out = dev_padded(np.zeros((n, 32)), fill=7.0)
+    ws = S.workspace(S.saga_gather_workspace_size(g.plan, op, 32), device())
+    torch.cuda.synchronize()
+    sh = S.stream_handle(side)
+    S.saga_scatter_apply_edge_gather(g.plan, op, inp, S.mat(out), C.c_void_p(ws.data_ptr()),
+                                     ws.numel(), sh)
+    S.saga_sync_check(sh)
+    assert rel_err(to_np(out), O.gather(rp, col, X, "sum")) <= FP32_TOL
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_relabelling_moves_degrees_and_max_exactly(dtype):
     """Permutation equivariance where it is exact: the vertices of a
