@@ -29,6 +29,12 @@ attributes every dispatch of the FETCH_SIZE and WRITE_SIZE runs to its
 workload, layer and stage:
   python -m paper_2009_00804_amd.profiling --suite FILE --fetch DIR --write DIR \\
       --copy-mib 1024 --command "..." --out profiles
+
+Marker mode (a rocprofv3 --marker-trace run of the same bench.py command):
+the roctx ranges saga_layer opens ("saga_layer", "saga stage k") are
+checked against the schedule and summarised per layer call and stage:
+  python -m paper_2009_00804_amd.profiling --suite FILE --markers DIR \\
+      --command "..." --out profiles
 """
 from __future__ import annotations
 
@@ -178,6 +184,78 @@ def attribute(disp, schedule):
     if ci != len(calls):
         raise ValueError(f"profile holds {ci} traced calls, the schedule {len(calls)}")
     return acc, kern
+
+
+def marker_ranges(marker_dir):
+    """[(name, start ns, end ns)] of the roctx ranges of a --marker-trace
+    run, by start time (an enclosing range before the ranges it holds)."""
+    rows = csv.DictReader(open(_csv(marker_dir, "marker_api_trace.csv")))
+    out = [(r["Function"], int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in rows]
+    out.sort(key=lambda x: (x[1], -x[2]))
+    return out
+
+
+def attribute_ranges(ranges, schedule):
+    """Host time (ns) of every traced layer call and of each of its stages,
+    walking the "saga_layer" ranges in the order the schedule lists the
+    calls.  Each layer range must hold its stages' ranges "saga stage 0"
+    .. "saga stage n-1", in order and nested inside it; anything else
+    raises ValueError.  Returns ({(workload, layer): [ns]},
+    {(workload, layer, stage): [ns]})."""
+    calls = []
+    for w in schedule:
+        for _ in range(w["calls"]):
+            for li, stages in enumerate(w["layers"]):
+                calls.append((w["workload"], li + 1, stages))
+    layers = [r for r in ranges if r[0] == "saga_layer"]
+    stage_r = [r for r in ranges if r[0].startswith("saga stage ")]
+    if len(layers) != len(calls):
+        raise ValueError(f"trace holds {len(layers)} layer ranges, the schedule {len(calls)} calls")
+    lay, acc = collections.defaultdict(list), collections.defaultdict(list)
+    si = 0
+    for (wl, li, names), (_, t0, t1) in zip(calls, layers):
+        lay[(wl, li)].append(t1 - t0)
+        for k, nm in enumerate(names):
+            if si >= len(stage_r):
+                raise ValueError("fewer stage ranges than the schedule's stages")
+            rn, s0, s1 = stage_r[si]
+            if rn != f"saga stage {k}" or s0 < t0 or s1 > t1:
+                raise ValueError(f"range {si} ({rn}) is not stage {k} of its layer call")
+            acc[(wl, li, nm)].append(s1 - s0)
+            si += 1
+    if si != len(stage_r):
+        raise ValueError(f"{len(stage_r) - si} stage ranges outside the traced calls")
+    return lay, acc
+
+
+def markers_main(a):
+    """Summary of the roctx ranges ("saga_layer", "saga stage k") of a
+    --marker-trace run of the suite: host time per layer call and stage."""
+    schedule = json.load(open(a.suite))
+    lay, acc = attribute_ranges(marker_ranges(a.markers), schedule)
+    med = lambda v: sorted(v)[(len(v) - 1) // 2] / 1e3  # noqa: E731
+    lines = ["# roctx ranges of the traced saga_layer calls: the suite workloads (float32)", "",
+             f"command: {a.command}",
+             "summary: python -m paper_2009_00804_amd.profiling --suite OUT/schedule.json "
+             "--markers OUT --command '...' --out profiles", "",
+             "Each layer call is one \"saga_layer\" range holding one \"saga stage k\" range per",
+             "stage, in order; every range was checked against the call schedule. The ranges",
+             "bracket the host side of each call (argument checks and kernel enqueue; the GPU",
+             "work runs asynchronously). Host microseconds, median and max over the calls; the",
+             "run traces markers only (a kernel trace adds a per-dispatch cost to these times).", "",
+             f"{'workload':10s} {'layer':>5s} {'stage':28s} {'calls':>6s} {'median us':>10s} "
+             f"{'max us':>10s}"]
+    for w in schedule:
+        for li, stages in enumerate(w["layers"]):
+            v = lay[(w["workload"], li + 1)]
+            lines.append(f"{w['workload']:10s} {li + 1:5d} {'(whole call)':28s} {len(v):6d} "
+                         f"{med(v):10.1f} {max(v) / 1e3:10.1f}")
+            for st in stages:
+                v = acc[(w["workload"], li + 1, st)]
+                lines.append(f"{'':10s} {'':5s} {st:28s} {len(v):6d} {med(v):10.1f} "
+                             f"{max(v) / 1e3:10.1f}")
+    with open(os.path.join(a.out, "marker_ranges_suite_f32.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def suite_main(a):
@@ -345,8 +423,11 @@ def main():
     ap.add_argument("--tag", default="gcn_rmat21")
     ap.add_argument("--counters", help="comma-separated --pmc output directories (counter mode)")
     ap.add_argument("--passes", default="", help="the counters of each pass, for the header")
+    ap.add_argument("--markers", help="--marker-trace output directory (with --suite: range mode)")
     a = ap.parse_args()
     os.makedirs(a.out, exist_ok=True)
+    if a.suite and a.markers:
+        return markers_main(a)
     if a.suite:
         return suite_counters_main(a) if a.counters else suite_main(a)
     if a.counters:

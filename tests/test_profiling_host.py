@@ -76,3 +76,26 @@ def test_short_names_drop_namespaces_and_arguments():
     assert P._short("saga::(anonymous namespace)::k_stage_mark()").startswith("k_stage_mark")
     assert P._short("void saga::(anonymous namespace)::k_combine<float>(saga::GatherArgs)") == \
         "k_combine<float>"
+
+
+def test_marker_ranges_attributed_to_layer_calls_and_stages():
+    """roctx ranges of a marker trace: each "saga_layer" range holds its
+    stages' "saga stage k" ranges in order; host times are attributed to
+    (workload, layer, stage) in the schedule's call order."""
+    sched = [{"workload": "w", "layers": [["a", "b"], ["c"]], "calls": 2}]
+    rng = []
+    t = 0
+    for _ in range(2):
+        rng.append(("saga_layer", t, t + 100))
+        rng += [("saga stage 0", t + 5, t + 40), ("saga stage 1", t + 45, t + 95)]
+        rng.append(("saga_layer", t + 200, t + 260))
+        rng.append(("saga stage 0", t + 210, t + 250))
+        t += 1000
+    lay, acc = P.attribute_ranges(sorted(rng, key=lambda x: (x[1], -x[2])), sched)
+    assert lay == {("w", 1): [100, 100], ("w", 2): [60, 60]}
+    assert acc == {("w", 1, "a"): [35, 35], ("w", 1, "b"): [50, 50], ("w", 2, "c"): [40, 40]}
+    bad = [r if r[1] != 45 else ("saga stage 1", 45, 150) for r in rng]  # stage outside its call
+    with pytest.raises(ValueError):
+        P.attribute_ranges(sorted(bad, key=lambda x: (x[1], -x[2])), sched)
+    with pytest.raises(ValueError):
+        P.attribute_ranges(sorted(rng, key=lambda x: (x[1], -x[2]))[:-2], sched)
