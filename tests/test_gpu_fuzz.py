@@ -358,3 +358,70 @@ def test_fuzz_layers(case):
         y = to_np(LY.run([layer], dev_padded(X)))
         want = O.gat_layer(rp, col, X, W, al, ar, b, H, "mean" if mean else "concat", act)
         assert rel_err(y, want) <= FP32_TOL
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_fuzz_gather_transform(case):
+    """The Gather with the next layer's transform fused in (Sec. 4, cross-stage
+    pipelining) over random graphs, plan options, widths of one to four
+    whole 128-byte lines, 1 to 64 output columns, split outputs, SUM or MEAN
+    with the epilogue, and an optional row scale."""
+    import ctypes as C
+
+    from gpu_util import device
+    from test_gpu_ops import ACTS, _transform_ref
+
+    S = lib()
+    rng = np.random.default_rng(8000 + case)
+    rp, col, V, Vs, kind = _random_graph(rng)
+    T = int(rng.choice([1, 2, 3, 5, 8, 16, 33, 64, 512]))
+    c = int(rng.integers(1, 9))
+    B = T + c + int(rng.choice([0, 1, 7, 100, 1000]))
+    g = graph(rp, col, num_src=Vs, seg_len=T, block_cost=B, row_cost=c)
+    dtype = str(rng.choice(["f32", "bf16"]))
+    es = 4 if dtype == "f32" else 2
+    F = int(rng.integers(1, 5)) * 128 // es
+    N = int(rng.integers(1, 65))
+    epv = 16 // es
+    split = 0
+    if N > epv and rng.random() < 0.5:
+        split = int(rng.integers(1, (N - 1) // epv + 1)) * epv
+    red = str(rng.choice(["sum", "mean"]))
+    dn = int(rng.integers(0, 2))
+    act = str(rng.choice(["none", "relu", "tanh"]))
+    rsd = rng.integers(0, 50, V).astype(np.int32) if rng.random() < 0.6 else None
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    X = rng.standard_normal((Vs, F)).astype(np.float32)
+    W = (rng.standard_normal((F, N)) / np.sqrt(F)).astype(np.float32)
+    if dtype == "bf16":
+        X, W = _bf16_round(X), _bf16_round(W)
+    bias = rng.standard_normal(F)
+    print(f"fuzz gather+transform {case}: {kind} V={V} Vs={Vs} seg_len={T} block_cost={B} "
+          f"row_cost={c} {dtype} F={F} N={N} split={split} {red} dst_norm={dn} {act} "
+          f"row_scale={rsd is not None}", flush=True)
+    op = S.saga_edge_op(S.SAGA_MSG_COPY, {"sum": S.SAGA_RED_SUM, "mean": S.SAGA_RED_MEAN}[red],
+                        S.dtype_code(tdt), 1, 0, dn, 0.0, ACTS[act])
+    Xt, Wt = dev_padded(X, tdt), torch.from_numpy(W).to(tdt).to(device()).contiguous()
+    b_t = torch.from_numpy(bias.astype(np.float32)).to(device())
+    rs_t = torch.from_numpy(rsd).to(device()) if rsd is not None else None
+    inp = S.saga_edge_inputs()
+    inp.src = S.cmat(Xt)
+    inp.bias = b_t.data_ptr()
+    out = dev_padded(np.zeros((V, split if split else N)), dtype=tdt, fill=7.0)
+    tail = dev_padded(np.zeros((V, N - split)), dtype=tdt, fill=7.0) if split else None
+    nx = S.saga_next_transform()
+    nx.w = S.cmat(Wt)
+    nx.row_scale_deg = rs_t.data_ptr() if rs_t is not None else None
+    nx.split_col = split
+    if split:
+        nx.tail = S.mat(tail)
+    ws = S.workspace(S.saga_gather_transform_workspace_size(g.plan, op, F), device())
+    S.saga_scatter_apply_edge_gather_transform(g.plan, op, inp, nx, S.mat(out),
+                                               C.c_void_p(ws.data_ptr()), ws.numel(),
+                                               S.stream_handle())
+    torch.cuda.synchronize()
+    got = to_np(out) if not split else np.concatenate([to_np(out), to_np(tail)], axis=1)
+    ref, h = _transform_ref(rp, col, X, red, dn, bias, act, Vs, W, rsd, dtype)
+    tol = FP32_TOL if dtype == "f32" else BF16_TOL
+    assert got.shape == ref.shape
+    assert rel_err(got, ref) <= tol

@@ -592,11 +592,15 @@ def test_gather_maximum_widths(dtype, F):
         run_gather(g, wider, dict(reduce=S.SAGA_RED_SUM), limit + 1, tdt)
 
 
-def _transform_ref(rp, col, X, red, dn, bias, act, n, W, rs_deg):
+def _transform_ref(rp, col, X, red, dn, bias, act, nsrc, W, rs_deg, dtype="f32"):
     """out[v] = rs(v) * (h_v W) with h the Gather output (the fused call's
-    definition), from the oracle's Gather and a float64 product."""
-    h = _ref_simple(rp, col, X, red, "copy", dn, bias, act, n)
-    rs = O.degree_scale(rs_deg) if rs_deg is not None else np.ones(n)
+    definition), from the oracle's Gather and a float64 product.  In bf16, h
+    is a stored intermediate of the call, so it is taken rounded to bf16
+    (the bf16 contract: storage in bf16, arithmetic in float64 here)."""
+    h = _ref_simple(rp, col, X, red, "copy", dn, bias, act, nsrc)
+    if dtype == "bf16":
+        h = _bf16_round(h.astype(np.float32)).astype(np.float64)
+    rs = O.degree_scale(rs_deg) if rs_deg is not None else np.ones(h.shape[0])
     return O.dense(h, W) * rs[:, None], h
 
 
@@ -642,7 +646,7 @@ def test_gather_transform_fused(gname, dtype, F, N, split):
                                                    C.c_void_p(ws.data_ptr()), ws.numel(), S.stream_handle())
         torch.cuda.synchronize()
         got = to_np(out) if not split else np.concatenate([to_np(out), to_np(tail)], axis=1)
-        ref, h = _transform_ref(rp, col, X, red, dn, bias, act, n, W, rsd)
+        ref, h = _transform_ref(rp, col, X, red, dn, bias, act, n, W, rsd, dtype)
         mag = O.dense(np.abs(h), np.abs(W)) * (O.degree_scale(rsd)[:, None] if rsd is not None else 1.0)
         assert rel_err(got, ref) <= tol
         assert rel_err_terms(got, ref, mag) <= tol
