@@ -64,6 +64,36 @@ def test_version_and_status_strings(S):
     assert L.saga_status_str(S.SAGA_EGRAPH) == b"invalid graph"
 
 
+def test_error_detail_is_per_thread(S):
+    """saga_last_error is thread-local: two threads that fail in different
+    ways each read back their own detail, and a success in one thread
+    clears only that thread's."""
+    import threading
+
+    L = S.lib()
+    bar = threading.Barrier(2)
+    seen = {}
+
+    def worker(name, fail):
+        fail()
+        bar.wait()  # both threads have failed before either reads
+        seen[name] = L.saga_last_error().decode()
+        bar.wait()
+        if name == "a":
+            assert L.saga_plan_workspace_size(10, 10, 5, None, C.byref(C.c_size_t())) == S.SAGA_OK
+        bar.wait()
+        seen[name + "2"] = L.saga_last_error().decode()
+
+    out = C.c_size_t()
+    ta = threading.Thread(target=worker, args=("a", lambda: L.saga_plan_workspace_size(
+        10, 10, -1, None, C.byref(out))))
+    tb = threading.Thread(target=worker, args=("b", lambda: L.saga_plan_workspace_size(
+        10, 10, 5, None, None)))
+    ta.start(); tb.start(); ta.join(); tb.join()
+    assert "out of range" in seen["a"] and "null" in seen["b"], seen
+    assert seen["a2"] == "" and seen["b2"] == seen["b"], seen
+
+
 def test_plan_workspace_size_rules(S):
     n = S.saga_plan_workspace_size(1000, 1000, 5000)
     assert n > 0 and n % 256 == 0
