@@ -165,6 +165,52 @@ def test_gather_attention(gname, heads, D, head_mean):
     assert rel_err(to_np(out), ref) <= FP32_TOL
 
 
+def test_concurrent_calls_from_two_threads():
+    """Two host threads, each with its own stream and workspace, run Gathers
+    of different widths and reductions at the same time: each result equals
+    the same call made alone, byte for byte (no shared host state in the
+    launch path)."""
+    import threading
+
+    S = lib()
+    rp, col, n, g = _get_graph("rmat")
+    rng = np.random.default_rng(31)
+    X = {F: dev_padded(rng.standard_normal((n, F)).astype(np.float32)) for F in (32, 100)}
+    jobs = [(32, S.SAGA_RED_SUM), (100, S.SAGA_RED_MAX), (32, S.SAGA_RED_MEAN), (100, S.SAGA_RED_SUM)]
+
+    def run(F, red, stream):
+        op = S.saga_edge_op()
+        op.msg, op.reduce, op.dtype, op.heads = S.SAGA_MSG_COPY, red, S.SAGA_F32, 1
+        inp = S.saga_edge_inputs()
+        inp.src = S.cmat(X[F])
+        out = dev_padded(np.zeros((n, F)), fill=7.0)
+        ws = S.workspace(S.saga_gather_workspace_size(g.plan, op, F), device())
+        sh = S.stream_handle(stream)
+        for _ in range(5):
+            S.saga_scatter_apply_edge_gather(g.plan, op, inp, S.mat(out), C.c_void_p(ws.data_ptr()),
+                                             ws.numel(), sh)
+        S.saga_sync_check(sh)
+        return to_np(out)
+
+    alone = [run(F, red, torch.cuda.current_stream()) for F, red in jobs]
+    got = [None] * len(jobs)
+    streams = [torch.cuda.Stream() for _ in jobs]
+    torch.cuda.synchronize()
+
+    def worker(k):
+        for i in range(k, len(jobs), 2):
+            got[i] = run(*jobs[i], streams[i])
+
+    print("concurrent gathers from two threads", flush=True)
+    th = [threading.Thread(target=worker, args=(k,)) for k in range(2)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    for i in range(len(jobs)):
+        assert got[i] is not None and np.array_equal(got[i], alone[i]), i
+
+
 def test_sync_check_after_work_on_a_stream():
     """saga_sync_check waits for a side stream's work (a Gather enqueued
     there) and reports no device error; the output is then complete."""
