@@ -584,7 +584,9 @@ saga_status saga_apply_vertex(const saga_gemm_op* op, saga_cmat a, saga_cmat w,
  *           (rel: a rel plan of the same graph).
  * Weights are dense device matrices (ld = cols) in the layer dtype; biases
  * and attention vectors f32.  x: num_src x F_in (num_src == num_dst).
- * act applies to GCN, GAT and RGCN.
+ * act applies to GCN, GAT and RGCN.  GCN and RGCN take f32 or bf16; GAT,
+ * SAGE_POOL, SAGE_LSTM and GATED_GRU are float32 only (SAGA_EUNSUPPORTED
+ * for bf16).
  */
 typedef enum saga_layer_kind {
   SAGA_LAYER_GCN = 0,
