@@ -306,6 +306,12 @@ def test_layer_rejects_bad_descriptors(S):
     d.w = d.attn_l = d.attn_r = 0x1000
     n = C.c_size_t()
     assert L.saga_layer_workspace_size(C.byref(p), C.byref(d), C.byref(n)) == S.SAGA_EUNSUPPORTED
+    # the other float32-only kinds refuse bf16 the same way
+    for kind in (S.SAGA_LAYER_SAGE_POOL, S.SAGA_LAYER_SAGE_LSTM, S.SAGA_LAYER_GATED_GRU):
+        e = S.saga_layer_desc()
+        e.kind, e.dtype, e.in_feat, e.out_feat, e.hidden = kind, S.SAGA_BF16, 8, 8, 32
+        e.w = e.w_pool = e.w_ih = e.w_hh = e.w_e = 0x1000
+        assert L.saga_layer_workspace_size(C.byref(p), C.byref(e), C.byref(n)) == S.SAGA_EUNSUPPORTED
     d.kind = 9
     assert L.saga_layer_workspace_size(C.byref(p), C.byref(d), C.byref(n)) == S.SAGA_EINVAL
     d.kind = S.SAGA_LAYER_GCN
