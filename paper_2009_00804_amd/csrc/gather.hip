@@ -257,10 +257,12 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
 }
 
 // The plain sum over whole slices of a source below 4 GiB (the GCN Gather):
-// built for seven waves per SIMD, which its registers allow without spills
-// (bfloat16 rows otherwise take 74 registers, six waves).
+// built for eight waves per SIMD, which its registers allow without spills
+// with four row loads in flight per lane (56 registers float32, 64
+// bfloat16).  Measured on the 2^21 graph, 128 bfloat16 columns: 2.38 ms,
+// against 2.47 with eight loads in flight at seven waves.
 template <typename T, int LPR, int VPL, int U, int CPL>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(7))) void k_gather_sum(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(8))) void k_gather_sum(
     GatherArgs a, int nslices, int slice0) {
   gather_simple_body<T, LPR, VPL, U, CPL, false, kWNone, true, false, true>(a, nslices, slice0);
 }
@@ -864,7 +866,12 @@ int concurrent_slices(const GatherArgs& a, int nslices, int slice_bytes_) {
 
 template <typename T, int LPR, int VPL>
 hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, hipStream_t st) {
+  // row loads in flight per lane: bfloat16 rows of one 16-byte vector per
+  // lane keep eight in flight (the narrow layer-2 Gather: 1.45 against 1.58
+  // ms with four); the sliced sum (k_gather_sum, built for eight waves per
+  // SIMD) keeps four
   constexpr int U = LPR >= 8 ? (VPL == 1 && sizeof(T) == 2 ? 8 : 4) : LPR;
+  constexpr int US = LPR >= 8 ? 4 : LPR;
   constexpr int CPL = LPR >= 32 ? 1 : (LPR >= 8 ? 4 : 8);
   int conc = concurrent_slices(a, nslices, LPR * VPL * 16);
   if (conc <= 0 || conc > nslices || nslices % conc != 0) conc = nslices;
@@ -902,7 +909,7 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
       // (whole slices of at most 128 bytes: wider lane groups never take
       // this path with 128-byte slices, and are not built)
       if constexpr (LPR <= 8)
-        hipLaunchKernelGGL((k_gather_sum<T, LPR, VPL, U, CPL>), grid, dim3(kThreads), 0, st, a,
+        hipLaunchKernelGGL((k_gather_sum<T, LPR, VPL, US, CPL>), grid, dim3(kThreads), 0, st, a,
                            conc, s0);
     } else {
       SAGA_LAUNCH_FULL(false, kWNone);
@@ -1049,7 +1056,7 @@ hipError_t launch_xf(const GatherArgs& a, unsigned grid, int nslices, hipStream_
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // the earlier slices, one launch each; U as in the plain sliced Gather
-  constexpr int U = sizeof(T) == 2 ? 8 : 4;
+  constexpr int U = 4;
   for (int s0 = 0; s0 < nslices - 1; ++s0) {
     hipLaunchKernelGGL((k_gather_sum<T, 8, 1, U, 4>), dim3(grid), dim3(kThreads), 0, st, a, 1, s0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
