@@ -60,7 +60,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 STAGES = {
     "gather1": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4>", 4, 5, (0, 1, 2, 3)),
                          ("k_combine<float>", 1, 3, (0,))],
-                 "bf16": [("k_gather_sum<unsigned short, 8, 1, 8, 4>", 2, 2, (0, 1)),
+                 "bf16": [("k_gather_sum<unsigned short, 8, 1, 4, 4>", 2, 2, (0, 1)),
                           ("k_combine<unsigned short>", 1, 2, (0,))]},
                 "gather.hip"),
     "gather2": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4>", 1, 5, (4,)),
