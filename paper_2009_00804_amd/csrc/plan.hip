@@ -149,19 +149,22 @@ __global__ __launch_bounds__(kThreads) void k_degrees(const int32_t* __restrict_
 // ------------------------------------------------------------------------
 // Out-degrees without global atomics.  A power-law graph sends a large share
 // of all edges to a few hub sources, and same-address atomics serialize, so
-// instead: (1) histogram the CSR source ids by bucket (8192 ids per bucket)
-// per tile, (2) scan, (3) scatter the ids into bucket order as 16-bit
-// offsets within their bucket, (4) count each bucket in a 32 KB LDS
-// histogram and store the counts.
+// instead: (1) each tile of kOdTile CSR entries is sorted by bucket (the
+// source id's high bits, kOdBucket ids per bucket) in LDS and written back
+// to its own place in one contiguous piece, as 16-bit offsets within the
+// bucket, with the start of every bucket's run in the tile; (2) per bucket,
+// workgroups count their share of the tiles' runs into an LDS histogram and
+// store it; (3) the partial histograms are summed.  Counting is order-free,
+// so no global scan is needed and every global write is contiguous.
 // ------------------------------------------------------------------------
 // Tile of this workgroup in an XCD-blocked order.  Workgroups are handed to
 // the eight XCDs in turn (w % 8), so with tile = w the tiles one L2 sees are
-// eight apart, and the tile-minor histogram entries of neighbouring tiles
-// (32 to a 128-byte line) are written and read as partial lines through
-// eight different L2s.  Here XCD x takes the contiguous run
-// [x * per, (x + 1) * per) of tiles.  The grid is xcd_grid(ntiles)
-// workgroups; the spare ones get -1.  Any dispatch order gives the same
-// result; only the locality depends on it.
+// eight apart, and the tile-minor entries of neighbouring tiles (32 to a
+// 128-byte line) are written and read as partial lines through eight
+// different L2s.  Here XCD x takes the contiguous run [x * per, (x + 1) *
+// per) of tiles.  The grid is xcd_grid(ntiles) workgroups; the spare ones
+// get -1.  Any dispatch order gives the same result; only the locality
+// depends on it.
 constexpr int kXcds = 8;
 __device__ __forceinline__ int64_t xcd_tile(int64_t ntiles) {
   const int64_t per = (ntiles + kXcds - 1) / kXcds;
@@ -172,95 +175,96 @@ inline unsigned xcd_grid(int64_t ntiles) {
   return (unsigned)(kXcds * ((ntiles + kXcds - 1) / kXcds));
 }
 
-constexpr int kBucketBits = 13;
-constexpr int kBucketSize = 1 << kBucketBits;
-constexpr int kMaxBuckets = 2048;  // keeps the scatter's LDS within 64 KB
-constexpr int kEdgeItems = 32;
-constexpr int kEdgeTile = kThreads * kEdgeItems;  // 8192 edges per tile
+// Shapes measured on the 2^21-source R-MAT graph (E = 1.07e8), whole
+// out-degree count: 16,384 ids per bucket and tiles of 16,384 entries; the
+// count with about 1024 workgroups (two per CU, 64 KB of LDS each), each
+// wave reading 4 tiles' runs at a time, 256 entries of each before counting.
+// 8,192 or 32,768 ids per bucket, 256 or 512 count workgroups, 8 x 2 or
+// 16 x 1 runs x loads, 32-bit loads of entry pairs, and persistent bin
+// workgroups that prefetch their next tile were all slower.
+constexpr int kOdBits = 14;
+constexpr int kOdBucket = 1 << kOdBits;
+constexpr int64_t kOdMaxSources = int64_t(1) << 23;  // larger graphs count in k_degrees
+constexpr int kOdMaxBuckets = (int)(kOdMaxSources >> kOdBits);
+constexpr int kOdThreads = 512, kOdWaves = kOdThreads / 64;
+constexpr int kOdItems = 32;
+constexpr int kOdTile = kOdThreads * kOdItems;  // 16384 entries per tile
+constexpr int kOdCountWgs = 1024, kOdRuns = 4, kOdLoads = 4;
+static_assert(kOdBits <= 15, "the count's LDS histogram holds 2^15 counters");
+static_assert(kOdTile <= 65536, "16-bit offsets");
+static_assert(64 * kOdItems < 0xffff, "16-bit ranks within a wave");
+// workgroups per bucket in the count: about kOdCountWgs workgroups in all
+inline int outdeg_split(int64_t nb) {
+  const int64_t s = nb >= kOdCountWgs || nb < 1 ? 1 : kOdCountWgs / nb;
+  return (int)(s > 16 ? 16 : s);
+}
+inline size_t outdeg_bin_lds(int nb) {
+  return (size_t)kOdWaves * nb * 4 + (size_t)kOdTile * 2;
+}
+static_assert((size_t)kOdWaves * kOdMaxBuckets * 4 + (size_t)kOdTile * 2 + 64 <= 65536,
+              "the bin kernel's LDS stays within 64 KB");
 
-// per-tile bucket histogram; each wave counts into its own copy (fewer
-// same-address LDS atomics), the copies are summed at the end
-__global__ __launch_bounds__(kThreads) void k_outdeg_hist(const int32_t* __restrict__ col,
-                                                          int64_t E, int32_t Vs, int nb,
-                                                          int32_t* __restrict__ hist,
-                                                          int64_t ntiles, int32_t* counts) {
-  extern __shared__ int32_t h[];  // [kThreads / 64][nb]
-  constexpr int NW = kThreads / 64;
+// Sort one tile by bucket.  Each wave ranks its own entries with counters
+// of its own, laid out wave-major (a wave's lanes hit nb consecutive words);
+// the bucket-major scan over (bucket, wave) then places bucket b's entries of
+// wave 0, 1, ... one after another.  loc[b * ntiles + tile] is the start of
+// bucket b's run within the tile, loc[nb * ntiles + tile] the tile's valid
+// entries.  Source ids outside [0, Vs) raise error bit 8 and are left out.
+// The loads are unconditional (E > 0, so a tile holds at least one entry):
+// an entry past the tile's end reads the tile's last one and is then
+// ignored, so no branch splits the batch of loads.
+__global__ __launch_bounds__(kOdThreads) void k_outdeg_bin(const int32_t* __restrict__ col,
+                                                           int64_t E, int32_t Vs, int nb,
+                                                           int64_t ntiles,
+                                                           uint16_t* __restrict__ out,
+                                                           int32_t* __restrict__ loc,
+                                                           int32_t* counts) {
+  extern __shared__ int32_t sm[];
+  int32_t* cnt = sm;  // [kOdWaves][nb]
+  uint16_t* sval = reinterpret_cast<uint16_t*>(sm + kOdWaves * nb);  // [kOdTile]
+  __shared__ int32_t wsum[kOdWaves];
   const int64_t tile = xcd_tile(ntiles);
   if (tile < 0) return;
-  for (int b = threadIdx.x; b < NW * nb; b += kThreads) h[b] = 0;
-  __syncthreads();
-  int32_t* hw = h + (threadIdx.x >> 6) * nb;
-  int err = 0;
-  const int64_t base = tile * (int64_t)kEdgeTile;
-  int32_t c[kEdgeItems];
+  const int tx = threadIdx.x, wave = tx >> 6, lane = tx & 63;
+  const int64_t base = tile * (int64_t)kOdTile;
+  const int n = E - base < kOdTile ? (int)(E - base) : kOdTile;
+  for (int b = tx; b < kOdWaves * nb; b += kOdThreads) cnt[b] = 0;
+  const int32_t* p = col + base;
+  int32_t c[kOdItems];
+  if (n == kOdTile) {
 #pragma unroll
-  for (int j = 0; j < kEdgeItems; ++j) {
-    const int64_t i = base + j * kThreads + threadIdx.x;
-    c[j] = i < E ? __builtin_nontemporal_load(col + i) : -1;
-  }
+    for (int j = 0; j < kOdItems; ++j) c[j] = __builtin_nontemporal_load(p + j * kOdThreads + tx);
+  } else {
 #pragma unroll
-  for (int j = 0; j < kEdgeItems; ++j) {
-    const int64_t i = base + j * kThreads + threadIdx.x;
-    if (i < E) {
-      if (c[j] < 0 || c[j] >= Vs)
-        err |= 8;
-      else
-        atomicAdd(&hw[c[j] >> kBucketBits], 1);
+    for (int j = 0; j < kOdItems; ++j) {
+      const int i = j * kOdThreads + tx;
+      c[j] = __builtin_nontemporal_load(p + (i < n ? i : n - 1));
     }
   }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) err |= __shfl_xor(err, off, 64);
-  if ((threadIdx.x & 63) == 0 && err) atomicOr(&counts[kErrFlags], err);
   __syncthreads();
-  for (int b = threadIdx.x; b < nb; b += kThreads) {
-    int32_t t = 0;
+  // rank within (wave, bucket), two 16-bit ranks to a register (a wave
+  // ranks at most 64 * kOdItems entries); 0xffff marks no entry
+  int32_t* cw = cnt + wave * nb;
+  uint32_t r[kOdItems / 2];
+  int err = 0;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) t += h[w * nb + b];
-    hist[(int64_t)b * ntiles + tile] = t;
+  for (int j = 0; j < kOdItems; ++j) {
+    const bool in = j * kOdThreads + tx < n;
+    const bool ok = in && c[j] >= 0 && c[j] < Vs;
+    err |= in && !ok;
+    const uint32_t rj = ok ? (uint32_t)atomicAdd(&cw[c[j] >> kOdBits], 1) : 0xffffu;
+    r[j / 2] = j % 2 ? r[j / 2] | rj << 16 : rj;
   }
-}
-
-// Scatter one tile into bucket order.  The tile is first ranked by bucket in
-// LDS, then written out so that consecutive threads store consecutive
-// positions of one bucket (coalesced 16-bit stores).  `offs` is the
-// exclusive scan of hist in bucket-major order, so the tile's count in
-// bucket b is offs[b * ntiles + tile + 1] - offs[b * ntiles + tile].
-__global__ __launch_bounds__(kThreads) void k_outdeg_scatter(const int32_t* __restrict__ col,
-                                                             int64_t E, int nb,
-                                                             const int32_t* __restrict__ offs,
-                                                             int64_t ntiles,
-                                                             uint16_t* __restrict__ out,
-                                                             int32_t* counts) {
-  if (counts[kErrFlags]) return;
-  extern __shared__ int32_t sm[];
-  __shared__ int s_bad;
-  int32_t* gbase = sm;            // [nb] global start of this tile's run in bucket b
-  int32_t* lbase = sm + nb;       // [nb] local start of bucket b within the tile
-  int32_t* cur = sm + 2 * nb;     // [nb] local cursor
-  uint16_t* sval = reinterpret_cast<uint16_t*>(sm + 3 * nb);  // [kEdgeTile]
-  uint16_t* sbkt = sval + kEdgeTile;                           // [kEdgeTile]
-  const int64_t tile = xcd_tile(ntiles);
-  if (tile < 0) return;
-  const int64_t base = tile * (int64_t)kEdgeTile;
-  const int n = (int)(E - base < kEdgeTile ? E - base : kEdgeTile);
-  for (int b = threadIdx.x; b < nb; b += kThreads) {
-    const int64_t f = (int64_t)b * ntiles + tile;
-    const int32_t g0 = offs[f];
-    const int32_t g1 = f + 1 < (int64_t)nb * ntiles ? offs[f + 1] : (int32_t)E;
-    gbase[b] = g0;
-    cur[b] = g1 - g0;  // count, scanned below
-  }
+  if (__any(err) && lane == 0) atomicOr(&counts[kErrFlags], 8);
   __syncthreads();
-  {  // exclusive scan of the tile's bucket counts: thread t owns buckets
-     // [t * per, (t + 1) * per), then a wave scan and a cross-wave pass
-    __shared__ int32_t wsum[kThreads / 64];
-    const int per = (nb + kThreads - 1) / kThreads;
-    const int b0 = threadIdx.x * per;
+  {  // exclusive scan over k = b * kOdWaves + w (entry cnt[w * nb + b]):
+     // thread t owns k in [t * pk, (t + 1) * pk), then a wave scan and a
+     // cross-wave pass
+    const int m = kOdWaves * nb;
+    const int pk = (m + kOdThreads - 1) / kOdThreads;
+    const int k0 = tx * pk;
     int32_t own = 0;
-    for (int k = 0; k < per; ++k)
-      if (b0 + k < nb) own += cur[b0 + k];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int k = k0; k < k0 + pk && k < m; ++k) own += cnt[(k % kOdWaves) * nb + k / kOdWaves];
     int32_t inc = own;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -271,101 +275,105 @@ __global__ __launch_bounds__(kThreads) void k_outdeg_scatter(const int32_t* __re
     __syncthreads();
     int32_t run = inc - own;
     for (int w = 0; w < wave; ++w) run += wsum[w];
-    int32_t total = 0;
-    for (int w = 0; w < kThreads / 64; ++w) total += wsum[w];
-    for (int k = 0; k < per; ++k)
-      if (b0 + k < nb) {
-        const int32_t c = cur[b0 + k];
-        lbase[b0 + k] = run;
-        cur[b0 + k] = run;
-        run += c;
-      }
-    if (threadIdx.x == 0) {
-      s_bad = total != n;
-      if (s_bad) atomicOr(&counts[kErrFlags], kErrInternal);
+    for (int k = k0; k < k0 + pk && k < m; ++k) {
+      const int a = (k % kOdWaves) * nb + k / kOdWaves;
+      const int32_t v = cnt[a];
+      cnt[a] = run;
+      if (k % kOdWaves == 0) loc[(int64_t)(k / kOdWaves) * ntiles + tile] = run;
+      run += v;
     }
+    if (tx == kOdThreads - 1) loc[(int64_t)nb * ntiles + tile] = run;
   }
   __syncthreads();
-  if (s_bad) return;
-  int32_t c[kEdgeItems];
+  int32_t total = 0;
+  for (int w = 0; w < kOdWaves; ++w) total += wsum[w];
 #pragma unroll
-  for (int j = 0; j < kEdgeItems; ++j) {
-    const int64_t i = base + j * kThreads + threadIdx.x;
-    c[j] = i < E ? __builtin_nontemporal_load(col + i) : 0;
-  }
-#pragma unroll
-  for (int j = 0; j < kEdgeItems; ++j) {
-    if (j * kThreads + (int)threadIdx.x < n) {
-      const int b = c[j] >> kBucketBits;
-      const int32_t p = atomicAdd(&cur[b], 1);
-      if (p >= 0 && p < n) {
-        sval[p] = (uint16_t)(c[j] & (kBucketSize - 1));
-        sbkt[p] = (uint16_t)b;
-      }
-    }
+  for (int j = 0; j < kOdItems; ++j) {
+    const uint32_t rj = r[j / 2] >> (16 * (j % 2)) & 0xffffu;
+    if (rj != 0xffffu) sval[cw[c[j] >> kOdBits] + (int)rj] = (uint16_t)(c[j] & (kOdBucket - 1));
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < n; i += kThreads) {
-    const int b = sbkt[i];
-    const int64_t g = (int64_t)gbase[b] + (i - lbase[b]);
-    if (g >= 0 && g < E)
-      out[g] = sval[i];
-    else
-      atomicOr(&counts[kErrFlags], kErrInternal);
-  }
+  // the tile's sorted entries, 8 to a 16-byte store
+  const int nv = total >> 3;
+  uint4* out4 = reinterpret_cast<uint4*>(out + base);
+  const uint4* s4 = reinterpret_cast<const uint4*>(sval);
+  for (int i = tx; i < nv; i += kOdThreads) out4[i] = s4[i];
+  for (int i = nv * 8 + tx; i < total; i += kOdThreads) out[base + i] = sval[i];
 }
 
-// kOutdegSplit workgroups per bucket, each counting one slice of the
-// bucket into LDS and storing its partial histogram (a hub's occurrences are
-// split over the workgroups, so same-address LDS atomics stay few per CU)
-constexpr int kOutdegSplit = 8;
-
-__global__ __launch_bounds__(1024) void k_outdeg_count(const uint16_t* __restrict__ bucketed,
-                                                       const int32_t* __restrict__ offs,
+// Bucket b's entries, from the runs of tiles [t0, t1) (slice s of
+// outdeg_split(nb)), counted into LDS; the histogram goes to
+// part[s][b * kOdBucket + i].  Each wave takes R tiles at a time and reads
+// the first J * 64 entries of each run before counting, so that R * J loads
+// are in flight; longer runs finish in a loop.
+__global__ __launch_bounds__(1024) void k_outdeg_count(const uint16_t* __restrict__ bk,
+                                                       const int32_t* __restrict__ loc,
                                                        int64_t ntiles, int nb, int64_t E,
-                                                       int32_t Vs, int32_t* __restrict__ part,
+                                                       int32_t* __restrict__ part,
                                                        const int32_t* counts) {
   if (counts[kErrFlags]) return;
-  __shared__ int32_t h[kBucketSize];
-  const int b = blockIdx.y, w = blockIdx.x;
-  for (int i = threadIdx.x; i < kBucketSize; i += 1024) h[i] = 0;
+  __shared__ int32_t h[kOdBucket];
+  constexpr int R = kOdRuns, J = kOdLoads, NW = 1024 / 64;
+  const int b = blockIdx.x, s = blockIdx.y, S = gridDim.y;
+  for (int i = threadIdx.x; i < kOdBucket; i += 1024) h[i] = 0;
   __syncthreads();
-  int64_t lo = offs[(int64_t)b * ntiles];
-  int64_t hi = b + 1 < nb ? (int64_t)offs[(int64_t)(b + 1) * ntiles] : E;
-  lo = lo < 0 ? 0 : (lo > E ? E : lo);
-  hi = hi < lo ? lo : (hi > E ? E : hi);
-  const int64_t n = hi - lo;
-  const int64_t s0 = lo + n * w / kOutdegSplit, s1 = lo + n * (w + 1) / kOutdegSplit;
-  constexpr int kB = 8;  // loads in flight per thread before the LDS atomics
-  for (int64_t i0 = s0; i0 < s1; i0 += 1024 * kB) {
-    int32_t v[kB];
+  const int64_t t0 = ntiles * s / S, t1 = ntiles * (s + 1) / S;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int32_t* lb = loc + (int64_t)b * ntiles;
+  const int32_t* le = loc + (int64_t)(b + 1) * ntiles;
+  for (int64_t tg = t0 + (int64_t)wave * R; tg < t1; tg += (int64_t)NW * R) {
+    int64_t beg[R];
+    int32_t len[R];
 #pragma unroll
-    for (int j = 0; j < kB; ++j) {
-      const int64_t i = i0 + j * 1024 + threadIdx.x;
-      v[j] = i < s1 ? (int32_t)__builtin_nontemporal_load(bucketed + i) : -1;
+    for (int q = 0; q < R; ++q) {
+      const int64_t t = tg + q;
+      len[q] = 0;
+      beg[q] = 0;
+      if (t < t1) {
+        const int64_t tbase = t * (int64_t)kOdTile;
+        const int32_t n = (int32_t)(E - tbase < kOdTile ? E - tbase : kOdTile);
+        int32_t lo = lb[t], hi = le[t];
+        lo = lo < 0 ? 0 : (lo > n ? n : lo);
+        hi = hi < lo ? lo : (hi > n ? n : hi);
+        beg[q] = tbase + lo;
+        len[q] = hi - lo;
+      }
     }
+    uint32_t v[R][J];
 #pragma unroll
-    for (int j = 0; j < kB; ++j)
-      if (v[j] >= 0) atomicAdd(&h[v[j] & (kBucketSize - 1)], 1);
+    for (int q = 0; q < R; ++q)
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int k = j * 64 + lane;
+        v[q][j] = k < len[q] ? (uint32_t)bk[beg[q] + k] : 0xffffffffu;
+      }
+#pragma unroll
+    for (int q = 0; q < R; ++q)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+        if (v[q][j] != 0xffffffffu) atomicAdd(&h[v[q][j] & (kOdBucket - 1)], 1);
+#pragma unroll
+    for (int q = 0; q < R; ++q)
+      for (int k = J * 64 + lane; k < len[q]; k += 64)
+        atomicAdd(&h[bk[beg[q] + k] & (kOdBucket - 1)], 1);
   }
   __syncthreads();
-  const int64_t v0 = (int64_t)b << kBucketBits;
-  int32_t* pw = part + (int64_t)w * nb * kBucketSize + v0;
-  for (int i = threadIdx.x; i < kBucketSize; i += 1024) pw[i] = h[i];
+  int32_t* pw = part + (int64_t)s * nb * kOdBucket + (int64_t)b * kOdBucket;
+  for (int i = threadIdx.x; i < kOdBucket; i += 1024) pw[i] = h[i];
 }
 
+// d_out[v] = the sum of the S partial counts
 __global__ __launch_bounds__(kThreads) void k_outdeg_reduce(const int32_t* __restrict__ part,
-                                                            int nb, int32_t Vs,
+                                                            int nb, int S, int32_t Vs,
                                                             int32_t* __restrict__ d_out,
                                                             const int32_t* counts) {
   if (counts[kErrFlags]) return;
-  const int64_t stride = (int64_t)nb * kBucketSize;
+  const int64_t stride = (int64_t)nb * kOdBucket;
   for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < Vs;
        v += (int64_t)gridDim.x * blockDim.x) {
-    int32_t s = 0;
-#pragma unroll
-    for (int w = 0; w < kOutdegSplit; ++w) s += part[w * stride + v];
-    d_out[v] = s;
+    int32_t sum = 0;
+    for (int w = 0; w < S; ++w) sum += part[w * stride + v];
+    d_out[v] = sum;
   }
 }
 
@@ -625,12 +633,10 @@ bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t
   L->scan_tiles_rows = cdiv(V, kTile);
   L->scan_tiles_segs = cdiv(L->max_segments, kTile);
   const int64_t hist_n = (int64_t)kBins * L->radix_tiles;
-  L->outdeg_nb = cdiv(Vs, kBucketSize);
-  L->edge_tiles = cdiv(E, kEdgeTile);
-  L->outdeg_bucketed = L->outdeg_nb <= kMaxBuckets && E > 0;
+  L->outdeg_nb = cdiv(Vs, kOdBucket);
+  L->edge_tiles = cdiv(E, kOdTile);
+  L->outdeg_bucketed = L->outdeg_nb > 0 && L->outdeg_nb <= kOdMaxBuckets && E > 0;
   int64_t scan_tiles = cdiv(hist_n, kTile);
-  if (L->outdeg_bucketed && cdiv(L->outdeg_nb * L->edge_tiles, kTile) > scan_tiles)
-    scan_tiles = cdiv(L->outdeg_nb * L->edge_tiles, kTile);
   if (L->scan_tiles_rows > scan_tiles) scan_tiles = L->scan_tiles_rows;
   if (L->scan_tiles_segs > scan_tiles) scan_tiles = L->scan_tiles_segs;
 
@@ -651,15 +657,16 @@ bool plan_layout(int32_t V, int32_t Vs, int64_t E, int32_t T, int32_t B, int32_t
   L->off_counts = take(kCountSlots);
   L->off_scratch = o;
   // scratch: keysA, valsA, keysB, valsB, row begins A and B, hist, tile
-  // sums, cost prefix, bucketed source ids, bucket histogram
+  // sums, cost prefix, bucketed source ids, bucket run starts, partial
+  // out-degree histograms
+  const bool bk = L->outdeg_bucketed;
   take(V); take(V); take(V); take(V); take(V); take(V);
   take(hist_n);
   take(scan_tiles + 1);
-  take(L->outdeg_bucketed ? scan_tiles + 1 : 0);  // tile sums of the out-degree branch
   take(L->max_segments);
-  take(L->outdeg_bucketed ? cdiv(E, 2) : 0);
-  take(L->outdeg_bucketed ? L->outdeg_nb * L->edge_tiles : 0);
-  take(L->outdeg_bucketed ? (int64_t)kOutdegSplit * L->outdeg_nb * kBucketSize : 0);
+  take(bk ? cdiv(E, 2) : 0);
+  take(bk ? (L->outdeg_nb + 1) * L->edge_tiles : 0);
+  take(bk ? (int64_t)outdeg_split(L->outdeg_nb) * L->outdeg_nb * kOdBucket : 0);
   L->scratch_bytes = o - L->off_scratch;
   L->total = o;
   return true;
@@ -687,15 +694,13 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   int64_t scan_tiles = cdiv((int64_t)kBins * ntiles, kTile);
   if (L.scan_tiles_rows > scan_tiles) scan_tiles = L.scan_tiles_rows;
   if (L.scan_tiles_segs > scan_tiles) scan_tiles = L.scan_tiles_segs;
-  if (L.outdeg_bucketed && cdiv(L.outdeg_nb * L.edge_tiles, kTile) > scan_tiles)
-    scan_tiles = cdiv(L.outdeg_nb * L.edge_tiles, kTile);
   int32_t* tile_sums = reinterpret_cast<int32_t*>(take(scan_tiles + 1));
-  int32_t* tile_sums2 = reinterpret_cast<int32_t*>(take(L.outdeg_bucketed ? scan_tiles + 1 : 0));
   int32_t* P = reinterpret_cast<int32_t*>(take(L.max_segments));
-  uint16_t* bucketed = reinterpret_cast<uint16_t*>(take(L.outdeg_bucketed ? cdiv(E, 2) : 0));
-  int32_t* ohist = reinterpret_cast<int32_t*>(take(L.outdeg_bucketed ? L.outdeg_nb * L.edge_tiles : 0));
+  const bool bk = L.outdeg_bucketed;
+  uint16_t* bucketed = reinterpret_cast<uint16_t*>(take(bk ? cdiv(E, 2) : 0));
+  int32_t* oloc = reinterpret_cast<int32_t*>(take(bk ? (L.outdeg_nb + 1) * L.edge_tiles : 0));
   int32_t* opart = reinterpret_cast<int32_t*>(
-      take(L.outdeg_bucketed ? (int64_t)kOutdegSplit * L.outdeg_nb * kBucketSize : 0));
+      take(bk ? (int64_t)outdeg_split(L.outdeg_nb) * L.outdeg_nb * kOdBucket : 0));
 
   hipLaunchKernelGGL(k_zero, dim3(1), dim3(64), 0, st, p.counts, (int64_t)kCountSlots);
   if (Vs > 0 && !L.outdeg_bucketed)
@@ -728,15 +733,12 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
   if (L.outdeg_bucketed) {
     const int nb = (int)L.outdeg_nb;
     const int64_t et = L.edge_tiles;
-    hipLaunchKernelGGL(k_outdeg_hist, dim3(xcd_grid(et)), dim3(kThreads), (kThreads / 64) * nb * 4, st,
-                       p.col_idx, E, Vs, nb, ohist, et, p.counts);
-    scan(ArrF{ohist}, (int64_t)nb * et, nullptr, ohist, nullptr, tile_sums2, p.counts, st);
-    hipLaunchKernelGGL(k_outdeg_scatter, dim3(xcd_grid(et)), dim3(kThreads),
-                       3 * nb * 4 + 2 * kEdgeTile * 2, st, p.col_idx, E, nb, ohist, et, bucketed,
-                       p.counts);
-    hipLaunchKernelGGL(k_outdeg_count, dim3(kOutdegSplit, nb), dim3(1024), 0, st, bucketed, ohist,
-                       et, nb, E, Vs, opart, p.counts);
-    hipLaunchKernelGGL(k_outdeg_reduce, dim3(grid_for(Vs)), dim3(kThreads), 0, st, opart, nb, Vs,
+    const int S = outdeg_split(nb);
+    hipLaunchKernelGGL(k_outdeg_bin, dim3(xcd_grid(et)), dim3(kOdThreads), outdeg_bin_lds(nb), st,
+                       p.col_idx, E, Vs, nb, et, bucketed, oloc, p.counts);
+    hipLaunchKernelGGL(k_outdeg_count, dim3(nb, S), dim3(1024), 0, st, bucketed, oloc, et, nb, E,
+                       opart, p.counts);
+    hipLaunchKernelGGL(k_outdeg_reduce, dim3(grid_for(Vs)), dim3(kThreads), 0, st, opart, nb, S, Vs,
                        p.d_out, p.counts);
   }
   st = qst;  // the row order

@@ -55,6 +55,26 @@ def test_plan_many_tiles_and_ties():
     _compare(rp, col, V, 16, 256, 1)
 
 
+@pytest.mark.parametrize("nsrc", [(1 << 23) - 5, 1 << 23, (1 << 23) + 1],
+                         ids=["below", "at", "past"])
+def test_plan_source_count_limit(nsrc):
+    """The bucketed out-degree count takes up to 2^23 sources; past that the
+    degree kernel counts with atomics.  Both sides of the boundary, with the
+    first and last source ids, a hub source and a ragged last edge tile."""
+    rng = np.random.default_rng(11)
+    V = 3000
+    deg = rng.integers(0, 60, V)
+    deg[:3] = 7000
+    rp = np.concatenate([[0], np.cumsum(deg)]).astype(np.int64)
+    E = int(rp[-1])
+    col = rng.integers(0, nsrc, E)
+    col[:40] = nsrc - 1
+    col[40:80] = 0
+    col[rng.choice(E, 20000, replace=False)] = nsrc // 3
+    assert E % 16384 != 0
+    _compare(rp, col, nsrc, 512, 4096, 4)
+
+
 def test_plan_edge_cases():
     # no edges at all
     _compare(np.zeros(6, np.int64), np.zeros(0, np.int64), 5, 4, 8, 1)
