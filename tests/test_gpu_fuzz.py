@@ -169,6 +169,42 @@ def _small_graph(rng, vmax, dmax, long_row=0):
     return rp.astype(np.int32), col, V
 
 
+@pytest.mark.parametrize("case", range(40))
+def test_fuzz_out_degrees(case):
+    """The plan over graphs with many sources (log-uniform up to 2^23) and
+    up to ~2e5 edges: several edge tiles with a ragged last one, hub
+    sources, the first and last ids and ids on both sides of powers of
+    two; d_out (and the rest of the plan) bit-exact against the oracle."""
+    rng = np.random.default_rng(7000 + case)
+    Vs = int(np.exp(rng.uniform(0.0, np.log(1 << 23))))
+    V = int(rng.integers(1, 2000))
+    d = rng.integers(0, int(rng.choice([2, 30, 200])), V)
+    if rng.random() < 0.5:
+        d[int(rng.integers(0, V))] = int(rng.integers(1000, 60000))
+    rp = np.zeros(V + 1, np.int64)
+    np.cumsum(d, out=rp[1:])
+    E = int(rp[-1])
+    col = rng.integers(0, Vs, E)
+    if E:
+        marks = [0, Vs - 1] + [x for k in range(1, 24) for x in ((1 << k) - 1, 1 << k)
+                               if x < Vs]
+        col[rng.integers(0, E, min(E, 4 * len(marks)))] = rng.choice(marks, min(E, 4 * len(marks)))
+        hubs = rng.integers(0, Vs, int(rng.integers(1, 6)))
+        k = int(rng.integers(0, E // 2 + 1))
+        col[rng.integers(0, E, k)] = rng.choice(hubs, k)
+    T = int(rng.choice([4, 64, 512]))
+    c = int(rng.integers(1, 9))
+    print(f"fuzz out-degrees {case}: V={V} Vs={Vs} E={E} seg_len={T} row_cost={c}", flush=True)
+    g = graph(rp.astype(np.int32), col.astype(np.int32), num_src=Vs, seg_len=T,
+              block_cost=T + c + 100, row_cost=c)
+    got = {k: v.cpu().numpy().astype(np.int64) for k, v in g.arrays().items()}
+    want = O.plan(rp, col, Vs, T, T + c + 100, c)
+    for k in ("d_in", "d_out", "perm", "row_seg_first", "seg_row", "seg_beg", "seg_end",
+              "block_ptr"):
+        assert np.array_equal(got[k], want[k]), k
+    assert g.counts.error_flags == 0
+
+
 @pytest.mark.parametrize("case", range(60))
 def test_fuzz_attention(case):
     """Edge-softmax Gather over random graphs, head counts and widths."""
