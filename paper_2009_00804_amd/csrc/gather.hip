@@ -16,7 +16,7 @@
 //     are fetched as 128-bit loads, U rows in flight per lane;
 //   * a segment that is a whole row applies the epilogue and writes the
 //     output row; segments of split rows (d_in > seg_len) write float32
-//     partials, merged in segment order by k_combine (deterministic: no
+//     partials, merged in a fixed order by k_combine (deterministic: no
 //     floating-point atomics anywhere).
 #include <algorithm>
 #include <utility>
@@ -676,16 +676,54 @@ __global__ __launch_bounds__(kThreads) void k_gather_gated(GatherArgs a) {
 }
 
 // ------------------------------------------------------------------------
-// Split rows: merge the segment partials of each row in segment order.
-// Thread t handles column t % pc of every SPL-th segment; the SPL partial
-// results are then merged in order through LDS.
+// Split rows: merge the segment partials of each row.  The result does not
+// depend on timing: every merge follows a fixed order or a fixed tree.
+//  - Edge softmax: thread t handles column t % pc of every SPL-th segment;
+//    the SPL partial results are then merged in order through LDS.
+//  - Sum, mean and max, the first kCombineWgRows split rows (the longest:
+//    rows are in degree order): the workgroup deals the row's segments
+//    round-robin to groups of pc / 4 lanes, each lane holding four columns,
+//    and the groups' values are merged in group order through LDS.
+//  - Sum, mean and max, the other split rows: one wave per row, no barrier,
+//    so that many rows are in flight per CU; the lanes' values are merged by
+//    a fixed shuffle tree.
 // ------------------------------------------------------------------------
+constexpr int kCombineWgRows = 256;
+
+__device__ __forceinline__ void merge4(int red, float4& A, const float4& x) {
+  if (red == kMax) {
+    A.x = fmaxf(A.x, x.x); A.y = fmaxf(A.y, x.y);
+    A.z = fmaxf(A.z, x.z); A.w = fmaxf(A.w, x.w);
+  } else {
+    A.x += x.x; A.y += x.y; A.z += x.z; A.w += x.w;
+  }
+}
+
+// the merged value of one output column of a split row: reduction finish,
+// then the self term, bias and activation, stored
+template <typename T>
+__device__ __forceinline__ void combine_store(const GatherArgs& a, int row, int d, int c, float v) {
+  const int red = a.reduce;
+  if (red == kMax && d == 0) v = 0.0f;
+  if (red == kMean) v = d > 0 ? v / (float)d : 0.0f;
+  if (a.dst_norm) v *= rsqrt_deg(d);
+  if (a.self) v += load_elem<T>(a.self, (int64_t)row * a.ld_self + c);
+  if (a.bias) v += a.bias[c];
+  v = apply_act(a.act, v);
+  T* o = static_cast<T*>(a.out) + (int64_t)row * a.ld_out + c;
+  if constexpr (sizeof(T) == 4)
+    *o = v;
+  else
+    *o = f32_to_bf16(v);
+}
+
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_combine(GatherArgs a) {
   __shared__ float sm_acc[kThreads];
   __shared__ float sm_m[kThreads];
   __shared__ float sm_l[kThreads];
   __shared__ float fin[1024];
+  __shared__ float4 sm4[kThreads];
   const int32_t* __restrict__ counts = a.counts;
   if (counts[kErrFlags]) return;
   if (a.err2 && a.err2[0]) return;
@@ -698,112 +736,203 @@ __global__ __launch_bounds__(kThreads) void k_combine(GatherArgs a) {
   const int spl = pc >= kThreads ? 1 : kThreads / pc;
   const int t = threadIdx.x;
 
-  for (int i = blockIdx.x; i < n_split; i += gridDim.x) {
-    const int row = a.perm[i];
-    const int f0 = a.row_seg_first[i], f1 = a.row_seg_first[i + 1];
-    const int d = a.d_in[row];
-    for (int c0 = 0; c0 < pc; c0 += kThreads) {
-      int colc, sp;
-      bool on;
-      if (spl > 1) {
-        sp = t / pc;
-        colc = t % pc;
-        on = sp < spl;
-      } else {
-        sp = 0;
-        colc = c0 + t;
-        on = colc < pc;
-      }
-      float A = red == kMax ? -INFINITY : 0.0f, M = -INFINITY, L = 0.0f;
-      if (on) {
-        const int hd = (red == kSoftmax && colc < F) ? colc / D : 0;
-        // partial j merged into (A, M, L); the order of j is kept
-        auto merge = [&](float v, float mj, float lj) {
-          if (red == kMax) {
-            A = fmaxf(A, v);
-          } else if (red == kSoftmax) {
-            const float mn = fmaxf(M, mj);
-            const float fa = __expf(M - mn), fb = __expf(mj - mn);
-            A = A * fa + v * fb;
-            L = L * fa + lj * fb;
-            M = mn;
-          } else {
-            A += v;
-          }
-        };
-        // a hub row has hundreds of segments: UJ of its partials are read
-        // before any is merged, so their loads overlap
-        constexpr int UJ = 8;
-        int j = f0 + sp;
-        for (; j + (UJ - 1) * spl < f1; j += UJ * spl) {
-          float v[UJ], mj[UJ], lj[UJ];
-#pragma unroll
-          for (int u = 0; u < UJ; ++u) {
-            const float* p = a.partial + (int64_t)(j + u * spl) * a.pstride;
-            v[u] = p[colc];
-            mj[u] = red == kSoftmax ? p[pc + hd] : 0.0f;
-            lj[u] = red == kSoftmax ? p[pc + H + hd] : 0.0f;
-          }
-#pragma unroll
-          for (int u = 0; u < UJ; ++u) merge(v[u], mj[u], lj[u]);
-        }
-        for (; j < f1; j += spl) {
-          const float* p = a.partial + (int64_t)j * a.pstride;
-          merge(p[colc], red == kSoftmax ? p[pc + hd] : 0.0f, red == kSoftmax ? p[pc + H + hd] : 0.0f);
-        }
-      }
-      sm_acc[t] = A;
-      sm_m[t] = M;
-      sm_l[t] = L;
-      __syncthreads();
-      if (on && sp == 0) {
-        for (int q = 1; q < spl; ++q) {
-          const int o = q * pc + colc;
-          if (red == kMax) {
-            A = fmaxf(A, sm_acc[o]);
-          } else if (red == kSoftmax) {
-            const float mn = fmaxf(M, sm_m[o]);
-            const float fa = __expf(M - mn), fb = __expf(sm_m[o] - mn);
-            A = A * fa + sm_acc[o] * fb;
-            L = L * fa + sm_l[o] * fb;
-            M = mn;
-          } else {
-            A += sm_acc[o];
-          }
-        }
-        float v;
-        if (red == kSoftmax) {
-          v = L > 0.0f ? A / L : 0.0f;
+  if (red == kSoftmax) {
+    for (int i = blockIdx.x; i < n_split; i += gridDim.x) {
+      const int row = a.perm[i];
+      const int f0 = a.row_seg_first[i], f1 = a.row_seg_first[i + 1];
+      const int d = a.d_in[row];
+      for (int c0 = 0; c0 < pc; c0 += kThreads) {
+        int colc, sp;
+        bool on;
+        if (spl > 1) {
+          sp = t / pc;
+          colc = t % pc;
+          on = sp < spl;
         } else {
-          v = A;
-          if (red == kMax && d == 0) v = 0.0f;
-          if (red == kMean) v = d > 0 ? v / (float)d : 0.0f;
-          if (a.dst_norm) v *= rsqrt_deg(d);
+          sp = 0;
+          colc = c0 + t;
+          on = colc < pc;
         }
-        fin[colc] = v;
+        float A = red == kMax ? -INFINITY : 0.0f, M = -INFINITY, L = 0.0f;
+        if (on) {
+          const int hd = (red == kSoftmax && colc < F) ? colc / D : 0;
+          // partial j merged into (A, M, L); the order of j is kept
+          auto merge = [&](float v, float mj, float lj) {
+            if (red == kMax) {
+              A = fmaxf(A, v);
+            } else if (red == kSoftmax) {
+              const float mn = fmaxf(M, mj);
+              const float fa = __expf(M - mn), fb = __expf(mj - mn);
+              A = A * fa + v * fb;
+              L = L * fa + lj * fb;
+              M = mn;
+            } else {
+              A += v;
+            }
+          };
+          // a hub row has hundreds of segments: UJ of its partials are read
+          // before any is merged, so their loads overlap
+          constexpr int UJ = 8;
+          int j = f0 + sp;
+          for (; j + (UJ - 1) * spl < f1; j += UJ * spl) {
+            float v[UJ], mj[UJ], lj[UJ];
+  #pragma unroll
+            for (int u = 0; u < UJ; ++u) {
+              const float* p = a.partial + (int64_t)(j + u * spl) * a.pstride;
+              v[u] = p[colc];
+              mj[u] = red == kSoftmax ? p[pc + hd] : 0.0f;
+              lj[u] = red == kSoftmax ? p[pc + H + hd] : 0.0f;
+            }
+  #pragma unroll
+            for (int u = 0; u < UJ; ++u) merge(v[u], mj[u], lj[u]);
+          }
+          for (; j < f1; j += spl) {
+            const float* p = a.partial + (int64_t)j * a.pstride;
+            merge(p[colc], red == kSoftmax ? p[pc + hd] : 0.0f, red == kSoftmax ? p[pc + H + hd] : 0.0f);
+          }
+        }
+        sm_acc[t] = A;
+        sm_m[t] = M;
+        sm_l[t] = L;
+        __syncthreads();
+        if (on && sp == 0) {
+          for (int q = 1; q < spl; ++q) {
+            const int o = q * pc + colc;
+            if (red == kMax) {
+              A = fmaxf(A, sm_acc[o]);
+            } else if (red == kSoftmax) {
+              const float mn = fmaxf(M, sm_m[o]);
+              const float fa = __expf(M - mn), fb = __expf(sm_m[o] - mn);
+              A = A * fa + sm_acc[o] * fb;
+              L = L * fa + sm_l[o] * fb;
+              M = mn;
+            } else {
+              A += sm_acc[o];
+            }
+          }
+          float v;
+          if (red == kSoftmax) {
+            v = L > 0.0f ? A / L : 0.0f;
+          } else {
+            v = A;
+            if (red == kMax && d == 0) v = 0.0f;
+            if (red == kMean) v = d > 0 ? v / (float)d : 0.0f;
+            if (a.dst_norm) v *= rsqrt_deg(d);
+          }
+          fin[colc] = v;
+        }
+        __syncthreads();
+      }
+      // epilogue over output columns
+      for (int c = t; c < a.out_cols; c += kThreads) {
+        float v;
+        if (a.head_mean) {
+          v = 0.0f;
+          for (int k = 0; k < H; ++k) v += fin[k * D + c];
+          v *= 1.0f / (float)H;
+        } else {
+          v = fin[c];
+        }
+        if (a.self) v += load_elem<T>(a.self, (int64_t)row * a.ld_self + c);
+        if (a.bias) v += a.bias[c];
+        v = apply_act(a.act, v);
+        T* o = static_cast<T*>(a.out) + (int64_t)row * a.ld_out + c;
+        if constexpr (sizeof(T) == 4)
+          *o = v;
+        else
+          *o = f32_to_bf16(v);
       }
       __syncthreads();
     }
-    // epilogue over output columns
-    for (int c = t; c < a.out_cols; c += kThreads) {
-      float v;
-      if (red == kSoftmax && a.head_mean) {
-        v = 0.0f;
-        for (int k = 0; k < H; ++k) v += fin[k * D + c];
-        v *= 1.0f / (float)H;
-      } else {
-        v = fin[c];
+    return;
+  }
+
+  // sum, mean, max; a partial row is vpr 16-byte vectors
+  const int vpr = pc / 4;
+  const float init = red == kMax ? -INFINITY : 0.0f;
+  constexpr int UJ = 8;  // partials read before any is merged, so that loads overlap
+  const int nwg = n_split < kCombineWgRows ? n_split : kCombineWgRows;
+  {  // the longest rows: a whole workgroup each
+    const int ng = kThreads / vpr;
+    const int vg = t / vpr, vv = t % vpr;
+    for (int i = blockIdx.x; i < nwg; i += gridDim.x) {
+      const int row = a.perm[i];
+      const int f0 = a.row_seg_first[i], f1 = a.row_seg_first[i + 1];
+      const int d = a.d_in[row];
+      float4 A = make_float4(init, init, init, init);
+      if (vg < ng) {
+        int j = f0 + vg;
+        for (; j + (UJ - 1) * ng < f1; j += UJ * ng) {
+          float4 x[UJ];
+#pragma unroll
+          for (int u = 0; u < UJ; ++u)
+            x[u] = *reinterpret_cast<const float4*>(a.partial + (int64_t)(j + u * ng) * a.pstride +
+                                                    4 * vv);
+#pragma unroll
+          for (int u = 0; u < UJ; ++u) merge4(red, A, x[u]);
+        }
+        for (; j < f1; j += ng)
+          merge4(red, A, *reinterpret_cast<const float4*>(a.partial + (int64_t)j * a.pstride + 4 * vv));
       }
-      if (a.self) v += load_elem<T>(a.self, (int64_t)row * a.ld_self + c);
-      if (a.bias) v += a.bias[c];
-      v = apply_act(a.act, v);
-      T* o = static_cast<T*>(a.out) + (int64_t)row * a.ld_out + c;
-      if constexpr (sizeof(T) == 4)
-        *o = v;
-      else
-        *o = f32_to_bf16(v);
+      sm4[t] = A;
+      __syncthreads();
+      if (vg == 0) {
+        for (int q = 1; q < ng; ++q) merge4(red, A, sm4[q * vpr + vv]);
+        const float r[4] = {A.x, A.y, A.z, A.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (4 * vv + k < a.out_cols) combine_store<T>(a, row, d, 4 * vv + k, r[k]);
+      }
+      __syncthreads();
     }
-    __syncthreads();
+  }
+  {  // the other rows: one wave each.  With vpr < 64 a wave instruction
+     // covers spw segments (lane = sub * vpr + vector); otherwise the
+     // vectors are taken 64 at a time.
+    const int lane = t & 63;
+    const int spw = vpr >= 64 ? 1 : 64 / vpr;
+    const int sub = vpr >= 64 ? 0 : lane / vpr;
+    const int waves = kThreads / 64;
+    for (int i = nwg + blockIdx.x * waves + (t >> 6); i < n_split; i += gridDim.x * waves) {
+      const int row = a.perm[i];
+      const int f0 = a.row_seg_first[i], f1 = a.row_seg_first[i + 1];
+      const int d = a.d_in[row];
+      for (int v0 = 0; v0 < vpr; v0 += 64) {
+        const int vv = vpr >= 64 ? v0 + lane : lane % vpr;
+        const bool on = sub < spw && vv < vpr;
+        float4 A = make_float4(init, init, init, init);
+        if (on) {
+          int j = f0 + sub;
+          for (; j + (UJ - 1) * spw < f1; j += UJ * spw) {
+            float4 x[UJ];
+#pragma unroll
+            for (int u = 0; u < UJ; ++u)
+              x[u] = *reinterpret_cast<const float4*>(a.partial +
+                                                      (int64_t)(j + u * spw) * a.pstride + 4 * vv);
+#pragma unroll
+            for (int u = 0; u < UJ; ++u) merge4(red, A, x[u]);
+          }
+          for (; j < f1; j += spw)
+            merge4(red, A, *reinterpret_cast<const float4*>(a.partial + (int64_t)j * a.pstride + 4 * vv));
+        }
+        // tree over the subs: at step s, sub k (k % 2s == 0) takes sub k + s
+        for (int s = 1; s < spw; s <<= 1) {
+          const int src = lane + s * vpr;
+          float4 y;
+          y.x = __shfl(A.x, src < 64 ? src : lane, 64);
+          y.y = __shfl(A.y, src < 64 ? src : lane, 64);
+          y.z = __shfl(A.z, src < 64 ? src : lane, 64);
+          y.w = __shfl(A.w, src < 64 ? src : lane, 64);
+          if (sub % (2 * s) == 0 && sub + s < spw) merge4(red, A, y);
+        }
+        if (on && sub == 0) {
+          const float r[4] = {A.x, A.y, A.z, A.w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (4 * vv + k < a.out_cols) combine_store<T>(a, row, d, 4 * vv + k, r[k]);
+        }
+      }
+    }
   }
 }
 
