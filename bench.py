@@ -999,7 +999,7 @@ def main():
     dom = max(stages, key=lambda n: r["mean"][n])
     byts, flops = algorithmic(step, dom)
     dur = r["mean"][dom] * 1e-3
-    kernel_name = {"gather1": "k_gather_sum", "gather2": "k_gather_sum + k_gather_simple",
+    kernel_name = {"gather1": "k_gather_sum", "gather2": "k_gather_sum",
                    "gemm1": "k_gemm_bres" if args.dtype == "bf16" else "k_gemm",
                    "gemm2": "k_gemm"}[dom]
     if dom.startswith("gemm") and args.dtype == "f32":

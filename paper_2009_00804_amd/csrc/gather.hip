@@ -261,10 +261,12 @@ __global__ __launch_bounds__(kThreads) void k_gather_simple(GatherArgs a, int ns
 // with four row loads in flight per lane (56 registers float32, 64
 // bfloat16).  Measured on the 2^21 graph, 128 bfloat16 columns: 2.38 ms,
 // against 2.47 with eight loads in flight at seven waves.
-template <typename T, int LPR, int VPL, int U, int CPL>
+// FL: whole slices (else the last slice's lanes past the row are idle, as
+// for 41 bfloat16 columns or the 9-column float32 tail).
+template <typename T, int LPR, int VPL, int U, int CPL, bool FL = true>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(8))) void k_gather_sum(
     GatherArgs a, int nslices, int slice0) {
-  gather_simple_body<T, LPR, VPL, U, CPL, false, kWNone, true, false, true>(a, nslices, slice0);
+  gather_simple_body<T, LPR, VPL, U, CPL, false, kWNone, FL, false, true>(a, nslices, slice0);
 }
 
 // ------------------------------------------------------------------------
@@ -1034,12 +1036,17 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
       else SAGA_LAUNCH_FULL(true, kWNone);
     } else if (srcnorm) {
       SAGA_LAUNCH_FULL(false, kWSrcNorm);
-    } else if (LPR <= 8 && full && o32) {
-      // (whole slices of at most 128 bytes: wider lane groups never take
-      // this path with 128-byte slices, and are not built)
-      if constexpr (LPR <= 8)
-        hipLaunchKernelGGL((k_gather_sum<T, LPR, VPL, US, CPL>), grid, dim3(kThreads), 0, st, a,
-                           conc, s0);
+    } else if (LPR <= 8 && o32) {
+      // (slices of at most 128 bytes: wider lane groups never take this
+      // path with 128-byte slices, and are not built)
+      if constexpr (LPR <= 8) {
+        if (full)
+          hipLaunchKernelGGL((k_gather_sum<T, LPR, VPL, US, CPL, true>), grid, dim3(kThreads), 0, st,
+                             a, conc, s0);
+        else
+          hipLaunchKernelGGL((k_gather_sum<T, LPR, VPL, US, CPL, false>), grid, dim3(kThreads), 0,
+                             st, a, conc, s0);
+      }
     } else {
       SAGA_LAUNCH_FULL(false, kWNone);
     }

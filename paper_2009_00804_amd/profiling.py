@@ -58,15 +58,15 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 # whole-line columns and the 9-column rest; each Gather with split rows ends
 # with a combine.
 STAGES = {
-    "gather1": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4>", 4, 5, (0, 1, 2, 3)),
+    "gather1": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4, true>", 4, 5, (0, 1, 2, 3)),
                          ("k_combine<float>", 1, 3, (0,))],
-                 "bf16": [("k_gather_sum<unsigned short, 8, 1, 4, 4>", 2, 2, (0, 1)),
+                 "bf16": [("k_gather_sum<unsigned short, 8, 1, 4, 4, true>", 2, 2, (0, 1)),
                           ("k_combine<unsigned short>", 1, 2, (0,))]},
                 "gather.hip"),
-    "gather2": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4>", 1, 5, (4,)),
-                         ("k_gather_simple<float, 4, 1, 4, 8, false, 0, false", 1, 1, (0,)),
+    "gather2": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4, true>", 1, 5, (4,)),
+                         ("k_gather_sum<float, 4, 1, 4, 8, false>", 1, 1, (0,)),
                          ("k_combine<float>", 2, 3, (1, 2))],
-                 "bf16": [("k_gather_simple<unsigned short, 8, 1, 8, 4, false, 0, false", 1, 1, (0,)),
+                 "bf16": [("k_gather_sum<unsigned short, 8, 1, 4, 4, false>", 1, 1, (0,)),
                           ("k_combine<unsigned short>", 1, 2, (1,))]},
                 "gather.hip"),
     "gemm1": ({"f32": [("k_gemm<float, 2, 8,", 1, 1, (0,))],

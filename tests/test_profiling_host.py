@@ -36,7 +36,7 @@ def test_counter_summary_sums_a_stages_dispatches_by_slot(tmp_path):
     figures come from the per-launch sums."""
     import csv
     import types
-    names = (["k_gather_sum<float, 8, 1, 4, 4>(saga::GatherArgs, int, int)"] * 5
+    names = (["k_gather_sum<float, 8, 1, 4, 4, true>(saga::GatherArgs, int, int)"] * 5
              + ["k_combine<float>(saga::GatherArgs)"] * 3)
     rows, did = [], 0
     for _ in range(2):
