@@ -224,8 +224,9 @@ saga_status saga_plan_build(int32_t num_dst, int32_t num_src, int64_t num_edges,
  * `stream`, the caller makes `stream` wait for join_event
  * (hipStreamWaitEvent).  fork_event and join_event are caller-created
  * hipEvent_t; order_stream must differ from `stream`; keep both streams at
- * the same priority.  Graphs small enough that the out-degrees are counted
- * in one pass run entirely on `stream` (join_event is then recorded there).
+ * the same priority.  Graphs whose out-degrees the degree kernel counts
+ * with atomics in the same pass (no edges, or more than 2^23 source
+ * vertices) run entirely on `stream` (join_event is then recorded there).
  * The arrays are the same, bit for bit, as saga_plan_build's.  Errors as
  * saga_plan_build, and SAGA_EINVAL if a stream or event is missing. */
 saga_status saga_plan_build_split(int32_t num_dst, int32_t num_src, int64_t num_edges,
