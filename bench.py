@@ -160,6 +160,7 @@ class Step:
         # stage pipelining: the plan's row-order branch on a second stream
         # (default priority) while the d_out-scaled transform runs here
         self.split = False
+        self.join_early = False
         self.side = torch.cuda.Stream()
         self.side_sh = S.stream_handle(self.side)
         self.fork, self.join = torch.cuda.Event(), torch.cuda.Event()
@@ -208,10 +209,14 @@ class Step:
         if ev:
             ev[1].record(self.stream)
         p = g.plan
+        if self.split and self.join_early:
+            # both plan branches finish before the transform, which then has
+            # the CUs to itself
+            self.stream.wait_event(self.join)
         S.saga_apply_vertex(self.gop, S.cmat(self.X), S.cmat(self.W1), self.none, self.none, None,
                             None, S.mat(self.Z1), C.c_void_p(self.mws.data_ptr()), self.mws.numel(),
                             self.sh)
-        if self.split:
+        if self.split and not self.join_early:
             self.stream.wait_event(self.join)
         if ev:
             ev[2].record(self.stream)
@@ -900,6 +905,11 @@ def main():
                     help="skip the per-layer timing of the six smaller workloads")
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip the fused-vs-unfused layer-1 aggregation comparison")
+    ap.add_argument("--plan-join", choices=["gather", "transform"], default="gather",
+                    help="with the pipelined plan, where the step waits for the plan's row-order "
+                         "branch: before the first Gather (it overlaps the first transform) or "
+                         "before the first transform (it overlaps the out-degree count only); "
+                         "both are measured and reported")
     ap.add_argument("--pipeline", choices=["on", "off"], default="on",
                     help="time the step with the plan's row-order branch on a second stream, "
                          "overlapping the first transform (on), or stage by stage (off); both "
@@ -965,6 +975,15 @@ def main():
         step.split = True
         wall_p, _, _ = time_step(step, args.steps, args.warmup)
         ms_pipe = wall_p * 1e3 / args.steps
+        # the plan's two branches joined before the transform instead
+        step.join_early = True
+        wall_j, _, _ = time_step(step, args.steps, args.warmup)
+        ms_pipe_early = wall_j * 1e3 / args.steps
+        step.join_early = args.plan_join == "transform"
+        if step.join_early:
+            ms_pipe_late, ms_pipe = ms_pipe, ms_pipe_early
+        else:
+            ms_pipe_late = ms_pipe
         # and with layer 2's transform fused into layer 1's Gather
         step.fused = True
         wall_f, per_f, _ = time_step(step, args.steps, args.warmup)
@@ -975,7 +994,8 @@ def main():
         ms = ms_fused if step.fused else (ms_pipe if step.split else ms_seq)
         results[dt] = dict(step=step, ms=ms, med=med, mean=mean, spread=stage_spread, counts=counts,
                            ev_ms=statistics.median(tot), ms_seq=ms_seq, ms_pipe=ms_pipe,
-                           ms_fused=ms_fused, fused_gather1=fused_gather1)
+                           ms_fused=ms_fused, fused_gather1=fused_gather1,
+                           ms_pipe_early=ms_pipe_early, ms_pipe_late=ms_pipe_late)
         log(f"{dt}: {ms_seq:.3f} ms/step stage by stage (events {statistics.median(tot):.3f}); "
             + ", ".join(f"{n} {med[n]:.3f}" for n in step.names)
             + f"; {ms_pipe:.3f} ms/step with the plan's row order overlapping gemm1"
@@ -1052,7 +1072,9 @@ def main():
         "what": "plan's row-order branch (in-degrees, validation, degree sort, segments, "
                 "blocks) on a second stream, overlapping the d_out-scaled layer-1 transform",
         "stage_by_stage_ms": r["ms_seq"], "pipelined_ms": r["ms_pipe"],
-        "speedup": r["ms_seq"] / r["ms_pipe"], "value_uses": args.pipeline}
+        "speedup": r["ms_seq"] / r["ms_pipe"], "value_uses": args.pipeline,
+        "joined_before_gather_ms": r["ms_pipe_late"],
+        "joined_before_transform_ms": r["ms_pipe_early"], "join": args.plan_join}
     out["cross_stage_fusion"] = {
         "what": "layer 2's transform (d_out^-1/2 (h1 W2)) done inside layer 1's last Gather "
                 "pass, each wave multiplying the rows it has just finished on the matrix cores "
@@ -1072,6 +1094,8 @@ def main():
         out.setdefault("variants", {})[dt] = {
             "value": 2 * E / (rr["ms"] * 1e-3), "ms_per_step": rr["ms"],
             "stage_by_stage_ms": rr["ms_seq"], "pipelined_ms": rr["ms_pipe"],
+            "joined_before_gather_ms": rr["ms_pipe_late"],
+            "joined_before_transform_ms": rr["ms_pipe_early"],
             "fused_ms": rr["ms_fused"], "fused_stage_ms": rr["fused_gather1"],
             "stage_ms": {n: round(rr["mean"][n], 4) for n in rr["mean"]},
             "stage_ms_spread": rr["spread"],
