@@ -269,6 +269,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(8))) v
   gather_simple_body<T, LPR, VPL, U, CPL, false, kWNone, FL, false, true>(a, nslices, slice0);
 }
 
+// The plain max over slices of a source below 4 GiB (the GraphSAGE-pool
+// Gather), built like k_gather_sum.
+template <typename T, int LPR, int VPL, int U, int CPL, bool FL>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(8))) void k_gather_max(
+    GatherArgs a, int nslices, int slice0) {
+  gather_simple_body<T, LPR, VPL, U, CPL, true, kWNone, FL, false, true>(a, nslices, slice0);
+}
+
 // ------------------------------------------------------------------------
 // The next layer's transform fused into this Gather (cross-stage
 // pipelining, Sec. 4): y[v] = xrs(v) * (h_v W) for W F x xn (xn <= 64),
@@ -1032,8 +1040,20 @@ hipError_t launch_simple_lpr(const GatherArgs& a, unsigned blocks, int nslices, 
     } else if (a.msg == SAGA_MSG_TYPED) {
       SAGA_LAUNCH_FULL(false, kWEdge);
     } else if (a.reduce == kMax) {
-      if (srcnorm) SAGA_LAUNCH_FULL(true, kWSrcNorm);
-      else SAGA_LAUNCH_FULL(true, kWNone);
+      if (srcnorm) {
+        SAGA_LAUNCH_FULL(true, kWSrcNorm);
+      } else if (LPR <= 8 && o32) {
+        if constexpr (LPR <= 8) {
+          if (full)
+            hipLaunchKernelGGL((k_gather_max<T, LPR, VPL, US, CPL, true>), grid, dim3(kThreads), 0,
+                               st, a, conc, s0);
+          else
+            hipLaunchKernelGGL((k_gather_max<T, LPR, VPL, US, CPL, false>), grid, dim3(kThreads), 0,
+                               st, a, conc, s0);
+        }
+      } else {
+        SAGA_LAUNCH_FULL(true, kWNone);
+      }
     } else if (srcnorm) {
       SAGA_LAUNCH_FULL(false, kWSrcNorm);
     } else if (LPR <= 8 && o32) {
