@@ -58,6 +58,11 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 # whole-line columns and the 9-column rest; each Gather with split rows ends
 # with a combine.
 STAGES = {
+    # the plan's out-degree count (tile sort by bucket, per-bucket count,
+    # partial sums), once per step
+    "outdeg": ({dt: [("k_outdeg_bin", 1, 1, (0,)), ("k_outdeg_count", 1, 1, (0,)),
+                     ("k_outdeg_reduce", 1, 1, (0,))] for dt in ("f32", "bf16")},
+               "plan.hip"),
     "gather1": ({"f32": [("k_gather_sum<float, 8, 1, 4, 4, true>", 4, 5, (0, 1, 2, 3)),
                          ("k_combine<float>", 1, 3, (0,))],
                  "bf16": [("k_gather_sum<unsigned short, 8, 1, 4, 4, true>", 2, 2, (0, 1)),
