@@ -314,7 +314,14 @@ __global__ __launch_bounds__(1024) void k_outdeg_count(const uint16_t* __restric
   if (counts[kErrFlags]) return;
   __shared__ int32_t h[kOdBucket];
   constexpr int R = kOdRuns, J = kOdLoads, NW = 1024 / 64;
-  const int b = blockIdx.x, s = blockIdx.y, S = gridDim.y;
+  // buckets in an XCD-blocked order (gridDim.x = xcd_grid(nb)): XCD x takes
+  // the contiguous buckets [x * per, (x + 1) * per), so that neighbouring
+  // buckets, whose runs share the 128-byte lines where they meet, read them
+  // through one L2
+  const int per = (int)((nb + kXcds - 1) / kXcds);
+  const int b = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
+  const int s = blockIdx.y, S = gridDim.y;
+  if (b >= nb) return;
   for (int i = threadIdx.x; i < kOdBucket; i += 1024) h[i] = 0;
   __syncthreads();
   const int64_t t0 = ntiles * s / S, t1 = ntiles * (s + 1) / S;
@@ -736,8 +743,8 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
     const int S = outdeg_split(nb);
     hipLaunchKernelGGL(k_outdeg_bin, dim3(xcd_grid(et)), dim3(kOdThreads), outdeg_bin_lds(nb), st,
                        p.col_idx, E, Vs, nb, et, bucketed, oloc, p.counts);
-    hipLaunchKernelGGL(k_outdeg_count, dim3(nb, S), dim3(1024), 0, st, bucketed, oloc, et, nb, E,
-                       opart, p.counts);
+    hipLaunchKernelGGL(k_outdeg_count, dim3(xcd_grid(nb), S), dim3(1024), 0, st, bucketed, oloc, et,
+                       nb, E, opart, p.counts);
     hipLaunchKernelGGL(k_outdeg_reduce, dim3(grid_for(Vs)), dim3(kThreads), 0, st, opart, nb, S, Vs,
                        p.d_out, p.counts);
   }
