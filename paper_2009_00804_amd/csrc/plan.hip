@@ -369,15 +369,28 @@ __global__ __launch_bounds__(1024) void k_outdeg_count(const uint16_t* __restric
   for (int i = threadIdx.x; i < kOdBucket; i += 1024) pw[i] = h[i];
 }
 
-// d_out[v] = the sum of the S partial counts
+// d_out[v] = the sum of the S partial counts, four sources per thread as
+// 16-byte loads (part and d_out are 256-byte aligned, stride a multiple of 4)
 __global__ __launch_bounds__(kThreads) void k_outdeg_reduce(const int32_t* __restrict__ part,
                                                             int nb, int S, int32_t Vs,
                                                             int32_t* __restrict__ d_out,
                                                             const int32_t* counts) {
   if (counts[kErrFlags]) return;
   const int64_t stride = (int64_t)nb * kOdBucket;
-  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < Vs;
-       v += (int64_t)gridDim.x * blockDim.x) {
+  const int64_t n4 = Vs / 4;
+  const int64_t g0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x, gs = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = g0; i < n4; i += gs) {
+    int4 sum = make_int4(0, 0, 0, 0);
+    for (int w = 0; w < S; ++w) {
+      const int4 x = reinterpret_cast<const int4*>(part + w * stride)[i];
+      sum.x += x.x;
+      sum.y += x.y;
+      sum.z += x.z;
+      sum.w += x.w;
+    }
+    reinterpret_cast<int4*>(d_out)[i] = sum;
+  }
+  for (int64_t v = 4 * n4 + g0; v < Vs; v += gs) {
     int32_t sum = 0;
     for (int w = 0; w < S; ++w) sum += part[w * stride + v];
     d_out[v] = sum;
@@ -745,8 +758,8 @@ hipError_t launch_plan_build(const saga_plan& p, const PlanLayout& L, hipStream_
                        p.col_idx, E, Vs, nb, et, bucketed, oloc, p.counts);
     hipLaunchKernelGGL(k_outdeg_count, dim3(xcd_grid(nb), S), dim3(1024), 0, st, bucketed, oloc, et,
                        nb, E, opart, p.counts);
-    hipLaunchKernelGGL(k_outdeg_reduce, dim3(grid_for(Vs)), dim3(kThreads), 0, st, opart, nb, S, Vs,
-                       p.d_out, p.counts);
+    hipLaunchKernelGGL(k_outdeg_reduce, dim3(grid_for((Vs + 3) / 4)), dim3(kThreads), 0, st, opart, nb,
+                       S, Vs, p.d_out, p.counts);
   }
   st = qst;  // the row order
 
